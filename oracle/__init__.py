@@ -1,0 +1,118 @@
+"""The oracle: a plain double-precision CPU implementation of the OPD loss.
+
+Test infrastructure.  Only tests/, ``__graft_entry__.smoke()`` and the
+benchmark's CPU-baseline leg may import this package.  It shares no code with
+the GPU library (``paper_2606_24143_amd``) and never imports it.
+
+The arithmetic lives in ``opd_oracle.c`` (one function per estimator, each
+citing the passage of the paper it follows); this module only marshals numpy
+arrays into it.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "opd_oracle.c")
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+
+ESTIMATORS = {"fkl_topk": 0, "rkl_topk": 1, "rkl_mc1": 2, "rkl_mc": 3, "fkl_dense": 4,
+              "rkl_dense": 5}
+DENSE = ("fkl_dense", "rkl_dense")
+MC = ("rkl_mc1", "rkl_mc")
+F32, BF16 = 0, 1
+
+
+def build(force: bool = False) -> str:
+    """Compile liboracle.so in place with gcc."""
+    if force or not os.path.exists(_LIB_PATH):
+        tmp = _LIB_PATH + ".tmp%d" % os.getpid()
+        subprocess.run(["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-Wall", "-Wextra", "-o", tmp,
+                        _SRC, "-lm"], check=True)
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        build()
+        L = ctypes.CDLL(_LIB_PATH)
+        P = ctypes.c_void_p
+        i64 = ctypes.c_int64
+        L.oracle_row.argtypes = [ctypes.c_int, P, P, i64, P, P, P, ctypes.c_int, ctypes.c_double,
+                                 ctypes.c_int, P, P, P, P]
+        L.oracle_row.restype = ctypes.c_int
+        L.oracle_rows.argtypes = [ctypes.c_int, ctypes.c_int, P, P, i64, i64, i64, P, P, P,
+                                  ctypes.c_int, P, ctypes.c_double, P, P, P, P, ctypes.c_int]
+        L.oracle_rows.restype = ctypes.c_int
+        L.oracle_max_threads.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _p(a):
+    return None if a is None else ctypes.c_void_p(a.ctypes.data)
+
+
+def row(est: str, z, ids=None, tau=None, beta=None, y=None, gamma: float = 1.0,
+        valid: bool = True, want_grad: bool = True):
+    """One token row in double.  Returns (loss, grad or None, lse, gathered or None)."""
+    z = np.ascontiguousarray(z, np.float64)
+    V = z.size
+    dense = est in DENSE
+    y = None if y is None else np.ascontiguousarray(y, np.float64)
+    if not dense:
+        ids = np.ascontiguousarray(ids, np.int32)
+        tau = np.ascontiguousarray(tau, np.float64)
+        beta = None if beta is None else np.ascontiguousarray(beta, np.float64)
+        K = ids.size
+    else:
+        K = 0
+    loss = np.zeros(1, np.float64)
+    lse = np.zeros(1, np.float64)
+    grad = np.zeros(V, np.float64) if want_grad else None
+    gathered = np.zeros(K, np.float64) if K else None
+    rc = lib().oracle_row(ESTIMATORS[est], _p(z), _p(y), V, _p(ids), _p(tau), _p(beta), K, gamma,
+                          int(valid), _p(loss), _p(grad), _p(lse), _p(gathered))
+    if rc != 0:
+        raise ValueError("oracle_row rejected its arguments (%d)" % rc)
+    return float(loss[0]), grad, float(lse[0]), gathered
+
+
+def rows(est: str, dtype: int, logits: np.ndarray, V: int, *, ids=None, tau=None, beta=None,
+         teacher_logits=None, mask=None, gamma: float = 1.0, want_grad: bool = True,
+         nthreads: int = 0) -> dict:
+    """Rows of stored inputs: logits [n, ld] (uint16 bf16 bits or float32)."""
+    logits = np.ascontiguousarray(logits)
+    n, ld = logits.shape
+    dense = est in DENSE
+    K = 0 if dense else ids.shape[1]
+    if not dense:
+        ids = np.ascontiguousarray(ids, np.int32)
+        tau = np.ascontiguousarray(tau, np.float32)
+        beta = None if beta is None else np.ascontiguousarray(beta, np.float32)
+    if teacher_logits is not None:
+        teacher_logits = np.ascontiguousarray(teacher_logits)
+    mask = None if mask is None else np.ascontiguousarray(mask, np.uint8)
+    out = {"loss": np.zeros(n, np.float64), "lse": np.zeros(n, np.float64)}
+    out["grad"] = np.zeros((n, V), np.float64) if want_grad else None
+    out["gathered"] = np.zeros((n, K), np.float64) if K else None
+    rc = lib().oracle_rows(ESTIMATORS[est], dtype, _p(logits), _p(teacher_logits), n, V, ld,
+                           _p(ids), _p(tau), _p(beta), K, _p(mask), gamma, _p(out["loss"]),
+                           _p(out["grad"]), _p(out["lse"]), _p(out["gathered"]), nthreads)
+    if rc != 0:
+        raise ValueError("oracle_rows rejected its arguments (%d)" % rc)
+    return out
+
+
+def max_threads() -> int:
+    return int(lib().oracle_max_threads())

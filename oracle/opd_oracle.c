@@ -1,0 +1,242 @@
+/*
+ * The oracle for the learner-time OPD loss: a plain double-precision CPU
+ * implementation, written from the paper's definitions, for testing only.
+ * Nothing here is blocked, fused or reordered beyond what the definitions
+ * state, so each function can be checked against the paper by eye.
+ *
+ * Test infrastructure: only tests/, the smoke check and the benchmark's
+ * CPU-baseline leg may load or call this code.  It shares no code with the
+ * GPU library.
+ *
+ * Notation (Sec. 3): at a fixed prefix s, p_theta = softmax(z) is the current
+ * student, q the teacher, p_old the stale behaviour policy.  The cache holds,
+ * per token, either a support S = {a_i} with teacher log-probs
+ * tau_i = log q(a_i|s), or M behaviour samples a_i ~ p_old with
+ * tau_i = log q(a_i|s) and beta_i = log p_old(a_i|s).
+ */
+#include "opd_oracle.h"
+
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+/* log sum_j exp(x_j): the log-partition of a logit row, two sweeps. */
+static double log_partition(const double* x, int64_t V) {
+  double m = x[0];
+  for (int64_t j = 1; j < V; ++j)
+    if (x[j] > m) m = x[j];
+  double s = 0.0;
+  for (int64_t j = 0; j < V; ++j) s += exp(x[j] - m);
+  return m + log(s);
+}
+
+/*
+ * Sparse top-k KL on a cached support S, both distributions renormalised on S
+ * (Sec. 3, "Sparse and sampled implementations"; App. A.1):
+ *   Z_p^S = sum_{u in S} p_theta(u|s),   Z_q^S = sum_{u in S} q(u|s),
+ *   p~(a) = p_theta(a|s) / Z_p^S,        q~(a) = q(a|s) / Z_q^S   (a in S).
+ * Forward:  KL(q~ || p~) = sum_S q~ (log q~ - log p~);
+ *           d/dz_{a_i} = p~_i - q~_i, zero off S.
+ * Reverse:  D_R^S = KL(p~ || q~) = -sum_S p~ (log q~ - log p~);
+ *           d/dz_{a_i} = p~_i ((log p~_i - log q~_i) - D_R^S), zero off S.
+ * The support is held fixed during the update (App. A.1).
+ */
+static void topk_kl(int reverse, const double* z, int64_t V, double L, const int32_t* ids,
+                    const double* tau, int K, double gamma, double* loss, double* grad) {
+  double Zp = 0.0, Zq = 0.0;
+  for (int i = 0; i < K; ++i) {
+    Zp += exp(z[ids[i]] - L); /* p_theta(a_i|s) */
+    Zq += exp(tau[i]);        /* q(a_i|s) */
+  }
+  const double logZp = log(Zp), logZq = log(Zq);
+  double kl = 0.0;
+  for (int i = 0; i < K; ++i) {
+    const double log_pt = (z[ids[i]] - L) - logZp; /* log p~(a_i) */
+    const double log_qt = tau[i] - logZq;          /* log q~(a_i) */
+    if (reverse)
+      kl += exp(log_pt) * (log_pt - log_qt);
+    else
+      kl += exp(log_qt) * (log_qt - log_pt);
+  }
+  *loss = kl;
+  if (!grad) return;
+  for (int64_t j = 0; j < V; ++j) grad[j] = 0.0;
+  for (int i = 0; i < K; ++i) {
+    const double log_pt = (z[ids[i]] - L) - logZp;
+    const double log_qt = tau[i] - logZq;
+    const double pt = exp(log_pt), qt = exp(log_qt);
+    grad[ids[i]] += reverse ? gamma * pt * ((log_pt - log_qt) - kl) : gamma * (pt - qt);
+  }
+}
+
+/*
+ * Monte-Carlo reverse KL with old-to-current importance sampling and the
+ * advantage recomputed under the current student, no clipping
+ * (Sec. 5.1, L_theta^noclip; Sec. 6.2 and App. E for m samples):
+ *   A_theta(a) = log q(a|s) - log p_theta(a|s)        (stop-gradient)
+ *   rho(a)     = p_theta(a|s) / p_old(a|s)
+ *   L_m        = -(1/m) sum_i rho(a_i) sg(A_theta(a_i)).
+ * Samples are iid with replacement, so ids may repeat; each occurrence is a
+ * separate term.  With A held fixed, d rho_i / d z_j = rho_i (1[j = a_i] - p_j),
+ * so  dL_m/dz_j = c p_j - (1/m) sum_{i: a_i = j} rho_i A_i,
+ * with c = (1/m) sum_i rho_i A_i = -L_m.
+ */
+static void mc_rkl(const double* z, int64_t V, double L, const int32_t* ids, const double* tau,
+                   const double* beta, int M, double gamma, double* loss, double* grad) {
+  double c = 0.0;
+  for (int i = 0; i < M; ++i) {
+    const double logp = z[ids[i]] - L; /* log p_theta(a_i|s) */
+    const double A = tau[i] - logp;    /* A_theta(a_i, s) */
+    const double rho = exp(logp - beta[i]);
+    c += rho * A;
+  }
+  c /= (double)M;
+  *loss = -c;
+  if (!grad) return;
+  for (int64_t j = 0; j < V; ++j) grad[j] = gamma * c * exp(z[j] - L);
+  for (int i = 0; i < M; ++i) {
+    const double logp = z[ids[i]] - L;
+    const double A = tau[i] - logp;
+    const double rho = exp(logp - beta[i]);
+    grad[ids[i]] -= gamma * rho * A / (double)M;
+  }
+}
+
+/*
+ * Dense full-vocabulary KL (Sec. 3):
+ *   D_F = sum_a q (log q - log p_theta),   dD_F/dz_j = p_j - q_j;
+ *   D_R = sum_a p_theta (log p_theta - log q),
+ *   dD_R/dz_j = p_j ((log p_j - log q_j) - D_R)   (eq. reverse-kl-gradient
+ *   pushed through the softmax Jacobian).
+ */
+static void dense_kl(int reverse, const double* z, const double* y, int64_t V, double L,
+                     double gamma, double* loss, double* grad) {
+  const double Ly = log_partition(y, V);
+  double kl = 0.0;
+  for (int64_t j = 0; j < V; ++j) {
+    const double logp = z[j] - L, logq = y[j] - Ly;
+    if (reverse)
+      kl += exp(logp) * (logp - logq);
+    else
+      kl += exp(logq) * (logq - logp);
+  }
+  *loss = kl;
+  if (!grad) return;
+  for (int64_t j = 0; j < V; ++j) {
+    const double logp = z[j] - L, logq = y[j] - Ly;
+    const double p = exp(logp), q = exp(logq);
+    grad[j] = reverse ? gamma * p * ((logp - logq) - kl) : gamma * (p - q);
+  }
+}
+
+int oracle_row(int est, const double* z, const double* y, int64_t V, const int32_t* ids,
+               const double* tau, const double* beta, int K, double gamma, int valid,
+               double* loss, double* grad, double* lse, double* gathered) {
+  const int dense = est == ORACLE_FKL_DENSE || est == ORACLE_RKL_DENSE;
+  if (!z || !loss || V < 1 || est < ORACLE_FKL_TOPK || est > ORACLE_RKL_DENSE) return -1;
+  if (dense && !y) return -1;
+  if (!dense && (K < 1 || !ids || !tau)) return -1;
+  if ((est == ORACLE_RKL_MC || est == ORACLE_RKL_MC1) && !beta) return -1;
+  if (est == ORACLE_RKL_MC1 && K != 1) return -1;
+  if (!dense)
+    for (int i = 0; i < K; ++i)
+      if (ids[i] < 0 || ids[i] >= V) return -1;
+
+  if (!valid) { /* padded token: contributes nothing */
+    *loss = 0.0;
+    if (grad) memset(grad, 0, sizeof(double) * (size_t)V);
+    if (lse) *lse = 0.0;
+    if (gathered && !dense) memset(gathered, 0, sizeof(double) * (size_t)K);
+    return 0;
+  }
+  const double L = log_partition(z, V);
+  if (lse) *lse = L;
+  if (gathered && !dense)
+    for (int i = 0; i < K; ++i) gathered[i] = z[ids[i]];
+  switch (est) {
+    case ORACLE_FKL_TOPK: topk_kl(0, z, V, L, ids, tau, K, gamma, loss, grad); break;
+    case ORACLE_RKL_TOPK: topk_kl(1, z, V, L, ids, tau, K, gamma, loss, grad); break;
+    case ORACLE_RKL_MC1:
+    case ORACLE_RKL_MC: mc_rkl(z, V, L, ids, tau, beta, K, gamma, loss, grad); break;
+    case ORACLE_FKL_DENSE: dense_kl(0, z, y, V, L, gamma, loss, grad); break;
+    case ORACLE_RKL_DENSE: dense_kl(1, z, y, V, L, gamma, loss, grad); break;
+  }
+  return 0;
+}
+
+/* Exact widening of one stored logit to double. */
+static double widen(int dtype, const void* base, int64_t off) {
+  if (dtype == ORACLE_BF16) {
+    const uint32_t bits = (uint32_t)((const uint16_t*)base)[off] << 16;
+    float f;
+    memcpy(&f, &bits, 4);
+    return (double)f;
+  }
+  return (double)((const float*)base)[off];
+}
+
+int oracle_max_threads(void) {
+#ifdef _OPENMP
+  return omp_get_max_threads();
+#else
+  return 1;
+#endif
+}
+
+int oracle_rows(int est, int dtype, const void* logits, const void* teacher_logits, int64_t n_rows,
+                int64_t V, int64_t ld, const int32_t* ids, const float* tau, const float* beta,
+                int K, const uint8_t* mask, double gamma, double* loss, double* grad, double* lse,
+                double* gathered, int nthreads) {
+  const int dense = est == ORACLE_FKL_DENSE || est == ORACLE_RKL_DENSE;
+  if (!logits || !loss || n_rows < 0 || V < 1 || ld < V) return -1;
+  if (dtype != ORACLE_F32 && dtype != ORACLE_BF16) return -1;
+  if (dense && !teacher_logits) return -1;
+  int err = 0;
+  if (nthreads <= 0) nthreads = oracle_max_threads();
+#ifdef _OPENMP
+#pragma omp parallel num_threads(nthreads)
+#endif
+  {
+    double* z = (double*)malloc(sizeof(double) * (size_t)V);
+    double* y = dense ? (double*)malloc(sizeof(double) * (size_t)V) : NULL;
+    double* t = (double*)malloc(sizeof(double) * (size_t)(K > 0 ? K : 1));
+    double* b = (double*)malloc(sizeof(double) * (size_t)(K > 0 ? K : 1));
+    if (!z || (dense && !y) || !t || !b) {
+#ifdef _OPENMP
+#pragma omp atomic write
+#endif
+      err = -2;
+    } else {
+#ifdef _OPENMP
+#pragma omp for schedule(dynamic, 1)
+#endif
+      for (int64_t r = 0; r < n_rows; ++r) {
+        for (int64_t j = 0; j < V; ++j) z[j] = widen(dtype, logits, r * ld + j);
+        if (dense)
+          for (int64_t j = 0; j < V; ++j) y[j] = widen(dtype, teacher_logits, r * ld + j);
+        for (int i = 0; i < K && !dense; ++i) {
+          t[i] = (double)tau[r * K + i];
+          b[i] = beta ? (double)beta[r * K + i] : 0.0;
+        }
+        const int rc = oracle_row(est, z, y, V, dense ? NULL : ids + r * K, t, beta ? b : NULL,
+                                  K, gamma, mask ? mask[r] != 0 : 1, loss + r,
+                                  grad ? grad + r * V : NULL, lse ? lse + r : NULL,
+                                  gathered && !dense ? gathered + r * K : NULL);
+        if (rc) {
+#ifdef _OPENMP
+#pragma omp atomic write
+#endif
+          err = rc;
+        }
+      }
+    }
+    free(z);
+    free(y);
+    free(t);
+    free(b);
+  }
+  return err;
+}

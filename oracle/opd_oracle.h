@@ -1,0 +1,55 @@
+/*
+ * The oracle: a plain, slow, double-precision CPU implementation of the
+ * learner-time on-policy-distillation (OPD) loss and its gradient with respect
+ * to the student logits.  It is test infrastructure: only the tests, the smoke
+ * check and the benchmark's CPU-baseline leg use it, and it shares no code
+ * with the GPU library.
+ */
+#ifndef OPD_ORACLE_H
+#define OPD_ORACLE_H
+#include <stdint.h>
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  ORACLE_FKL_TOPK = 0,  /* forward KL on a cached support, renormalised (Sec. 3; App. A.1) */
+  ORACLE_RKL_TOPK = 1,  /* reverse KL on a cached support, renormalised (App. A.1) */
+  ORACLE_RKL_MC1 = 2,   /* one-sample MC, A_theta, no clip (Sec. 5.1, L_theta^noclip) */
+  ORACLE_RKL_MC = 3,    /* m-sample MC average (Sec. 6.2; App. E) */
+  ORACLE_FKL_DENSE = 4, /* full-vocabulary forward KL (Sec. 3, eq. dense-forward-kl) */
+  ORACLE_RKL_DENSE = 5  /* full-vocabulary reverse KL (Sec. 3, eq. dense-reverse-kl) */
+};
+
+enum { ORACLE_F32 = 0, ORACLE_BF16 = 1 };
+
+/* One token row, everything in double.
+ *   z[V]      student logits;  y[V] teacher logits (dense estimators, else NULL)
+ *   ids[K]    cached support (top-k) or behaviour samples (MC)
+ *   tau[K]    teacher log-probs log q(a|s) at ids (full-vocabulary normalised)
+ *   beta[K]   behaviour log-probs log p_old(a|s) at ids (MC only, else NULL)
+ *   gamma     gradient scale; valid = 0 marks a padded token
+ * Outputs: *loss, grad[V] (nullable), *lse (log-partition of z; nullable),
+ * gathered[K] = z at ids (nullable).  Returns 0, or -1 on bad arguments
+ * (id out of range, K < 1, missing input). */
+int oracle_row(int est, const double* z, const double* y, int64_t V, const int32_t* ids,
+               const double* tau, const double* beta, int K, double gamma, int valid,
+               double* loss, double* grad, double* lse, double* gathered);
+
+/* Rows of stored inputs (fp32, or bf16 bit patterns widened exactly), rows
+ * processed by `nthreads` threads (0 = all).  logits/teacher_logits are
+ * [n_rows, ld]; ids/tau/beta are [n_rows, K]; mask [n_rows] is nullable;
+ * grad is [n_rows, V] (nullable), lse [n_rows], gathered [n_rows, K]
+ * (nullable).  Returns 0 or the first row error. */
+int oracle_rows(int est, int dtype, const void* logits, const void* teacher_logits, int64_t n_rows,
+                int64_t V, int64_t ld, const int32_t* ids, const float* tau, const float* beta,
+                int K, const uint8_t* mask, double gamma, double* loss, double* grad, double* lse,
+                double* gathered, int nthreads);
+
+/* Number of threads oracle_rows uses for nthreads = 0. */
+int oracle_max_threads(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif
