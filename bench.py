@@ -1,0 +1,252 @@
+"""Benchmark of the learner-time OPD loss forward+backward on one MI355X.
+
+A step is one fused forward+backward call over a batch of N token rows
+(student log-softmax over V, gather at the cached support, estimator,
+gradient write).  The default workload is 16-sample Monte-Carlo reverse KL
+over N = 32,768 tokens of a V = 151,936 vocabulary with bf16 logits and fp32
+gradients.  Inputs are synthetic (seeded generator), resident in HBM before
+the timed region.
+
+Prints one JSON line on stdout:
+  value       tokens per second over the timed steps (valid tokens)
+  roofline    HBM roofline of the loss kernel: algorithmic bytes per launch
+              (one read of the logits, one write of the gradient, the cache)
+              over the mean launch time measured with HIP events on the
+              launch stream, against the 8 TB/s MI355X peak
+  cpu_baseline  the oracle on a bounded sample of the same workload, on the
+              host cores
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2606_24143_amd", "csrc", f)
+                  for f in ("opd_kernels.hip", "opd_api.cpp", "opd_internal.h")]
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+def log(msg: str):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def kernel_hash() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def algorithmic_bytes(w, est: str, n_valid: int, n_masked: int) -> int:
+    """Bytes the method must move per launch: each valid row's logits read
+    once, every gradient row written once (masked rows are written as zeros),
+    the cache entries read once, and the per-token loss written."""
+    in_b = 2 if w.dtype == 1 else 4
+    out_b = 4
+    V = w.V
+    K = w.k if est in ("fkl_topk", "rkl_topk") else (1 if est == "rkl_mc1" else w.M)
+    if est in ("fkl_topk", "rkl_topk"):
+        row_read = K * in_b                 # only the cached logits are needed
+        cache = K * (4 + 4)
+    elif est in ("fkl_dense", "rkl_dense"):
+        row_read = 2 * V * in_b             # student and teacher rows
+        cache = 0
+    else:
+        row_read = V * in_b
+        cache = K * (4 + 4 + 4)
+    return n_valid * (row_read + cache) + (n_valid + n_masked) * (V * out_b + 4)
+
+
+def read_traffic(est_key: str):
+    """Measured HBM bytes per launch from the committed counter summary, if it
+    was taken on the current kernel sources."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("kernel_hash") != kernel_hash():
+        return None
+    e = t.get("workloads", {}).get(est_key)
+    return None if e is None else e.get("bytes_per_launch")
+
+
+def cpu_baseline(w, est, d, rows: int, threads: int, chunk: int = 512):
+    """The oracle as it stands, over the first `rows` token rows of the timed
+    workload, in chunks (so its fp64 gradient buffer stays small); only the
+    oracle calls are timed."""
+    import numpy as np
+
+    import oracle
+
+    n = min(rows, w.N) if rows > 0 else w.N
+    dt = 0.0
+    for r0 in range(0, n, chunk):
+        r1 = min(n, r0 + chunk)
+        ids = tau = beta = None
+        if est in ("fkl_topk", "rkl_topk"):
+            ids, tau = d["topk_idx"][r0:r1], d["topk_tau"][r0:r1]
+        elif est in ("rkl_mc", "rkl_mc1"):
+            m = 1 if est == "rkl_mc1" else w.M
+            ids = np.ascontiguousarray(d["mc_ids"][r0:r1, :m])
+            tau = np.ascontiguousarray(d["mc_tau"][r0:r1, :m])
+            beta = np.ascontiguousarray(d["mc_beta"][r0:r1, :m])
+        teacher = d["teacher_logits"][r0:r1] if "teacher_logits" in d else None
+        t0 = time.perf_counter()
+        oracle.rows(est, oracle.BF16 if w.dtype == 1 else oracle.F32, d["logits"][r0:r1], w.V,
+                    ids=ids, tau=tau, beta=beta, teacher_logits=teacher, mask=d["mask"][r0:r1],
+                    nthreads=threads)
+        dt += time.perf_counter() - t0
+    used = threads if threads > 0 else oracle.max_threads()
+    return {"value": n / dt, "unit": "tokens/s", "cores": used, "kind": "oracle",
+            "sample": "first %d of the %d token rows of the timed workload, fp64 oracle "
+                      "forward+backward, %.1f s wall on %d threads" % (n, w.N, dt, used)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="n32768_v151936_bf16_mc16")
+    ap.add_argument("--estimator", default=None)
+    ap.add_argument("--cpu-rows", type=int, default=0, help="0 = every row")
+    ap.add_argument("--cpu-threads", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calib-copy", type=int, default=0,
+                    help="also time a plain device copy of this many MiB (counter calibration)")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (rows are independent; "
+              "each GPU would run the same kernel on its own share of rows). Use --gpus 1.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2606_24143_amd as opd
+    import synth
+
+    opd.lib()  # fails loudly when the HIP library is not built
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    w = synth.WORKLOADS[args.workload]
+    est = args.estimator or w.estimators[0]
+
+    log("generating %s ..." % w.name)
+    t0 = time.perf_counter()
+    d = synth.generate(w)
+    log("generated in %.1f s" % (time.perf_counter() - t0))
+
+    def dev_t(a):
+        if a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16)).to(dev).view(torch.bfloat16)
+        return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+
+    logits = dev_t(d["logits"])
+    kw = {}
+    if est in ("fkl_topk", "rkl_topk"):
+        kw = dict(idx=dev_t(d["topk_idx"]), teacher_logp=dev_t(d["topk_tau"]))
+    elif est in ("rkl_mc", "rkl_mc1"):
+        m = 1 if est == "rkl_mc1" else w.M
+        kw = dict(sampled_ids=dev_t(d["mc_ids"][:, :m]), teacher_logp=dev_t(d["mc_tau"][:, :m]),
+                  behav_logp=dev_t(d["mc_beta"][:, :m]))
+    else:
+        kw = dict(teacher_logits=dev_t(d["teacher_logits"]))
+    mask_np = d["mask"]
+    mask = dev_t(mask_np) if w.ragged else None
+    n_valid = int(mask_np.sum())
+    N = w.N
+    out = {"loss": torch.empty(N, dtype=torch.float32, device=dev),
+           "dlogits": torch.empty((N, w.V), dtype=torch.float32, device=dev)}
+    nbytes = opd.workspace_bytes(N, w.V, w.dtype, est, w.k, w.M)
+    ws = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev) if nbytes else None
+    stream = torch.cuda.current_stream()
+
+    def step():
+        opd.loss_fwd_bwd(logits, est, mask=mask, out=out, workspace=ws, stream=stream, **kw)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        starts[i].record(stream)
+        step()
+        ends[i].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    launch_ms = [s.elapsed_time(e) for s, e in zip(starts, ends)]
+    mean_launch_s = sum(launch_ms) / len(launch_ms) / 1e3
+    ms_per_step = wall / args.steps * 1e3
+
+    alg = algorithmic_bytes(w, est, n_valid, N - n_valid)
+    achieved = alg / mean_launch_s / 1e9
+    traffic = read_traffic(w.name + "/" + est)
+    res = {
+        "metric": "OPD loss fwd+bwd tokens/sec at V=151,936 bf16; achieved HBM GB/s vs peak",
+        "value": n_valid / (ms_per_step / 1e3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "estimator": est, "tokens": N, "valid_tokens": n_valid,
+                   "vocab": w.V, "logits_dtype": "bf16" if w.dtype == 1 else "f32",
+                   "dlogits_dtype": "f32", "k": w.k, "M": w.M,
+                   "path": "split" if nbytes else "rowwise"},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": achieved / PEAK_HBM_GBS,
+                     "traffic": traffic,
+                     "algorithmic_bytes_per_launch": alg,
+                     "mean_launch_ms": mean_launch_s * 1e3,
+                     "min_launch_ms": min(launch_ms)},
+    }
+    if args.calib_copy:
+        n = args.calib_copy * (1 << 20) // 4
+        a = torch.ones(n, dtype=torch.float32, device=dev)
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(10):
+            b.copy_(a)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        res["copy_calibration"] = {"bytes_per_copy": 2 * n * 4,
+                                   "GBps": 2 * n * 4 * 10 / (e0.elapsed_time(e1) / 1e3) / 1e9}
+    if not args.no_cpu_baseline:
+        del logits, out
+        torch.cuda.empty_cache()
+        log("timing the oracle ...")
+        res["cpu_baseline"] = cpu_baseline(w, est, d, args.cpu_rows, args.cpu_threads)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,205 @@
+/*
+ * opd.h - C ABI of the learner-time on-policy-distillation (OPD) loss for
+ * AMD Instinct MI355X (gfx950).
+ *
+ * One call takes the student logits of N generated tokens over a vocabulary
+ * of V entries, plus the finite teacher-score cache those tokens carry, and
+ * returns the per-token loss and its gradient with respect to every logit
+ * (Sec. 4.1, "Stage 3: Student update": the learner recomputes log p_theta
+ * on the cached actions).  All work runs in HIP kernels on the caller's
+ * stream; nothing is computed on the host.
+ *
+ * Conventions shared by every entry point
+ *  - Array pointers are DEVICE pointers owned by the caller.  The library
+ *    keeps no reference to them after the call returns and allocates no
+ *    device memory.
+ *  - Logit rows have stride `ld` elements (ld >= V).  logits, dlogits and
+ *    teacher_logits must be 16-byte aligned and ld * element_size must be a
+ *    multiple of 16 bytes (ld % 8 == 0 when any of them is bf16, else
+ *    ld % 4 == 0).  Columns [V, ld) of dlogits are never written.
+ *  - Calls are stream-ordered and asynchronous.  Argument errors are
+ *    reported synchronously, before anything is launched; a HIP launch
+ *    failure returns OPD_ERR_HIP.  Faults in the DATA (a cached id outside
+ *    [0, V), NaN or infinite logits) never fault the device: an out-of-range
+ *    id makes that row's loss NaN and fills its dlogits row with NaN, and
+ *    NaN/Inf logits propagate into that row's outputs.
+ *  - Results are deterministic: repeated calls with the same inputs produce
+ *    bitwise-identical outputs (fixed-order reductions, no float atomics).
+ *  - Entry points hold no mutable global state and are safe to call from
+ *    several host threads (each call on its own stream and buffers).
+ */
+#ifndef OPD_H
+#define OPD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define OPD_VERSION 1
+/* Largest cached support size k, and largest sample count M. */
+#define OPD_K_MAX 256
+
+typedef enum opd_status {
+  OPD_OK = 0,
+  OPD_ERR_NULL = -1,      /* a pointer the estimator needs is NULL */
+  OPD_ERR_SHAPE = -2,     /* N < 0, V < 2, V >= 2^31, or ld < V */
+  OPD_ERR_SUPPORT = -3,   /* k or M outside [1, min(V, OPD_K_MAX)], or RKL_MC1 with M != 1 */
+  OPD_ERR_DTYPE = -4,     /* unknown logits or dlogits dtype */
+  OPD_ERR_ALIGN = -5,     /* a logit/gradient pointer or row stride is not 16-byte aligned */
+  OPD_ERR_WORKSPACE = -6, /* split-vocabulary path forced with a missing or short workspace */
+  OPD_ERR_ESTIMATOR = -7, /* unknown estimator */
+  OPD_ERR_FLAGS = -8,     /* unknown or contradictory flag bits */
+  OPD_ERR_HIP = -9        /* a HIP runtime call or kernel launch failed */
+} opd_status;
+
+/*
+ * Estimators.  Notation of Sec. 3: p_theta = softmax(z) the current student,
+ * q the teacher, p_old the stale behaviour policy.  For token t with logits
+ * z (row of `logits`), L = log sum_j exp(z_j) and log p_theta(j) = z_j - L.
+ *
+ * OPD_FKL_TOPK  Forward KL on the cached support S = {idx[t, 0..k)}, teacher
+ *               and student both renormalised on S (Sec. 3, "Sparse and
+ *               sampled implementations"; normalisers of App. A.1):
+ *                 loss = sum_S q~ (log q~ - log p~),
+ *                 dloss/dz_{a_i} = p~_i - q~_i, zero off S.
+ * OPD_RKL_TOPK  Sparse reverse KL D_R^S = KL(p~ || q~) (App. A.1), support
+ *               held fixed:  dloss/dz_{a_i} = p~_i ((log p~_i - log q~_i) - D_R^S).
+ *               Renormalisation cancels L, so both top-k estimators read only
+ *               the k cached logits unless lse_out is requested.
+ * OPD_RKL_MC1   One-sample MC reverse KL with old-to-current importance
+ *               ratio and the advantage recomputed under the current student,
+ *               unclipped (Sec. 5.1, L_theta^noclip):
+ *                 loss = -rho(a) sg(A_theta(a)),  A_theta = log q - log p_theta,
+ *                 rho = p_theta(a) / p_old(a).   Requires M == 1.
+ * OPD_RKL_MC    M-sample average of the same surrogate (Sec. 6.2; App. E):
+ *                 loss = -(1/M) sum_i rho(a_i) sg(A_theta(a_i)),
+ *                 dloss/dz_j = c p_theta(j) - (1/M) sum_{i: a_i = j} rho_i A_i,
+ *               c = -loss.  Samples are iid with replacement; repeated ids are
+ *               separate terms, accumulated in ascending i.
+ * OPD_FKL_DENSE Full-vocabulary forward KL against dense teacher logits
+ *               (Sec. 3, eq. dense-forward-kl): gradient p_theta - q.
+ * OPD_RKL_DENSE Full-vocabulary reverse KL (Sec. 3, eq. dense-reverse-kl and
+ *               eq. reverse-kl-gradient): gradient p_j ((log p_j - log q_j) - D_R).
+ */
+typedef enum opd_estimator {
+  OPD_FKL_TOPK = 0,
+  OPD_RKL_TOPK = 1,
+  OPD_RKL_MC1 = 2,
+  OPD_RKL_MC = 3,
+  OPD_FKL_DENSE = 4,
+  OPD_RKL_DENSE = 5
+} opd_estimator;
+
+typedef enum opd_dtype { OPD_F32 = 0, OPD_BF16 = 1 } opd_dtype;
+
+/* Flags (opd_opts.flags). */
+#define OPD_FLAG_SKIP_MASKED 1u   /* leave dlogits rows of masked tokens untouched */
+#define OPD_FLAG_FORCE_ROWWISE 2u /* one workgroup per token row, whatever N is */
+#define OPD_FLAG_FORCE_SPLITV 4u  /* split each row over several workgroups (needs workspace) */
+
+/*
+ * The teacher-score cache of N tokens (Sec. 4.1, Stage 1 and Stage 2).
+ * Row-major device arrays; which fields are read depends on the estimator.
+ *   idx            [N, k] int32  top-k support S (top-k estimators); ids must
+ *                  be distinct within a row (opd_validate_cache checks this)
+ *   sampled_ids    [N, M] int32  behaviour-policy samples a_i ~ p_old (MC
+ *                  estimators); repeats allowed
+ *   teacher_logp   [N, k] or [N, M] fp32  log q(a|s) at idx / sampled_ids,
+ *                  normalised over the full vocabulary (the top-k estimators
+ *                  renormalise on S, so any per-row constant cancels there)
+ *   behav_logp     [N, M] fp32  log p_old(a|s) at sampled_ids (MC only),
+ *                  recorded per token by the rollout policy
+ *   teacher_logits [N, ld] dense teacher logits (dense estimators only),
+ *                  same dtype and stride as the student logits
+ */
+typedef struct opd_cache {
+  const int32_t* idx;
+  const int32_t* sampled_ids;
+  const float* teacher_logp;
+  const float* behav_logp;
+  const void* teacher_logits;
+} opd_cache;
+
+/*
+ * grad_scale    gamma: dlogits[t, :] = gamma * mask[t] * dloss_t/dz_t; 1.0 gives
+ *               the gradient of the masked sum of per-token losses.  Reductions
+ *               over tokens (token mean, sequence mean) are the caller's: they
+ *               are a choice of gamma.
+ * dlogits_dtype OPD_F32 (default) or OPD_BF16 (round to nearest even).
+ * flags         OPD_FLAG_* bits.
+ * A NULL opts pointer means {1.0f, OPD_F32, 0}.
+ */
+typedef struct opd_opts {
+  float grad_scale;
+  int32_t dlogits_dtype;
+  uint32_t flags;
+} opd_opts;
+
+/*
+ * Fused forward + backward of the OPD loss over N token rows.
+ *
+ *   logits        [N, ld] student logits, dtype OPD_F32 or OPD_BF16
+ *   N, V, ld      tokens, vocabulary size, row stride (elements)
+ *   cache         see opd_cache; must not be NULL
+ *   estimator     opd_estimator
+ *   k             support size for the top-k estimators (else ignored)
+ *   M             samples per token for the MC estimators (else ignored)
+ *   mask          [N] uint8, nullable (NULL = every token valid).  A masked
+ *                 token (mask == 0) has loss 0, lse_out 0, gathered_out 0, and
+ *                 a zero dlogits row (untouched with OPD_FLAG_SKIP_MASKED);
+ *                 its logits are not read.
+ *   opts          nullable, see opd_opts
+ *   loss          [N] fp32 per-token loss (the MC loss is the surrogate value,
+ *                 an unbiased estimate of the dense reverse KL, and can be
+ *                 negative)
+ *   dlogits       [N, ld] gradient, dtype opts->dlogits_dtype; may not alias
+ *                 logits
+ *   lse_out       [N] fp32 log sum_j exp(z_j), nullable.  For the top-k
+ *                 estimators, requesting it adds one read of the logits.
+ *   gathered_out  [N, k or M] fp32 student logits at the cached ids (exact
+ *                 widening), nullable; not produced by the dense estimators.
+ *   workspace     device scratch for the split-vocabulary path, nullable;
+ *   workspace_bytes  its size.  The split path is taken for small N (or when
+ *                 forced) only if workspace_bytes >= opd_workspace_bytes(...);
+ *                 otherwise the row-per-workgroup path runs.
+ *   stream        hipStream_t to launch on (NULL = default stream)
+ * Returns OPD_OK or an opd_status error.  N == 0 is a no-op returning OPD_OK.
+ */
+int opd_loss_fwd_bwd(const void* logits, int32_t dtype, int64_t N, int64_t V, int64_t ld,
+                     const opd_cache* cache, int32_t estimator, int32_t k, int32_t M,
+                     const uint8_t* mask, const opd_opts* opts, float* loss, void* dlogits,
+                     float* lse_out, float* gathered_out, void* workspace,
+                     size_t workspace_bytes, void* stream);
+
+/*
+ * Bytes of workspace opd_loss_fwd_bwd uses for these arguments (0 when the
+ * call takes the row-per-workgroup path).  Pure host function: the answer
+ * depends only on its arguments.  Invalid arguments return 0.
+ */
+size_t opd_workspace_bytes(int64_t N, int64_t V, int32_t dtype, int32_t estimator, int32_t k,
+                           int32_t M, uint32_t flags);
+
+/*
+ * Checks a cache against the preconditions of the estimator and ADDS the
+ * number of violations to *violations (a device int32 the caller zeroes):
+ * ids outside [0, V), repeated ids within a top-k row, and non-finite
+ * teacher_logp (and behav_logp for MC).  Each bad entry counts once, each
+ * repeated top-k pair once.  Stream-ordered; read the counter after
+ * synchronising.  Dense estimators have no cache to check (returns OPD_OK).
+ */
+int opd_validate_cache(const opd_cache* cache, int32_t estimator, int64_t N, int64_t V,
+                       int32_t k, int32_t M, int32_t* violations, void* stream);
+
+/* Static description of a status code ("ok", "null pointer", ...). */
+const char* opd_status_string(int status);
+
+/* OPD_VERSION of the built library. */
+int opd_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* OPD_H */

@@ -1,0 +1,188 @@
+"""ctypes binding over libopd.so (the C ABI declared in include/opd.h).
+
+Argument marshalling only: this module turns torch tensors into device
+pointers, sizes and a HIP stream, allocates the output buffers, and raises on
+a non-zero status.  Every step of the computation runs in the library's HIP
+kernels.  There is no fallback: if libopd.so is missing or a GPU is absent,
+calls fail loudly.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libopd.so")
+
+# opd_estimator, opd_dtype, flags (include/opd.h)
+ESTIMATORS = {"fkl_topk": 0, "rkl_topk": 1, "rkl_mc1": 2, "rkl_mc": 3, "fkl_dense": 4,
+              "rkl_dense": 5}
+F32, BF16 = 0, 1
+FLAG_SKIP_MASKED = 1
+FLAG_FORCE_ROWWISE = 2
+FLAG_FORCE_SPLITV = 4
+K_MAX = 256
+
+STATUS = {0: "OPD_OK", -1: "OPD_ERR_NULL", -2: "OPD_ERR_SHAPE", -3: "OPD_ERR_SUPPORT",
+          -4: "OPD_ERR_DTYPE", -5: "OPD_ERR_ALIGN", -6: "OPD_ERR_WORKSPACE",
+          -7: "OPD_ERR_ESTIMATOR", -8: "OPD_ERR_FLAGS", -9: "OPD_ERR_HIP"}
+
+# every symbol include/opd.h declares
+EXPORTS = ("opd_loss_fwd_bwd", "opd_workspace_bytes", "opd_validate_cache", "opd_status_string",
+           "opd_version")
+
+
+class OpdError(RuntimeError):
+    def __init__(self, code: int, where: str):
+        self.code = code
+        self.status = STATUS.get(code, str(code))
+        super().__init__("%s failed: %s (%s)" % (where, self.status, status_string(code)))
+
+
+class OpdCache(ctypes.Structure):
+    _fields_ = [("idx", ctypes.c_void_p), ("sampled_ids", ctypes.c_void_p),
+                ("teacher_logp", ctypes.c_void_p), ("behav_logp", ctypes.c_void_p),
+                ("teacher_logits", ctypes.c_void_p)]
+
+
+class OpdOpts(ctypes.Structure):
+    _fields_ = [("grad_scale", ctypes.c_float), ("dlogits_dtype", ctypes.c_int32),
+                ("flags", ctypes.c_uint32)]
+
+
+_lib = None
+
+
+def lib():
+    """Load libopd.so (built by __graft_entry__.build() or paper_2606_24143_amd.build)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError("libopd.so is not built at %s; run __graft_entry__.build()" % LIB_PATH)
+        L = ctypes.CDLL(LIB_PATH)
+        P, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+        L.opd_loss_fwd_bwd.argtypes = [P, i32, i64, i64, i64, ctypes.POINTER(OpdCache), i32, i32,
+                                       i32, P, ctypes.POINTER(OpdOpts), P, P, P, P, P,
+                                       ctypes.c_size_t, P]
+        L.opd_loss_fwd_bwd.restype = ctypes.c_int
+        L.opd_workspace_bytes.argtypes = [i64, i64, i32, i32, i32, i32, ctypes.c_uint32]
+        L.opd_workspace_bytes.restype = ctypes.c_size_t
+        L.opd_validate_cache.argtypes = [ctypes.POINTER(OpdCache), i32, i64, i64, i32, i32, P, P]
+        L.opd_validate_cache.restype = ctypes.c_int
+        L.opd_status_string.argtypes = [ctypes.c_int]
+        L.opd_status_string.restype = ctypes.c_char_p
+        L.opd_version.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def status_string(code: int) -> str:
+    return lib().opd_status_string(code).decode()
+
+
+def version() -> int:
+    return int(lib().opd_version())
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _dt(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return BF16
+    if t.dtype == torch.float32:
+        return F32
+    raise TypeError("logits must be float32 or bfloat16, got %s" % t.dtype)
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _rowmajor(t: torch.Tensor, name: str):
+    if t.dim() != 2 or t.stride(1) != 1:
+        raise ValueError("%s must be a 2-D tensor with unit column stride" % name)
+
+
+def workspace_bytes(N: int, V: int, dtype: int, estimator: str, k: int = 0, M: int = 0,
+                    flags: int = 0) -> int:
+    return int(lib().opd_workspace_bytes(N, V, dtype, ESTIMATORS[estimator], k, M, flags))
+
+
+def loss_fwd_bwd(logits: torch.Tensor, estimator: str, *, idx=None, sampled_ids=None,
+                 teacher_logp=None, behav_logp=None, teacher_logits=None, mask=None,
+                 grad_scale: float = 1.0, dlogits_dtype=torch.float32, flags: int = 0,
+                 want_lse: bool = False, want_gathered: bool = False, workspace=None,
+                 out=None, stream=None):
+    """One fused forward+backward call of opd_loss_fwd_bwd.
+
+    logits: [N, V] device tensor (a row-strided view of an [N, ld] buffer is
+    fine).  Cache tensors are [N, k] / [N, M] device tensors.  Returns a dict
+    with "loss" [N], "dlogits" [N, V] (a view of the [N, ld] buffer), and
+    "lse" / "gathered" when requested.  `workspace=None` allocates what the
+    split path needs; pass a tensor to supply your own (or an empty one to
+    force the row-per-workgroup path).  `out` may hold preallocated "loss"
+    and "dlogits" ([N, ld]) tensors.
+    """
+    est = ESTIMATORS[estimator]
+    _rowmajor(logits, "logits")
+    N, V = logits.shape
+    ld = logits.stride(0) if N > 1 else V
+    dev = logits.device
+    dt = _dt(logits)
+    odt = {torch.float32: F32, torch.bfloat16: BF16}[dlogits_dtype]
+    k = int(idx.shape[1]) if idx is not None else 0
+    M = int(sampled_ids.shape[1]) if sampled_ids is not None else 0
+    if teacher_logits is not None:
+        _rowmajor(teacher_logits, "teacher_logits")
+    cache = OpdCache(_ptr(idx), _ptr(sampled_ids), _ptr(teacher_logp), _ptr(behav_logp),
+                     _ptr(teacher_logits))
+    opts = OpdOpts(grad_scale, odt, flags)
+    if out is not None:
+        loss, dbuf = out["loss"], out["dlogits"]
+    else:
+        loss = torch.empty(N, dtype=torch.float32, device=dev)
+        dbuf = torch.empty((N, ld), dtype=dlogits_dtype, device=dev)
+    lse = torch.empty(N, dtype=torch.float32, device=dev) if want_lse else None
+    K = k if estimator in ("fkl_topk", "rkl_topk") else M
+    gathered = (torch.empty((N, max(K, 1)), dtype=torch.float32, device=dev)
+                if want_gathered and estimator not in ("fkl_dense", "rkl_dense") else None)
+    if workspace is None:
+        nbytes = workspace_bytes(N, V, dt, estimator, k, M, flags)
+        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev) if nbytes else None
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    rc = lib().opd_loss_fwd_bwd(_ptr(logits), dt, N, V, ld, ctypes.byref(cache), est, k, M,
+                                _ptr(mask), ctypes.byref(opts), _ptr(loss), _ptr(dbuf), _ptr(lse),
+                                _ptr(gathered), _ptr(workspace) if ws_bytes else None, ws_bytes,
+                                _stream(stream))
+    if rc != 0:
+        raise OpdError(rc, "opd_loss_fwd_bwd")
+    res = {"loss": loss, "dlogits": dbuf[:, :V]}
+    if lse is not None:
+        res["lse"] = lse
+    if gathered is not None:
+        res["gathered"] = gathered[:, :K]
+    return res
+
+
+def validate_cache(estimator: str, V: int, *, idx=None, sampled_ids=None, teacher_logp=None,
+                   behav_logp=None, stream=None) -> int:
+    """Number of cache entries violating the estimator's preconditions (synchronises)."""
+    ids = idx if idx is not None else sampled_ids
+    N, K = (0, 0) if ids is None else ids.shape
+    dev = (ids if ids is not None else teacher_logp).device
+    counter = torch.zeros(1, dtype=torch.int32, device=dev)
+    cache = OpdCache(_ptr(idx), _ptr(sampled_ids), _ptr(teacher_logp), _ptr(behav_logp), None)
+    k = K if estimator in ("fkl_topk", "rkl_topk") else 0
+    M = K if estimator in ("rkl_mc1", "rkl_mc") else 0
+    rc = lib().opd_validate_cache(ctypes.byref(cache), ESTIMATORS[estimator], N, V, k, M,
+                                  _ptr(counter), _stream(stream))
+    if rc != 0:
+        raise OpdError(rc, "opd_validate_cache")
+    return int(counter.item())

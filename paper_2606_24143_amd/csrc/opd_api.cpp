@@ -1,0 +1,228 @@
+// C-ABI entry points of libopd: argument validation, path selection, launch.
+// Every argument check runs on the host before any HIP call, so argument
+// errors are reported without touching the device.
+#include <limits.h>
+#include <stdint.h>
+
+#include "../../include/opd.h"
+#include "opd_internal.h"
+
+namespace {
+
+using opd::Args;
+using opd::Path;
+
+// Below this many rows the split-vocabulary path runs (when it has a
+// workspace): N rows alone give too few workgroups to keep 256 CUs streaming.
+constexpr int64_t kSplitMaxRows = 2048;
+// Workgroups the split path aims for, and its largest chunk count.
+constexpr int64_t kSplitTargetGroups = 8192;
+constexpr int kSplitMaxChunks = 64;
+
+constexpr uint32_t kKnownFlags =
+    OPD_FLAG_SKIP_MASKED | OPD_FLAG_FORCE_ROWWISE | OPD_FLAG_FORCE_SPLITV;
+
+bool valid_est(int32_t e) { return e >= OPD_FKL_TOPK && e <= OPD_RKL_DENSE; }
+bool est_topk(int32_t e) { return e == OPD_FKL_TOPK || e == OPD_RKL_TOPK; }
+bool est_mc(int32_t e) { return e == OPD_RKL_MC1 || e == OPD_RKL_MC; }
+bool est_dense(int32_t e) { return e == OPD_FKL_DENSE || e == OPD_RKL_DENSE; }
+int elt_bytes(int32_t dt) { return dt == OPD_BF16 ? 2 : 4; }
+int elems_per_vec(int32_t dt) { return 16 / elt_bytes(dt); }
+
+int check_shape(int64_t N, int64_t V, int64_t ld) {
+  if (N < 0 || N > INT32_MAX) return OPD_ERR_SHAPE;
+  if (V < 2 || V > INT32_MAX) return OPD_ERR_SHAPE;
+  if (ld < V) return OPD_ERR_SHAPE;
+  return OPD_OK;
+}
+
+int check_support(int32_t est, int64_t V, int32_t k, int32_t M) {
+  if (est_topk(est)) {
+    const int64_t kmax = V < OPD_K_MAX ? V : OPD_K_MAX;
+    if (k < 1 || k > kmax) return OPD_ERR_SUPPORT;
+  } else if (est_mc(est)) {
+    if (M < 1 || M > OPD_K_MAX) return OPD_ERR_SUPPORT;
+    if (est == OPD_RKL_MC1 && M != 1) return OPD_ERR_SUPPORT;
+  }
+  return OPD_OK;
+}
+
+int check_flags(uint32_t flags) {
+  if (flags & ~kKnownFlags) return OPD_ERR_FLAGS;
+  if ((flags & OPD_FLAG_FORCE_ROWWISE) && (flags & OPD_FLAG_FORCE_SPLITV)) return OPD_ERR_FLAGS;
+  return OPD_OK;
+}
+
+struct Plan {
+  bool split;
+  int P;
+  int64_t chunk_vec;
+  size_t ws_bytes;
+};
+
+// The split-path layout for N rows of nvec vectors: enough chunks for about
+// kSplitTargetGroups workgroups, each chunk at least one vector per lane.
+Plan split_plan(int64_t N, int64_t nvec) {
+  Plan p{true, 1, nvec, 0};
+  int64_t P = (kSplitTargetGroups + N - 1) / N;
+  const int64_t by_width = nvec / opd::kSplitThreads;
+  if (P > by_width) P = by_width;
+  if (P > kSplitMaxChunks) P = kSplitMaxChunks;
+  if (P < 1) P = 1;
+  p.P = (int)P;
+  p.chunk_vec = (nvec + P - 1) / P;
+  p.ws_bytes = (size_t)N * (size_t)P * opd::kPartialFloats * sizeof(float);
+  return p;
+}
+
+bool split_wanted(int64_t N, uint32_t flags) {
+  if (flags & OPD_FLAG_FORCE_SPLITV) return true;
+  if (flags & OPD_FLAG_FORCE_ROWWISE) return false;
+  return N < kSplitMaxRows;
+}
+
+int64_t nvec_of(int64_t V, int32_t dt) {
+  const int64_t epv = elems_per_vec(dt);
+  return (V + epv - 1) / epv;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+}  // namespace
+
+extern "C" {
+
+int opd_version(void) { return OPD_VERSION; }
+
+const char* opd_status_string(int status) {
+  switch (status) {
+    case OPD_OK: return "ok";
+    case OPD_ERR_NULL: return "a required pointer is NULL";
+    case OPD_ERR_SHAPE: return "invalid shape (N, V or ld)";
+    case OPD_ERR_SUPPORT: return "support size k or sample count M out of range";
+    case OPD_ERR_DTYPE: return "unknown dtype";
+    case OPD_ERR_ALIGN: return "pointer or row stride not 16-byte aligned";
+    case OPD_ERR_WORKSPACE: return "workspace missing or too small for the split path";
+    case OPD_ERR_ESTIMATOR: return "unknown estimator";
+    case OPD_ERR_FLAGS: return "unknown or contradictory flags";
+    case OPD_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+size_t opd_workspace_bytes(int64_t N, int64_t V, int32_t dtype, int32_t estimator, int32_t k,
+                           int32_t M, uint32_t flags) {
+  if (!valid_est(estimator) || (dtype != OPD_F32 && dtype != OPD_BF16)) return 0;
+  if (check_shape(N, V, V) != OPD_OK || N == 0) return 0;
+  if (check_support(estimator, V, k, M) != OPD_OK || check_flags(flags) != OPD_OK) return 0;
+  if (!split_wanted(N, flags)) return 0;
+  return split_plan(N, nvec_of(V, dtype)).ws_bytes;
+}
+
+int opd_loss_fwd_bwd(const void* logits, int32_t dtype, int64_t N, int64_t V, int64_t ld,
+                     const opd_cache* cache, int32_t estimator, int32_t k, int32_t M,
+                     const uint8_t* mask, const opd_opts* opts, float* loss, void* dlogits,
+                     float* lse_out, float* gathered_out, void* workspace,
+                     size_t workspace_bytes, void* stream) {
+  if (!valid_est(estimator)) return OPD_ERR_ESTIMATOR;
+  const opd_opts o = opts ? *opts : opd_opts{1.0f, OPD_F32, 0u};
+  if (dtype != OPD_F32 && dtype != OPD_BF16) return OPD_ERR_DTYPE;
+  if (o.dlogits_dtype != OPD_F32 && o.dlogits_dtype != OPD_BF16) return OPD_ERR_DTYPE;
+  if (int rc = check_flags(o.flags)) return rc;
+  if (int rc = check_shape(N, V, ld)) return rc;
+  if (int rc = check_support(estimator, V, k, M)) return rc;
+  if (N == 0) return OPD_OK;
+
+  if (!logits || !cache || !loss || !dlogits) return OPD_ERR_NULL;
+  const int32_t* ids = nullptr;
+  int K = 0;
+  if (est_topk(estimator)) {
+    if (!cache->idx || !cache->teacher_logp) return OPD_ERR_NULL;
+    ids = cache->idx;
+    K = k;
+  } else if (est_mc(estimator)) {
+    if (!cache->sampled_ids || !cache->teacher_logp || !cache->behav_logp) return OPD_ERR_NULL;
+    ids = cache->sampled_ids;
+    K = M;
+  } else {
+    if (!cache->teacher_logits) return OPD_ERR_NULL;
+  }
+
+  if (!aligned16(logits) || !aligned16(dlogits)) return OPD_ERR_ALIGN;
+  if (est_dense(estimator) && !aligned16(cache->teacher_logits)) return OPD_ERR_ALIGN;
+  if ((ld * elt_bytes(dtype)) % 16 != 0) return OPD_ERR_ALIGN;
+  if ((ld * elt_bytes(o.dlogits_dtype)) % 16 != 0) return OPD_ERR_ALIGN;
+
+  const int64_t nvec = nvec_of(V, dtype);
+  const int epv = elems_per_vec(dtype);
+  const int tail = (int)(V - (nvec - 1) * epv);
+
+  Plan plan{false, 1, nvec, 0};
+  if (split_wanted(N, o.flags)) {
+    const Plan sp = split_plan(N, nvec);
+    if (workspace && workspace_bytes >= sp.ws_bytes && aligned16(workspace))
+      plan = sp;
+    else if (o.flags & OPD_FLAG_FORCE_SPLITV)
+      return OPD_ERR_WORKSPACE;
+  }
+
+  Args a{};
+  a.logits = logits;
+  a.teacher = est_dense(estimator) ? cache->teacher_logits : nullptr;
+  a.N = N;
+  a.V = V;
+  a.ld = ld;
+  a.nvec = nvec;
+  a.tail = tail;
+  a.ids = ids;
+  a.tau = est_dense(estimator) ? nullptr : cache->teacher_logp;
+  a.beta = est_mc(estimator) ? cache->behav_logp : nullptr;
+  a.K = K;
+  a.mask = mask;
+  a.gamma = o.grad_scale;
+  a.skip_masked = (o.flags & OPD_FLAG_SKIP_MASKED) ? 1 : 0;
+  a.loss = loss;
+  a.dlogits = dlogits;
+  a.lse_out = lse_out;
+  a.gathered_out = est_dense(estimator) ? nullptr : gathered_out;
+  a.ws = (float*)workspace;
+  a.P = plan.P;
+  a.chunk_vec = plan.chunk_vec;
+
+  // The top-k estimators need the row itself only for lse_out.
+  const bool read_row = !est_topk(estimator) || lse_out != nullptr;
+  hipStream_t s = (hipStream_t)stream;
+  hipError_t err;
+  if (plan.split) {
+    err = opd::launch_split(a, estimator, dtype, o.dlogits_dtype, read_row, s);
+  } else {
+    Path path = Path::RowStream;
+    // register-resident rows need whole 16-byte vectors
+    if (!est_dense(estimator) && tail == epv) {
+      if (nvec <= (int64_t)opd::kSlotsSmall * opd::kRowThreads)
+        path = Path::RowResidentSmall;
+      else if (nvec <= (int64_t)opd::kSlotsLarge * opd::kRowThreads)
+        path = Path::RowResidentLarge;
+    }
+    err = opd::launch_rowwise(a, estimator, dtype, o.dlogits_dtype, path, read_row, s);
+  }
+  return err == hipSuccess ? OPD_OK : OPD_ERR_HIP;
+}
+
+int opd_validate_cache(const opd_cache* cache, int32_t estimator, int64_t N, int64_t V,
+                       int32_t k, int32_t M, int32_t* violations, void* stream) {
+  if (!valid_est(estimator)) return OPD_ERR_ESTIMATOR;
+  if (int rc = check_shape(N, V, V)) return rc;
+  if (int rc = check_support(estimator, V, k, M)) return rc;
+  if (est_dense(estimator) || N == 0) return OPD_OK;
+  if (!cache || !violations) return OPD_ERR_NULL;
+  const bool topk = est_topk(estimator);
+  const int32_t* ids = topk ? cache->idx : cache->sampled_ids;
+  if (!ids || !cache->teacher_logp || (!topk && !cache->behav_logp)) return OPD_ERR_NULL;
+  const hipError_t err =
+      opd::launch_validate(ids, cache->teacher_logp, topk ? nullptr : cache->behav_logp, N, V,
+                           topk ? k : M, topk ? 1 : 0, violations, (hipStream_t)stream);
+  return err == hipSuccess ? OPD_OK : OPD_ERR_HIP;
+}
+
+}  // extern "C"

@@ -1,0 +1,60 @@
+// Internal interface between the C-ABI layer (opd_api.cpp) and the HIP
+// kernels (opd_kernels.hip).  Not installed; the public interface is opd.h.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace opd {
+
+enum Est : int { FKL_TOPK = 0, RKL_TOPK = 1, RKL_MC1 = 2, RKL_MC = 3, FKL_DENSE = 4, RKL_DENSE = 5 };
+enum Dt : int { F32 = 0, BF16 = 1 };
+
+constexpr int kKMax = 256;
+// Row-per-workgroup kernels: one 1024-lane workgroup per token row.
+constexpr int kRowThreads = 1024;
+// Resident variants keep the whole logit row in registers between the two
+// sweeps: up to kSlotsLarge 16-byte vectors per lane.
+constexpr int kSlotsSmall = 8;
+constexpr int kSlotsLarge = 19;
+// Split-vocabulary kernels: 256 lanes per (row, chunk) workgroup.
+constexpr int kSplitThreads = 256;
+// Pass-1 partial record per (row, chunk): m, s, m_y, s_y, t_f, t_r, pad, pad.
+constexpr int kPartialFloats = 8;
+
+// Everything a kernel needs for one call.  Plain pointers and sizes.
+struct Args {
+  const void* logits;
+  const void* teacher;  // dense estimators only
+  int64_t N, V, ld;
+  int64_t nvec;         // 16-byte vectors per row covering [0, V)
+  int tail;             // valid elements in the last vector (== elements per vector if full)
+  const int32_t* ids;   // [N, K]
+  const float* tau;     // [N, K]
+  const float* beta;    // [N, K] (MC only)
+  int K;
+  const uint8_t* mask;  // nullable
+  float gamma;
+  int skip_masked;
+  float* loss;
+  void* dlogits;
+  float* lse_out;       // nullable
+  float* gathered_out;  // nullable
+  float* ws;            // split path partials [N, P, kPartialFloats]
+  int P;                // split path chunks per row
+  int64_t chunk_vec;    // split path vectors per chunk
+};
+
+enum class Path { RowResidentSmall, RowResidentLarge, RowStream, Split };
+
+// Launchers; each returns hipSuccess or the launch error.
+hipError_t launch_rowwise(const Args& a, int est, int in_dt, int out_dt, Path path, bool read_row,
+                          hipStream_t stream);
+hipError_t launch_split(const Args& a, int est, int in_dt, int out_dt, bool read_row,
+                        hipStream_t stream);
+hipError_t launch_validate(const int32_t* ids, const float* tau, const float* beta, int64_t N,
+                           int64_t V, int K, int check_dups, int32_t* violations,
+                           hipStream_t stream);
+
+}  // namespace opd

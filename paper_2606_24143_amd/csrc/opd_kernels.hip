@@ -1,0 +1,977 @@
+// HIP kernels of the learner-time OPD loss for gfx950 (MI355X).
+//
+// Per token row t (Sec. 3 notation): logits z, L = log sum_j exp(z_j),
+// log p_theta(j) = z_j - L.  Every estimator is a two-sweep computation over
+// the vocabulary:
+//   sweep 1  online max / sum-exp over V (plus, for the dense estimators, the
+//            teacher's normaliser and the two cross sums that give D_F, D_R);
+//   gather   the student logits at the cached ids;
+//   estimate one wavefront turns (L, gathered logits, cached teacher and
+//            behaviour log-probs) into the loss, a per-row coefficient C of
+//            p_theta and up to K point corrections ("spikes");
+//   sweep 2  dlogits_j = C * p_theta(j) + spikes at cached ids, or the dense
+//            gradient.
+// The work is HBM-bound (a few VALU operations per byte, no contraction), so
+// the kernels are organised around bytes: 16-byte loads and stores, one read
+// of each logit where the row fits in registers, non-temporal hints so the
+// stream does not evict anything useful from L2.
+#include <math.h>
+
+#include "opd_internal.h"
+
+namespace opd {
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kNegInf = -__builtin_huge_valf();
+// Spike filter: one bit per 16-byte vector index (mod kFilterBits).  A set
+// bit sends that vector through the exact K-entry check; false positives
+// only cost the check.
+constexpr int kFilterBits = 16384;
+constexpr int kFilterWords = kFilterBits / 32;
+
+struct InBf16 {
+  static constexpr int EPV = 8;  // elements per 16-byte vector
+  static constexpr int BYTES = 2;
+};
+struct InF32 {
+  static constexpr int EPV = 4;
+  static constexpr int BYTES = 4;
+};
+struct OutF32 {
+  static constexpr int BYTES = 4;
+};
+struct OutBf16 {
+  static constexpr int BYTES = 2;
+};
+
+constexpr bool is_mc(int e) { return e == RKL_MC || e == RKL_MC1; }
+constexpr bool is_dense(int e) { return e == FKL_DENSE || e == RKL_DENSE; }
+constexpr bool is_topk(int e) { return e == FKL_TOPK || e == RKL_TOPK; }
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// ---------------------------------------------------------------- dtype helpers
+
+template <class TI>
+__device__ __forceinline__ void unpack(const u32x4& x, float (&f)[TI::EPV]);
+template <>
+__device__ __forceinline__ void unpack<InBf16>(const u32x4& x, float (&f)[8]) {
+#pragma unroll
+  for (int d = 0; d < 4; ++d) {
+    f[2 * d] = __uint_as_float(x[d] << 16);           // element 2d: low half
+    f[2 * d + 1] = __uint_as_float(x[d] & 0xFFFF0000u);  // element 2d+1: high half
+  }
+}
+template <>
+__device__ __forceinline__ void unpack<InF32>(const u32x4& x, float (&f)[4]) {
+#pragma unroll
+  for (int d = 0; d < 4; ++d) f[d] = __uint_as_float(x[d]);
+}
+
+template <class TI>
+__device__ __forceinline__ float load_elem(const void* row, int64_t j) {
+  if constexpr (TI::BYTES == 2)
+    return __uint_as_float((uint32_t)((const uint16_t*)row)[j] << 16);
+  else
+    return ((const float*)row)[j];
+}
+
+template <class TI>
+__device__ __forceinline__ u32x4 neg_inf_vec() {
+  const uint32_t w = TI::BYTES == 2 ? 0xFF80FF80u : 0xFF800000u;
+  return u32x4{w, w, w, w};
+}
+
+// Elements [valid, EPV) of a loaded vector become -inf, so they drop out of
+// the max and the sum without a branch in the hot loop.
+template <class TI>
+__device__ __forceinline__ void mask_tail(u32x4& x, int valid) {
+#pragma unroll
+  for (int d = 0; d < 4; ++d) {
+    if constexpr (TI::BYTES == 2) {
+      if (2 * d >= valid)
+        x[d] = 0xFF80FF80u;
+      else if (2 * d + 1 >= valid)
+        x[d] = (x[d] & 0x0000FFFFu) | 0xFF800000u;
+    } else {
+      if (d >= valid) x[d] = 0xFF800000u;
+    }
+  }
+}
+
+// Empty register barrier: the compiler must assume x changed, so it re-derives
+// fp32 values from the packed row instead of keeping an unpacked copy alive
+// across sweeps (which would double the registers the row occupies).
+__device__ __forceinline__ void keep_packed(u32x4& x) { asm volatile("" : "+v"(x)); }
+
+template <class IdxT>
+__device__ __forceinline__ u32x4 ld_nt(const void* row, IdxT v) {
+  return __builtin_nontemporal_load((const u32x4*)row + v);
+}
+__device__ __forceinline__ u32x4 ld_cached(const void* row, int64_t v) {
+  return ((const u32x4*)row)[v];
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  const uint32_t a = __builtin_bit_cast(uint16_t, (__bf16)lo);
+  const uint32_t b = __builtin_bit_cast(uint16_t, (__bf16)hi);
+  return a | (b << 16);
+}
+
+// Store the EPV gradient values of vector v (elements [v*EPV, v*EPV + valid)).
+// IdxT = uint32_t lets the compiler address with a uniform row base plus a
+// 32-bit lane offset instead of a 64-bit address per vector.
+template <class TI, class TO, class IdxT>
+__device__ __forceinline__ void store_vec(void* grow, IdxT v, const float (&g)[TI::EPV],
+                                          int valid) {
+  constexpr int EPV = TI::EPV;
+  if constexpr (TO::BYTES == 4) {
+    float* p = (float*)grow + v * EPV;
+    if (valid == EPV) {
+#pragma unroll
+      for (int q = 0; q < EPV / 4; ++q)
+        __builtin_nontemporal_store(f32x4{g[4 * q], g[4 * q + 1], g[4 * q + 2], g[4 * q + 3]},
+                                    (f32x4*)p + q);
+    } else {
+      for (int e = 0; e < valid; ++e) p[e] = g[e];
+    }
+  } else {
+    uint16_t* p = (uint16_t*)grow + v * EPV;
+    if (valid == EPV) {
+      if constexpr (EPV == 8)
+        __builtin_nontemporal_store(u32x4{pack_bf16x2(g[0], g[1]), pack_bf16x2(g[2], g[3]),
+                                          pack_bf16x2(g[4], g[5]), pack_bf16x2(g[6], g[7])},
+                                    (u32x4*)p);
+      else
+        __builtin_nontemporal_store(u32x2{pack_bf16x2(g[0], g[1]), pack_bf16x2(g[2], g[3])},
+                                    (u32x2*)p);
+    } else {
+      for (int e = 0; e < valid; ++e) p[e] = __builtin_bit_cast(uint16_t, (__bf16)g[e]);
+    }
+  }
+}
+
+// ---------------------------------------------------------------- reductions
+// Butterfly reductions: every lane ends with the same value (each pairwise
+// step is commutative), and the order is fixed, so results are reproducible.
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+template <int NW>
+__device__ __forceinline__ float block_max(float v, float* red) {
+  v = wave_max(v);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  float r = red[0];
+#pragma unroll
+  for (int w = 1; w < NW; ++w) r = fmaxf(r, red[w]);
+  __syncthreads();
+  return r;
+}
+template <int NW>
+__device__ __forceinline__ float block_sum(float v, float* red) {
+  v = wave_sum(v);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  float r = red[0];
+#pragma unroll
+  for (int w = 1; w < NW; ++w) r += red[w];
+  __syncthreads();
+  return r;
+}
+
+// Running (max, sum of exp(x - max)) statistics of a row, plus, for the dense
+// estimators, those of the teacher row and the two cross sums
+//   tr = sum_j e^{z_j - mz} (z_j - y_j),   tf = sum_j e^{y_j - my} (y_j - z_j),
+// which give E_p[z - y] = tr / sz and E_q[y - z] = tf / sy.
+struct Stats {
+  float mz, sz, tr;
+  float my, sy, tf;
+};
+
+__device__ __forceinline__ Stats stats_empty() { return Stats{kNegInf, 0.f, 0.f, kNegInf, 0.f, 0.f}; }
+
+// factor exp(m_old - m_new) for rescaling a running sum; 0 for an empty sum.
+__device__ __forceinline__ float rescale(float m_old, float m_new) {
+  return m_old == kNegInf ? 0.f : fast_exp2((m_old - m_new) * kLog2e);
+}
+
+template <bool DENSE>
+__device__ __forceinline__ Stats stats_merge(const Stats& a, const Stats& b) {
+  Stats r;
+  r.mz = fmaxf(a.mz, b.mz);
+  {
+    const float fa = rescale(a.mz, r.mz), fb = rescale(b.mz, r.mz);
+    r.sz = a.sz * fa + b.sz * fb;
+    r.tr = DENSE ? a.tr * fa + b.tr * fb : 0.f;
+  }
+  if constexpr (DENSE) {
+    r.my = fmaxf(a.my, b.my);
+    const float fa = rescale(a.my, r.my), fb = rescale(b.my, r.my);
+    r.sy = a.sy * fa + b.sy * fb;
+    r.tf = a.tf * fa + b.tf * fb;
+  } else {
+    r.my = kNegInf;
+    r.sy = 0.f;
+    r.tf = 0.f;
+  }
+  return r;
+}
+
+template <bool DENSE>
+__device__ __forceinline__ Stats wave_merge(Stats s) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    Stats t;
+    t.mz = __shfl_xor(s.mz, o, 64);
+    t.sz = __shfl_xor(s.sz, o, 64);
+    t.tr = __shfl_xor(s.tr, o, 64);
+    t.my = __shfl_xor(s.my, o, 64);
+    t.sy = __shfl_xor(s.sy, o, 64);
+    t.tf = __shfl_xor(s.tf, o, 64);
+    s = stats_merge<DENSE>(s, t);
+  }
+  return s;
+}
+
+template <bool DENSE, int NW>
+__device__ __forceinline__ Stats block_merge(Stats s, Stats* red) {
+  s = wave_merge<DENSE>(s);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
+  __syncthreads();
+  Stats r = red[0];
+#pragma unroll
+  for (int w = 1; w < NW; ++w) r = stats_merge<DENSE>(r, red[w]);
+  __syncthreads();
+  return r;
+}
+
+// Fold one 16-byte vector of z (and y) into a lane's running statistics.
+template <class TI, bool DENSE>
+__device__ __forceinline__ void stats_add(Stats& s, const u32x4& xz, const u32x4& xy) {
+  constexpr int EPV = TI::EPV;
+  float fz[EPV];
+  unpack<TI>(xz, fz);
+  float vm = fz[0];
+#pragma unroll
+  for (int e = 1; e < EPV; ++e) vm = fmaxf(vm, fz[e]);
+  if constexpr (!DENSE) {
+    const float mn = fmaxf(s.mz, vm);
+    if (mn != kNegInf) {
+      float acc = s.sz * rescale(s.mz, mn);
+      const float nm = -mn * kLog2e;
+#pragma unroll
+      for (int e = 0; e < EPV; ++e) acc += fast_exp2(fmaf(fz[e], kLog2e, nm));
+      s.sz = acc;
+      s.mz = mn;
+    }
+  } else {
+    float fy[EPV];
+    unpack<TI>(xy, fy);
+    float vmy = fy[0];
+#pragma unroll
+    for (int e = 1; e < EPV; ++e) vmy = fmaxf(vmy, fy[e]);
+    const float mnz = fmaxf(s.mz, vm), mny = fmaxf(s.my, vmy);
+    if (mnz != kNegInf && mny != kNegInf) {
+      const float cz = rescale(s.mz, mnz), cy = rescale(s.my, mny);
+      float sz = s.sz * cz, tr = s.tr * cz, sy = s.sy * cy, tf = s.tf * cy;
+      const float nmz = -mnz * kLog2e, nmy = -mny * kLog2e;
+#pragma unroll
+      for (int e = 0; e < EPV; ++e) {
+        const float pz = fast_exp2(fmaf(fz[e], kLog2e, nmz));
+        const float py = fast_exp2(fmaf(fy[e], kLog2e, nmy));
+        const float d = fz[e] - fy[e];
+        // tail elements are -inf in both rows: their weight is 0 but d is
+        // NaN, so they are excluded explicitly
+        if (pz != 0.f) tr = fmaf(pz, d, tr);
+        if (py != 0.f) tf = fmaf(py, -d, tf);
+        sz += pz;
+        sy += py;
+      }
+      s.mz = mnz; s.sz = sz; s.tr = tr;
+      s.my = mny; s.sy = sy; s.tf = tf;
+    }
+  }
+}
+
+// ---------------------------------------------------------------- cache, estimator, spikes
+
+struct CacheLds {
+  int id[kKMax];  // -1 marks an id outside [0, V)
+  float z[kKMax];
+  float t[kKMax];
+  float b[kKMax];
+  float w[kKMax];  // spike weights, already scaled by gamma
+  uint32_t filter[kFilterWords];
+  float C;        // coefficient of p_theta in the gradient row
+  int bad;        // the row has an id outside [0, V)
+};
+
+// Wave 0: read the row's cache entries and gather the student logits there.
+template <class TI>
+__device__ __forceinline__ void load_cache(const Args& a, int64_t row, const void* zrow,
+                                           CacheLds& c) {
+  const int lane = threadIdx.x & 63;
+  const int K = a.K;
+  int bad = 0;
+  for (int i = lane; i < K; i += 64) {
+    const int32_t id = a.ids[row * K + i];
+    const bool ok = id >= 0 && (int64_t)id < a.V;
+    c.id[i] = ok ? id : -1;
+    c.z[i] = ok ? load_elem<TI>(zrow, id) : __builtin_nanf("");
+    c.t[i] = a.tau[row * K + i];
+    c.b[i] = a.beta ? a.beta[row * K + i] : 0.f;
+    bad |= ok ? 0 : 1;
+  }
+  bad = __any(bad);
+  if (lane == 0) c.bad = bad;
+}
+
+// Wave 0: the estimator arithmetic of one row.  gmu = gamma for a valid row.
+// Writes the spike weights and C into LDS and returns the loss (lane-uniform).
+template <int EST>
+__device__ __forceinline__ float estimate(int K, float L, float gmu, CacheLds& c) {
+  const int lane = threadIdx.x & 63;
+  if constexpr (is_mc(EST)) {
+    // L_m = -(1/M) sum_i rho_i sg(A_i), A_i = tau_i - log p_theta(a_i),
+    // rho_i = p_theta(a_i) / p_old(a_i)  (Sec. 5.1 L_theta^noclip; App. E)
+    float acc = 0.f;
+    for (int i = lane; i < K; i += 64) {
+      const float lp = c.z[i] - L;
+      const float A = c.t[i] - lp;
+      const float rho = expf(lp - c.b[i]);
+      const float w = rho * A;
+      c.w[i] = w;
+      acc += w;
+    }
+    const float inv_m = 1.0f / (float)K;
+    const float cc = wave_sum(acc) * inv_m;
+    for (int i = lane; i < K; i += 64) c.w[i] = -gmu * c.w[i] * inv_m;
+    if (lane == 0) c.C = gmu * cc;
+    return -cc;
+  } else {
+    // renormalised restricted KL on S (Sec. 3; App. A.1): the full-vocabulary
+    // normaliser cancels, so only the K gathered logits enter
+    float zm = kNegInf, tm = kNegInf;
+    for (int i = lane; i < K; i += 64) {
+      zm = fmaxf(zm, c.z[i]);
+      tm = fmaxf(tm, c.t[i]);
+    }
+    zm = wave_max(zm);
+    tm = wave_max(tm);
+    float sz = 0.f, st = 0.f;
+    for (int i = lane; i < K; i += 64) {
+      sz += expf(c.z[i] - zm);
+      st += expf(c.t[i] - tm);
+    }
+    const float lse_s = zm + logf(wave_sum(sz));
+    const float lse_t = tm + logf(wave_sum(st));
+    float part = 0.f;
+    for (int i = lane; i < K; i += 64) {
+      const float lpt = c.z[i] - lse_s, lqt = c.t[i] - lse_t;
+      part += EST == FKL_TOPK ? expf(lqt) * (lqt - lpt) : expf(lpt) * (lpt - lqt);
+    }
+    const float kl = wave_sum(part);
+    for (int i = lane; i < K; i += 64) {
+      const float lpt = c.z[i] - lse_s, lqt = c.t[i] - lse_t;
+      const float pt = expf(lpt), qt = expf(lqt);
+      c.w[i] = EST == FKL_TOPK ? gmu * (pt - qt) : gmu * pt * ((lpt - lqt) - kl);
+    }
+    if (lane == 0) c.C = 0.f;
+    return kl;
+  }
+}
+
+template <int EPV>
+__device__ __forceinline__ void set_filter(int K, CacheLds& c) {
+  for (int i = threadIdx.x & 63; i < K; i += 64) {
+    const int id = c.id[i];
+    if (id >= 0) {
+      const int v = id / EPV;
+      atomicOr(&c.filter[(v & (kFilterBits - 1)) >> 5], 1u << (v & 31));
+    }
+  }
+}
+
+// Add the spikes that fall inside vector v, in ascending cache order.
+template <int EPV, class IdxT>
+__device__ __forceinline__ void apply_spikes(IdxT v, float (&g)[EPV], int K, const CacheLds& c) {
+  const uint32_t word = c.filter[(v & (kFilterBits - 1)) >> 5];
+  if ((word >> (v & 31)) & 1u) {
+    const int64_t base = v * EPV;
+    for (int i = 0; i < K; ++i) {
+      const int64_t off = (int64_t)c.id[i] - base;
+      if (off >= 0 && off < EPV) {
+        const float w = c.w[i];
+#pragma unroll
+        for (int e = 0; e < EPV; ++e)
+          if (off == e) g[e] += w;
+      }
+    }
+  }
+}
+
+// A masked token: zero its gradient vectors [v0, v1) (unless told to skip)
+// and, if `writer`, its per-token outputs.
+template <class TI, class TO, int NT>
+__device__ void masked_row(const Args& a, int64_t row, void* grow, int64_t v0, int64_t v1,
+                           bool writer) {
+  constexpr int EPV = TI::EPV;
+  if (!a.skip_masked) {
+    float g[EPV];
+#pragma unroll
+    for (int e = 0; e < EPV; ++e) g[e] = 0.f;
+    for (int64_t v = v0 + threadIdx.x; v < v1; v += NT)
+      store_vec<TI, TO>(grow, v, g, v == a.nvec - 1 ? a.tail : EPV);
+  }
+  if (writer) {
+    if (threadIdx.x == 0) {
+      a.loss[row] = 0.f;
+      if (a.lse_out) a.lse_out[row] = 0.f;
+    }
+    if (a.gathered_out)
+      for (int i = threadIdx.x; i < a.K; i += NT) a.gathered_out[row * a.K + i] = 0.f;
+  }
+}
+
+// Wave 0 after the statistics are known: estimator, spikes, per-token outputs.
+template <class TI, int EST>
+__device__ __forceinline__ void finish_row(const Args& a, int64_t row, float L, bool writer,
+                                           CacheLds& c) {
+  const int lane = threadIdx.x & 63;
+  const float loss = estimate<EST>(a.K, L, a.gamma, c);
+  set_filter<TI::EPV>(a.K, c);
+  if (writer) {
+    if (lane == 0) {
+      a.loss[row] = c.bad ? __builtin_nanf("") : loss;
+      if (a.lse_out) a.lse_out[row] = L;
+    }
+    if (a.gathered_out)
+      for (int i = lane; i < a.K; i += 64) a.gathered_out[row * a.K + i] = c.z[i];
+  }
+}
+
+// ---------------------------------------------------------------- row-per-workgroup kernels
+
+// One 1024-lane workgroup per token row, the whole row held in registers
+// between the sweeps (NSLOT 16-byte vectors per lane): HBM sees one read of
+// the logits and one write of the gradient.  Requires whole vectors
+// (V a multiple of the elements per vector).  READ = false is the top-k
+// write-only form (nothing of the row but the K cached logits is needed).
+template <class TI, class TO, int EST, bool READ, int NSLOT>
+__global__ void __launch_bounds__(kRowThreads) k_row_resident(Args a) {
+  constexpr int NT = kRowThreads, NW = NT / 64, EPV = TI::EPV;
+  static_assert(!is_dense(EST), "dense estimators stream two rows");
+  __shared__ float s_red[NW];
+  __shared__ CacheLds c;
+  const int tid = threadIdx.x;
+  const int64_t row = blockIdx.x;
+  const void* zrow = (const char*)a.logits + row * a.ld * TI::BYTES;
+  void* grow = (char*)a.dlogits + row * a.ld * TO::BYTES;
+  if (a.mask && a.mask[row] == 0) {
+    masked_row<TI, TO, NT>(a, row, grow, 0, a.nvec, true);
+    return;
+  }
+  for (int w = tid; w < kFilterWords; w += NT) c.filter[w] = 0u;
+  const uint32_t nvec = (uint32_t)a.nvec;  // <= NSLOT * NT when READ
+  const int K = a.K;
+
+  // The first 64 cache entries are requested before the row, so the
+  // dependent gather below does not wait behind the whole row.
+  int32_t id0 = 0;
+  float t0 = 0.f, b0 = 0.f;
+  if (tid < K && tid < 64) {
+    id0 = a.ids[row * K + tid];
+    t0 = a.tau[row * K + tid];
+    if (a.beta) b0 = a.beta[row * K + tid];
+  }
+
+  u32x4 x[READ ? NSLOT : 1];
+  if constexpr (READ) {
+    // Unconditional loads (lanes past the row end re-read its last vector
+    // and then discard it), so the wait counts stay exact.
+#pragma unroll
+    for (int s = 0; s < NSLOT; ++s) {
+      const uint32_t v = (uint32_t)(s * NT + tid);
+      x[s] = ld_nt(zrow, v < nvec ? v : nvec - 1);
+    }
+  }
+  if (tid < 64) {
+    int bad = 0;
+    if (tid < K) {
+      const bool ok = id0 >= 0 && (int64_t)id0 < a.V;
+      c.id[tid] = ok ? id0 : -1;
+      c.z[tid] = ok ? load_elem<TI>(zrow, id0) : __builtin_nanf("");
+      c.t[tid] = t0;
+      c.b[tid] = b0;
+      bad = ok ? 0 : 1;
+    }
+    for (int i = tid + 64; i < K; i += 64) {
+      const int32_t id = a.ids[row * K + i];
+      const bool ok = id >= 0 && (int64_t)id < a.V;
+      c.id[i] = ok ? id : -1;
+      c.z[i] = ok ? load_elem<TI>(zrow, id) : __builtin_nanf("");
+      c.t[i] = a.tau[row * K + i];
+      c.b[i] = a.beta ? a.beta[row * K + i] : 0.f;
+      bad |= ok ? 0 : 1;
+    }
+    bad = __any(bad);
+    if (tid == 0) c.bad = bad;
+  }
+
+  float L = 0.f;
+  if constexpr (READ) {
+#pragma unroll
+    for (int s = 0; s < NSLOT; ++s)
+      if ((uint32_t)(s * NT + tid) >= nvec) x[s] = neg_inf_vec<TI>();
+    // sweep 1a: row max (EPV independent chains)
+    float mx[EPV];
+#pragma unroll
+    for (int e = 0; e < EPV; ++e) mx[e] = kNegInf;
+#pragma unroll
+    for (int s = 0; s < NSLOT; ++s) {
+      float f[EPV];
+      unpack<TI>(x[s], f);
+#pragma unroll
+      for (int e = 0; e < EPV; ++e) mx[e] = fmaxf(mx[e], f[e]);
+    }
+    float m = mx[0];
+#pragma unroll
+    for (int e = 1; e < EPV; ++e) m = fmaxf(m, mx[e]);
+#pragma unroll
+    for (int s = 0; s < NSLOT; ++s) keep_packed(x[s]);
+    m = block_max<NW>(m, s_red);
+    // sweep 1b: sum of exp(z - m) over the registers
+    const float nm = -m * kLog2e;
+    float sm[EPV];
+#pragma unroll
+    for (int e = 0; e < EPV; ++e) sm[e] = 0.f;
+#pragma unroll
+    for (int s = 0; s < NSLOT; ++s) {
+      float f[EPV];
+      unpack<TI>(x[s], f);
+#pragma unroll
+      for (int e = 0; e < EPV; ++e) sm[e] += fast_exp2(fmaf(f[e], kLog2e, nm));
+    }
+    float ssum = 0.f;
+#pragma unroll
+    for (int e = 0; e < EPV; ++e) ssum += sm[e];
+#pragma unroll
+    for (int s = 0; s < NSLOT; ++s) keep_packed(x[s]);
+    ssum = block_sum<NW>(ssum, s_red);
+    L = m + logf(ssum);
+  } else {
+    __syncthreads();
+  }
+
+  if (tid < 64) finish_row<TI, EST>(a, row, L, true, c);
+  __syncthreads();
+  const float C = c.C;
+  const bool bad = c.bad != 0;
+  const float nL = -L * kLog2e;
+
+  // sweep 2: gradient row
+  if constexpr (READ) {
+#pragma unroll
+    for (int s = 0; s < NSLOT; ++s) {
+      const uint32_t v = (uint32_t)(s * NT + tid);
+      if (v < nvec) {
+        float g[EPV];
+        if constexpr (is_mc(EST)) {
+          float f[EPV];
+          unpack<TI>(x[s], f);
+#pragma unroll
+          for (int e = 0; e < EPV; ++e) g[e] = C * fast_exp2(fmaf(f[e], kLog2e, nL));
+        } else {
+#pragma unroll
+          for (int e = 0; e < EPV; ++e) g[e] = 0.f;
+        }
+        apply_spikes<EPV>(v, g, K, c);
+        if (bad)
+#pragma unroll
+          for (int e = 0; e < EPV; ++e) g[e] = __builtin_nanf("");
+        store_vec<TI, TO>(grow, v, g, EPV);
+      }
+    }
+  } else {
+    for (int64_t v = tid; v < a.nvec; v += NT) {
+      float g[EPV];
+#pragma unroll
+      for (int e = 0; e < EPV; ++e) g[e] = bad ? __builtin_nanf("") : 0.f;
+      if (!bad) apply_spikes<EPV>(v, g, K, c);
+      store_vec<TI, TO>(grow, v, g, v == a.nvec - 1 ? a.tail : EPV);
+    }
+  }
+}
+
+// Sweep-1 statistics of vectors [v0, v1) of a row, one lane's share
+// (stride NT), with two loads in flight per step.
+template <class TI, bool DENSE, int NT>
+__device__ __forceinline__ Stats lane_stats(const void* zrow, const void* yrow, int64_t v0,
+                                            int64_t v1, int64_t nvec, int tail) {
+  constexpr int EPV = TI::EPV;
+  Stats s = stats_empty();
+  int64_t v = v0 + threadIdx.x;
+  for (; v + NT < v1; v += 2 * NT) {
+    u32x4 z0 = ld_cached(zrow, v), z1 = ld_cached(zrow, v + NT);
+    u32x4 y0 = z0, y1 = z1;
+    if constexpr (DENSE) {
+      y0 = ld_cached(yrow, v);
+      y1 = ld_cached(yrow, v + NT);
+    }
+    if (tail != EPV && v + NT == nvec - 1) {
+      mask_tail<TI>(z1, tail);
+      if constexpr (DENSE) mask_tail<TI>(y1, tail);
+    }
+    stats_add<TI, DENSE>(s, z0, y0);
+    stats_add<TI, DENSE>(s, z1, y1);
+  }
+  if (v < v1) {
+    u32x4 z0 = ld_cached(zrow, v), y0 = z0;
+    if constexpr (DENSE) y0 = ld_cached(yrow, v);
+    if (tail != EPV && v == nvec - 1) {
+      mask_tail<TI>(z0, tail);
+      if constexpr (DENSE) mask_tail<TI>(y0, tail);
+    }
+    stats_add<TI, DENSE>(s, z0, y0);
+  }
+  return s;
+}
+
+// Per-row constants of the dense estimators from the merged statistics.
+struct DenseRow {
+  float Lz, Ly;  // log-partitions of student and teacher rows
+  float ez;      // E_p[z - y]
+  float loss;
+};
+template <int EST>
+__device__ __forceinline__ DenseRow dense_row(const Stats& s) {
+  DenseRow d;
+  d.Lz = s.mz + logf(s.sz);
+  d.Ly = s.my + logf(s.sy);
+  d.ez = s.tr / s.sz;
+  // D_R = E_p[(z - Lz) - (y - Ly)],  D_F = E_q[(y - Ly) - (z - Lz)]
+  d.loss = EST == RKL_DENSE ? d.ez + (d.Ly - d.Lz) : s.tf / s.sy + (d.Lz - d.Ly);
+  return d;
+}
+
+// Gradient values of one vector for the dense estimators:
+//   forward  g = gamma (p - q);   reverse  g = gamma p ((z - y) - E_p[z - y]),
+// the softmax-Jacobian form of eq. reverse-kl-gradient.
+template <class TI, int EST>
+__device__ __forceinline__ void dense_grad(const u32x4& xz, const u32x4& xy, const DenseRow& d,
+                                           float gamma, float (&g)[TI::EPV]) {
+  float fz[TI::EPV], fy[TI::EPV];
+  unpack<TI>(xz, fz);
+  unpack<TI>(xy, fy);
+  const float nLz = -d.Lz * kLog2e, nLy = -d.Ly * kLog2e;
+#pragma unroll
+  for (int e = 0; e < TI::EPV; ++e) {
+    const float p = fast_exp2(fmaf(fz[e], kLog2e, nLz));
+    if constexpr (EST == FKL_DENSE)
+      g[e] = gamma * (p - fast_exp2(fmaf(fy[e], kLog2e, nLy)));
+    else
+      g[e] = gamma * p * ((fz[e] - fy[e]) - d.ez);
+  }
+}
+
+// One 1024-lane workgroup per row, streaming: sweep 1 reads the row(s),
+// sweep 2 reads them again (plain loads, so the second read can hit L2 or the
+// Infinity Cache).  For rows wider than the registers hold, and for the dense
+// estimators, which read two rows.
+template <class TI, class TO, int EST, bool READ>
+__global__ void __launch_bounds__(kRowThreads) k_row_stream(Args a) {
+  constexpr int NT = kRowThreads, NW = NT / 64, EPV = TI::EPV;
+  constexpr bool DENSE = is_dense(EST);
+  __shared__ Stats s_red[NW];
+  __shared__ CacheLds c;
+  const int tid = threadIdx.x;
+  const int64_t row = blockIdx.x;
+  const void* zrow = (const char*)a.logits + row * a.ld * TI::BYTES;
+  const void* yrow = DENSE ? (const char*)a.teacher + row * a.ld * TI::BYTES : nullptr;
+  void* grow = (char*)a.dlogits + row * a.ld * TO::BYTES;
+  if (a.mask && a.mask[row] == 0) {
+    masked_row<TI, TO, NT>(a, row, grow, 0, a.nvec, true);
+    return;
+  }
+  if constexpr (!DENSE) {
+    for (int w = tid; w < kFilterWords; w += NT) c.filter[w] = 0u;
+    if (tid < 64) load_cache<TI>(a, row, zrow, c);
+  }
+  Stats st = stats_empty();
+  if constexpr (READ) {
+    st = lane_stats<TI, DENSE, NT>(zrow, yrow, 0, a.nvec, a.nvec, a.tail);
+    st = block_merge<DENSE, NW>(st, s_red);
+  } else {
+    __syncthreads();
+  }
+  const float L = st.mz + logf(st.sz);
+
+  if constexpr (DENSE) {
+    const DenseRow d = dense_row<EST>(st);
+    if (tid == 0) {
+      a.loss[row] = d.loss;
+      if (a.lse_out) a.lse_out[row] = d.Lz;
+    }
+    for (int64_t v = tid; v < a.nvec; v += NT) {
+      float g[EPV];
+      dense_grad<TI, EST>(ld_cached(zrow, v), ld_cached(yrow, v), d, a.gamma, g);
+      store_vec<TI, TO>(grow, v, g, v == a.nvec - 1 ? a.tail : EPV);
+    }
+  } else {
+    if (tid < 64) finish_row<TI, EST>(a, row, L, true, c);
+    __syncthreads();
+    const float C = c.C;
+    const bool bad = c.bad != 0;
+    const float nL = -L * kLog2e;
+    for (int64_t v = tid; v < a.nvec; v += NT) {
+      float g[EPV];
+      if constexpr (is_mc(EST)) {
+        float f[EPV];
+        unpack<TI>(ld_cached(zrow, v), f);
+#pragma unroll
+        for (int e = 0; e < EPV; ++e) g[e] = C * fast_exp2(fmaf(f[e], kLog2e, nL));
+      } else {
+#pragma unroll
+        for (int e = 0; e < EPV; ++e) g[e] = 0.f;
+      }
+      apply_spikes<EPV>(v, g, a.K, c);
+      if (bad)
+#pragma unroll
+        for (int e = 0; e < EPV; ++e) g[e] = __builtin_nanf("");
+      store_vec<TI, TO>(grow, v, g, v == a.nvec - 1 ? a.tail : EPV);
+    }
+  }
+}
+
+// ---------------------------------------------------------------- split-vocabulary kernels
+// For small N a row is cut into P chunks of whole 16-byte vectors, one
+// 256-lane workgroup each.  Pass 1 writes per-chunk statistics; pass 2
+// merges the P records of its row in a fixed order (the same in every chunk
+// of the row, so every chunk sees bit-identical row constants), repeats the
+// K-entry estimator, and writes its chunk of the gradient.
+
+template <class TI, bool DENSE>
+__global__ void __launch_bounds__(kSplitThreads) k_split_stats(Args a) {
+  constexpr int NT = kSplitThreads, NW = NT / 64;
+  __shared__ Stats s_red[NW];
+  const int64_t row = blockIdx.x / a.P;
+  const int chunk = (int)(blockIdx.x % a.P);
+  if (a.mask && a.mask[row] == 0) return;
+  const int64_t v0 = (int64_t)chunk * a.chunk_vec;
+  const int64_t v1 = v0 + a.chunk_vec < a.nvec ? v0 + a.chunk_vec : a.nvec;
+  const void* zrow = (const char*)a.logits + row * a.ld * TI::BYTES;
+  const void* yrow = DENSE ? (const char*)a.teacher + row * a.ld * TI::BYTES : nullptr;
+  Stats st = lane_stats<TI, DENSE, NT>(zrow, yrow, v0, v1, a.nvec, a.tail);
+  st = block_merge<DENSE, NW>(st, s_red);
+  if (threadIdx.x == 0) {
+    float* p = a.ws + ((size_t)row * a.P + chunk) * kPartialFloats;
+    p[0] = st.mz; p[1] = st.sz; p[2] = st.tr;
+    p[3] = st.my; p[4] = st.sy; p[5] = st.tf;
+  }
+}
+
+template <class TI, class TO, int EST, bool READ>
+__global__ void __launch_bounds__(kSplitThreads) k_split_write(Args a) {
+  constexpr int NT = kSplitThreads, EPV = TI::EPV;
+  constexpr bool DENSE = is_dense(EST);
+  __shared__ CacheLds c;
+  __shared__ Stats s_row;
+  const int tid = threadIdx.x;
+  const int64_t row = blockIdx.x / a.P;
+  const int chunk = (int)(blockIdx.x % a.P);
+  const int64_t v0 = (int64_t)chunk * a.chunk_vec;
+  const int64_t v1 = v0 + a.chunk_vec < a.nvec ? v0 + a.chunk_vec : a.nvec;
+  const void* zrow = (const char*)a.logits + row * a.ld * TI::BYTES;
+  const void* yrow = DENSE ? (const char*)a.teacher + row * a.ld * TI::BYTES : nullptr;
+  void* grow = (char*)a.dlogits + row * a.ld * TO::BYTES;
+  if (a.mask && a.mask[row] == 0) {
+    masked_row<TI, TO, NT>(a, row, grow, v0, v1, chunk == 0);
+    return;
+  }
+  if constexpr (!DENSE) {
+    for (int w = tid; w < kFilterWords; w += NT) c.filter[w] = 0u;
+  }
+  if (tid < 64) {
+    if constexpr (!DENSE) load_cache<TI>(a, row, zrow, c);
+    if constexpr (READ) {
+      Stats s = stats_empty();
+      if (tid < a.P) {
+        const float* p = a.ws + ((size_t)row * a.P + tid) * kPartialFloats;
+        s = Stats{p[0], p[1], p[2], p[3], p[4], p[5]};
+      }
+      s = wave_merge<DENSE>(s);
+      if (tid == 0) s_row = s;
+    }
+  }
+  __syncthreads();
+  const Stats st = READ ? s_row : stats_empty();
+  const float L = st.mz + logf(st.sz);
+  if constexpr (DENSE) {
+    const DenseRow d = dense_row<EST>(st);
+    if (chunk == 0 && tid == 0) {
+      a.loss[row] = d.loss;
+      if (a.lse_out) a.lse_out[row] = d.Lz;
+    }
+    for (int64_t v = v0 + tid; v < v1; v += NT) {
+      float g[EPV];
+      dense_grad<TI, EST>(ld_cached(zrow, v), ld_cached(yrow, v), d, a.gamma, g);
+      store_vec<TI, TO>(grow, v, g, v == a.nvec - 1 ? a.tail : EPV);
+    }
+  } else {
+    if (tid < 64) finish_row<TI, EST>(a, row, L, chunk == 0, c);
+    __syncthreads();
+    const float C = c.C;
+    const bool bad = c.bad != 0;
+    const float nL = -L * kLog2e;
+    for (int64_t v = v0 + tid; v < v1; v += NT) {
+      float g[EPV];
+      if constexpr (is_mc(EST)) {
+        float f[EPV];
+        unpack<TI>(ld_cached(zrow, v), f);
+#pragma unroll
+        for (int e = 0; e < EPV; ++e) g[e] = C * fast_exp2(fmaf(f[e], kLog2e, nL));
+      } else {
+#pragma unroll
+        for (int e = 0; e < EPV; ++e) g[e] = 0.f;
+      }
+      apply_spikes<EPV>(v, g, a.K, c);
+      if (bad)
+#pragma unroll
+        for (int e = 0; e < EPV; ++e) g[e] = __builtin_nanf("");
+      store_vec<TI, TO>(grow, v, g, v == a.nvec - 1 ? a.tail : EPV);
+    }
+  }
+}
+
+// ---------------------------------------------------------------- cache validation
+
+__global__ void __launch_bounds__(256) k_validate(const int32_t* ids, const float* tau,
+                                                  const float* beta, int64_t V, int K,
+                                                  int check_dups, int32_t* violations) {
+  __shared__ int32_t s_ids[kKMax];
+  __shared__ int s_red[4];
+  const int64_t row = blockIdx.x;
+  const int tid = threadIdx.x;
+  int bad = 0;
+  for (int i = tid; i < K; i += 256) {
+    const int32_t id = ids[row * K + i];
+    s_ids[i] = id;
+    bad += (id < 0 || (int64_t)id >= V) ? 1 : 0;
+    bad += isfinite(tau[row * K + i]) ? 0 : 1;
+    if (beta) bad += isfinite(beta[row * K + i]) ? 0 : 1;
+  }
+  __syncthreads();
+  if (check_dups)
+    for (int i = tid; i < K; i += 256)
+      for (int j = i + 1; j < K; ++j) bad += s_ids[j] == s_ids[i] ? 1 : 0;
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) bad += __shfl_xor(bad, o, 64);
+  if ((tid & 63) == 0) s_red[tid >> 6] = bad;
+  __syncthreads();
+  if (tid == 0) {
+    const int total = s_red[0] + s_red[1] + s_red[2] + s_red[3];
+    if (total) atomicAdd(violations, total);
+  }
+}
+
+// ---------------------------------------------------------------- dispatch
+
+template <class TI, class TO, int EST>
+hipError_t row_t(const Args& a, Path path, bool read, hipStream_t s) {
+  const dim3 grid((unsigned)a.N), block(kRowThreads);
+  if constexpr (is_dense(EST)) {
+    hipLaunchKernelGGL((k_row_stream<TI, TO, EST, true>), grid, block, 0, s, a);
+  } else {
+    if (!read) {
+      if constexpr (is_topk(EST))
+        hipLaunchKernelGGL((k_row_resident<TI, TO, EST, false, 1>), grid, block, 0, s, a);
+      else
+        return hipErrorInvalidValue;
+    } else if (path == Path::RowResidentSmall) {
+      hipLaunchKernelGGL((k_row_resident<TI, TO, EST, true, kSlotsSmall>), grid, block, 0, s, a);
+    } else if (path == Path::RowResidentLarge) {
+      hipLaunchKernelGGL((k_row_resident<TI, TO, EST, true, kSlotsLarge>), grid, block, 0, s, a);
+    } else {
+      hipLaunchKernelGGL((k_row_stream<TI, TO, EST, true>), grid, block, 0, s, a);
+    }
+  }
+  return hipGetLastError();
+}
+
+template <class TI, class TO, int EST>
+hipError_t split_t(const Args& a, bool read, hipStream_t s) {
+  const dim3 grid((unsigned)(a.N * a.P)), block(kSplitThreads);
+  if (read) {
+    hipLaunchKernelGGL((k_split_stats<TI, is_dense(EST)>), grid, block, 0, s, a);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((k_split_write<TI, TO, EST, true>), grid, block, 0, s, a);
+  } else {
+    if constexpr (is_topk(EST))
+      hipLaunchKernelGGL((k_split_write<TI, TO, EST, false>), grid, block, 0, s, a);
+    else
+      return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+template <class TI, class TO, class F>
+hipError_t by_est(int est, F&& f) {
+  switch (est) {
+    case FKL_TOPK: return f.template operator()<TI, TO, FKL_TOPK>();
+    case RKL_TOPK: return f.template operator()<TI, TO, RKL_TOPK>();
+    case RKL_MC1:
+    case RKL_MC: return f.template operator()<TI, TO, RKL_MC>();
+    case FKL_DENSE: return f.template operator()<TI, TO, FKL_DENSE>();
+    case RKL_DENSE: return f.template operator()<TI, TO, RKL_DENSE>();
+  }
+  return hipErrorInvalidValue;
+}
+
+template <class F>
+hipError_t by_types(int est, int in_dt, int out_dt, F&& f) {
+  if (in_dt == BF16)
+    return out_dt == BF16 ? by_est<InBf16, OutBf16>(est, f) : by_est<InBf16, OutF32>(est, f);
+  return out_dt == BF16 ? by_est<InF32, OutBf16>(est, f) : by_est<InF32, OutF32>(est, f);
+}
+
+}  // namespace
+
+hipError_t launch_rowwise(const Args& a, int est, int in_dt, int out_dt, Path path, bool read_row,
+                          hipStream_t stream) {
+  return by_types(est, in_dt, out_dt, [&]<class TI, class TO, int EST>() {
+    return row_t<TI, TO, EST>(a, path, read_row, stream);
+  });
+}
+
+hipError_t launch_split(const Args& a, int est, int in_dt, int out_dt, bool read_row,
+                        hipStream_t stream) {
+  return by_types(est, in_dt, out_dt, [&]<class TI, class TO, int EST>() {
+    return split_t<TI, TO, EST>(a, read_row, stream);
+  });
+}
+
+hipError_t launch_validate(const int32_t* ids, const float* tau, const float* beta, int64_t N,
+                           int64_t V, int K, int check_dups, int32_t* violations,
+                           hipStream_t stream) {
+  hipLaunchKernelGGL(k_validate, dim3((unsigned)N), dim3(256), 0, stream, ids, tau, beta, V, K,
+                     check_dups, violations);
+  return hipGetLastError();
+}
+
+}  // namespace opd

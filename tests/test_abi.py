@@ -1,0 +1,143 @@
+"""The C ABI without a GPU: the library loads, exports every symbol the
+header declares, and rejects every argument error before touching the device.
+
+Each error case below has exactly one invalid argument and never reaches a
+launch (the pointers are placeholders and are never dereferenced)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+import paper_2606_24143_amd as opd
+from paper_2606_24143_amd._binding import OpdCache, OpdOpts
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "opd.h")
+
+OK, NULL, SHAPE, SUPPORT, DTYPE, ALIGN, WORKSPACE, ESTIMATOR, FLAGS = 0, -1, -2, -3, -4, -5, -6, -7, -8
+FAKE = 0x10000  # 16-byte aligned placeholder address, never dereferenced
+
+
+def header_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\*?\s+\**(opd_[a-z_]+)\(", text,
+                                 re.M)))
+
+
+def test_library_loads_and_exports_every_declared_symbol():
+    L = opd.lib()
+    declared = header_functions()
+    assert declared == sorted(opd.EXPORTS)
+    for name in declared:
+        assert hasattr(L, name), name
+    dyn = subprocess.run(["nm", "-D", "--defined-only", opd.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r" T (opd_[a-z_]+)$", dyn, re.M))
+    assert set(declared) <= exported
+
+
+def test_version_matches_header():
+    m = re.search(r"#define OPD_VERSION (\d+)", open(HEADER).read())
+    assert opd.version() == int(m.group(1))
+
+
+def test_status_strings():
+    for code in range(-9, 1):
+        s = opd.status_string(code)
+        assert s and s != "unknown status"
+    assert opd.status_string(-100) == "unknown status"
+
+
+def call(logits=FAKE, dtype=1, N=4, V=1024, ld=None, cache="mc", est=3, k=16, M=4, mask=None,
+         opts=None, loss=FAKE, dlogits=FAKE, lse=None, gathered=None, ws=None, ws_bytes=0):
+    ld = V if ld is None else ld
+    if cache == "mc":
+        c = OpdCache(None, FAKE, FAKE, FAKE, None)
+    elif cache == "topk":
+        c = OpdCache(FAKE, None, FAKE, None, None)
+    elif cache == "dense":
+        c = OpdCache(None, None, None, None, FAKE)
+    else:
+        c = cache
+    cp = None if c is None else ctypes.byref(c)
+    op = None if opts is None else ctypes.byref(opts)
+    return opd.lib().opd_loss_fwd_bwd(logits, dtype, N, V, ld, cp, est, k, M, mask, op, loss,
+                                      dlogits, lse, gathered, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(est=6), ESTIMATOR),
+    (dict(est=-1), ESTIMATOR),
+    (dict(dtype=2), DTYPE),
+    (dict(opts=OpdOpts(1.0, 7, 0)), DTYPE),
+    (dict(opts=OpdOpts(1.0, 0, 64)), FLAGS),
+    (dict(opts=OpdOpts(1.0, 0, 2 | 4)), FLAGS),
+    (dict(N=-1), SHAPE),
+    (dict(N=2 ** 31), SHAPE),
+    (dict(V=1), SHAPE),
+    (dict(V=2 ** 31), SHAPE),
+    (dict(ld=1000), SHAPE),
+    (dict(est=3, M=0), SUPPORT),
+    (dict(est=3, M=257), SUPPORT),
+    (dict(est=2, M=2), SUPPORT),
+    (dict(est=0, cache="topk", k=0), SUPPORT),
+    (dict(est=1, cache="topk", k=257, V=4096), SUPPORT),
+    (dict(est=0, cache="topk", k=9, V=8), SUPPORT),
+    (dict(logits=None), NULL),
+    (dict(loss=None), NULL),
+    (dict(dlogits=None), NULL),
+    (dict(cache=None), NULL),
+    (dict(cache=OpdCache(None, None, FAKE, FAKE, None)), NULL),
+    (dict(cache=OpdCache(None, FAKE, None, FAKE, None)), NULL),
+    (dict(cache=OpdCache(None, FAKE, FAKE, None, None)), NULL),
+    (dict(est=0, cache=OpdCache(None, FAKE, FAKE, FAKE, None)), NULL),
+    (dict(est=1, cache=OpdCache(FAKE, None, None, None, None)), NULL),
+    (dict(est=4, cache=OpdCache(FAKE, FAKE, FAKE, FAKE, None)), NULL),
+    (dict(logits=FAKE + 2), ALIGN),
+    (dict(dlogits=FAKE + 8), ALIGN),
+    (dict(est=5, cache=OpdCache(None, None, None, None, FAKE + 4)), ALIGN),
+    (dict(V=1020), ALIGN),                       # bf16 rows of 2040 bytes
+    (dict(dtype=0, V=1022), ALIGN),              # fp32 rows of 4088 bytes
+    (dict(dtype=0, V=1020, opts=OpdOpts(1.0, 1, 0)), ALIGN),  # bf16 gradient rows of 2040 bytes
+    (dict(N=8, opts=OpdOpts(1.0, 0, 4)), WORKSPACE),  # split path forced, no workspace
+    (dict(N=8, opts=OpdOpts(1.0, 0, 4), ws=FAKE, ws_bytes=16), WORKSPACE),
+])
+def test_argument_errors_are_reported_before_launch(kw, code):
+    assert call(**kw) == code
+
+
+def test_zero_rows_is_a_noop():
+    assert call(N=0, logits=None, loss=None, dlogits=None, cache=None) == OK
+
+
+def test_workspace_sizing():
+    L = opd.lib()
+    ws = L.opd_workspace_bytes
+    # small N takes the split path: N * P * 8 floats
+    b = ws(256, 151936, 1, 3, 0, 16, 0)
+    assert b > 0 and b % (256 * 32) == 0
+    P = b // (256 * 32)
+    assert 1 <= P <= 64
+    # large N or forced row-wise: none
+    assert ws(32768, 151936, 1, 3, 0, 16, 0) == 0
+    assert ws(256, 151936, 1, 3, 0, 16, 2) == 0
+    # forced split at large N
+    assert ws(32768, 151936, 1, 3, 0, 16, 4) > 0
+    # invalid arguments: 0
+    assert ws(256, 1, 1, 3, 0, 16, 0) == 0
+    assert ws(256, 151936, 1, 9, 0, 16, 0) == 0
+    assert ws(0, 151936, 1, 3, 0, 16, 0) == 0
+
+
+def test_validate_cache_argument_errors():
+    L = opd.lib()
+    c = OpdCache(FAKE, None, FAKE, None, None)
+    assert L.opd_validate_cache(ctypes.byref(c), 9, 4, 100, 4, 0, FAKE, None) == ESTIMATOR
+    assert L.opd_validate_cache(ctypes.byref(c), 0, 4, 1, 4, 0, FAKE, None) == SHAPE
+    assert L.opd_validate_cache(ctypes.byref(c), 0, 4, 100, 0, 0, FAKE, None) == SUPPORT
+    assert L.opd_validate_cache(ctypes.byref(c), 0, 4, 100, 4, 0, None, None) == NULL
+    assert L.opd_validate_cache(None, 0, 4, 100, 4, 0, FAKE, None) == NULL
+    assert L.opd_validate_cache(ctypes.byref(c), 3, 4, 100, 0, 4, FAKE, None) == NULL
+    assert L.opd_validate_cache(ctypes.byref(c), 4, 4, 100, 0, 0, FAKE, None) == OK  # dense: no-op

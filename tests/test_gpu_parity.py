@@ -1,0 +1,319 @@
+"""GPU parity: the HIP path through the C ABI against the oracle, element by
+element, on the same seeded inputs.
+
+Small shapes cover every estimator, both input dtypes, both gradient dtypes,
+every kernel path (register-resident rows, streaming rows, split
+vocabulary), ragged tails (V not a multiple of the vector width), padded row
+strides, masks, and the degenerate cases.  Full-size workloads run in the
+configuration the benchmark times and compare every row's loss and
+log-partition plus a sample of gradient rows."""
+import functools
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2606_24143_amd as opd
+import synth
+from gpu_common import (DENSE, DEV, MC, TOPK, cache_arrays, check_grad, check_loss,
+                        dlogits_f64, loss_scale, oracle_dtype, rtol_for, run_gpu, say, to_dev)
+
+pytestmark = pytest.mark.gpu
+
+ALL = TOPK + MC + DENSE
+SHAPES = {  # name: (N, V, ld)
+    "v1000": (37, 1000, 1000),
+    "v3001_tail": (19, 3001, 3008),
+    "v32000": (24, 32000, 32000),
+    "v151936": (6, 151936, 151936),
+    "v7_tail": (5, 7, 8),
+    "v200000_wide": (3, 200000, 200000),
+}
+PATHS = {"rowwise": opd.FLAG_FORCE_ROWWISE, "split": opd.FLAG_FORCE_SPLITV}
+
+
+@functools.lru_cache(maxsize=8)
+def small_inputs(shape: str, dtype: int):
+    N, V, ld = SHAPES[shape]
+    w = synth.Workload("t_" + shape, N=N, V=V, dtype=dtype, estimators=ALL, k=min(16, V), M=6,
+                       sigma_student=2.5, sigma_teacher=1.0, sigma_behaviour=0.5,
+                       dense_teacher=True, seed=7 + V + 3 * dtype)
+    d = synth.generate(w, ld=ld)
+    mask = np.ones(N, np.uint8)
+    mask[1::4] = 0
+    return w, d, mask
+
+
+def compare(name, w, d, est, out, ref, mask=None, bf16_out=False):
+    ids, tau, beta = cache_arrays(d, est)
+    check_loss(name, out["loss"].cpu().numpy(), ref["loss"],
+               loss_scale(est, ids, tau, beta, ref), rtol_for(w.dtype), mask)
+    check_grad(name, dlogits_f64(out["dlogits"]), ref["grad"], bf16_out=bf16_out)
+    if "lse" in out:
+        lse = out["lse"].cpu().numpy().astype(np.float64)
+        valid = ref["lse"] != 0
+        np.testing.assert_allclose(lse[valid], ref["lse"][valid], rtol=2e-6, atol=0,
+                                   err_msg=name + " lse")
+    if "gathered" in out:
+        g = out["gathered"].cpu().numpy().astype(np.float64)
+        assert np.array_equal(g, ref["gathered"]), name + ": gathered logits not bit-exact"
+
+
+def oracle_for(w, d, est, mask, gamma=1.0):
+    ids, tau, beta = cache_arrays(d, est)
+    return oracle.rows(est, oracle_dtype(w.dtype), d["logits"], w.V, ids=ids, tau=tau, beta=beta,
+                       teacher_logits=d.get("teacher_logits") if est in DENSE else None,
+                       mask=mask, gamma=gamma)
+
+
+@pytest.mark.parametrize("path", list(PATHS))
+@pytest.mark.parametrize("est", ALL)
+@pytest.mark.parametrize("dtype", [synth.F32, synth.BF16], ids=["f32", "bf16"])
+@pytest.mark.parametrize("shape", list(SHAPES))
+def test_parity_small(shape, dtype, est, path):
+    w, d, mask = small_inputs(shape, dtype)
+    N, V, ld = SHAPES[shape]
+    say("parity %s %s %s %s" % (shape, "bf16" if dtype else "f32", est, path))
+    logits = to_dev(d["logits"])[:, :V]
+    teacher = to_dev(d["teacher_logits"])[:, :V] if est in DENSE else None
+    ids, tau, beta = cache_arrays(d, est)
+    out = run_gpu(logits, est, ids, tau, beta, teacher, mask=mask, grad_scale=0.75,
+                  flags=PATHS[path], want_lse=True, want_gathered=est not in DENSE)
+    ref = oracle_for(w, d, est, mask, gamma=0.75)
+    compare("%s/%s/%s" % (shape, est, path), w, d, est, out, ref, mask)
+
+
+@pytest.mark.parametrize("est", ALL)
+@pytest.mark.parametrize("shape", ["v1000", "v3001_tail", "v151936"])
+def test_parity_bf16_gradient_output(shape, est):
+    w, d, mask = small_inputs(shape, synth.BF16)
+    N, V, ld = SHAPES[shape]
+    say("bf16-out %s %s" % (shape, est))
+    logits = to_dev(d["logits"])[:, :V]
+    teacher = to_dev(d["teacher_logits"])[:, :V] if est in DENSE else None
+    ids, tau, beta = cache_arrays(d, est)
+    for flags in PATHS.values():
+        out = run_gpu(logits, est, ids, tau, beta, teacher, mask=mask, flags=flags,
+                      dlogits_dtype=torch.bfloat16)
+        assert out["dlogits"].dtype == torch.bfloat16
+        compare("%s/%s/bf16out" % (shape, est), w, d, est, out, oracle_for(w, d, est, mask), mask,
+                bf16_out=True)
+
+
+@pytest.mark.parametrize("K", [1, 2, 63, 64, 65, 100, 256])
+@pytest.mark.parametrize("est", ["fkl_topk", "rkl_topk", "rkl_mc"])
+def test_support_sizes(est, K):
+    """k and M from 1 to the maximum, across the 64-entry wavefront boundary."""
+    V = 4096
+    w = synth.Workload("t_k", N=9, V=V, dtype=synth.BF16, estimators=(est,), k=K, M=K,
+                       sigma_student=2.0, sigma_behaviour=0.4, seed=100 + K)
+    d = synth.generate(w)
+    say("support %s K=%d" % (est, K))
+    ids, tau, beta = cache_arrays(d, est)
+    logits = to_dev(d["logits"])
+    for flags in PATHS.values():
+        out = run_gpu(logits, est, ids, tau, beta, flags=flags, want_lse=True, want_gathered=True)
+        compare("%s/K=%d" % (est, K), w, d, est, out, oracle_for(w, d, est, None))
+        if est in TOPK and K == 1:
+            assert not out["loss"].any() and not out["dlogits"].any()
+
+
+def test_mc_duplicate_samples_accumulate():
+    """Samples are iid with replacement (App. E): repeated ids are separate
+    terms of the average, so their gradient spikes add."""
+    V, N, M = 512, 8, 12
+    w = synth.Workload("t_dup", N=N, V=V, dtype=synth.F32, estimators=("rkl_mc",), M=M, seed=5)
+    d = synth.generate(w)
+    rng = np.random.default_rng(0)
+    ids = d["mc_ids"].copy()
+    for r in range(N):  # force repeats: 3 distinct ids repeated over 12 slots
+        ids[r] = rng.choice(rng.choice(V, 3, replace=False), M)
+    d = dict(d, mc_ids=ids)
+    say("mc duplicates")
+    for flags in PATHS.values():
+        out = run_gpu(to_dev(d["logits"]), "rkl_mc", *cache_arrays(d, "rkl_mc"), flags=flags,
+                      want_gathered=True)
+        compare("dup", w, d, "rkl_mc", out, oracle_for(w, d, "rkl_mc", None))
+
+
+def test_topk_gradient_zero_pattern_is_exact():
+    """Top-k gradients are exactly zero off the cached support (App. A.1)."""
+    w, d, mask = small_inputs("v32000", synth.BF16)
+    say("topk zero pattern")
+    for est in TOPK:
+        for flags in PATHS.values():
+            out = run_gpu(to_dev(d["logits"]), est, *cache_arrays(d, est), flags=flags)
+            g = out["dlogits"].cpu().numpy()
+            support = np.zeros_like(g, dtype=bool)
+            np.put_along_axis(support, d["topk_idx"].astype(np.int64), True, axis=1)
+            assert not g[~support].any()
+            assert np.count_nonzero(g[support]) > 0.9 * support.sum()
+
+
+def test_padding_columns_and_skip_masked_rows_untouched():
+    N, V, ld = 11, 1001, 1008
+    w = synth.Workload("t_pad", N=N, V=V, dtype=synth.BF16, estimators=("rkl_mc",), M=4, seed=9)
+    d = synth.generate(w, ld=ld)
+    mask = np.ones(N, np.uint8)
+    mask[[0, 5, 10]] = 0
+    say("padding / skip-masked")
+    ids, tau, beta = cache_arrays(d, "rkl_mc")
+    for flags in PATHS.values():
+        buf = torch.full((N, ld), 7.0, dtype=torch.float32, device=DEV)
+        loss = torch.empty(N, dtype=torch.float32, device=DEV)
+        out = run_gpu(to_dev(d["logits"])[:, :V], "rkl_mc", ids, tau, beta, mask=mask,
+                      flags=flags | opd.FLAG_SKIP_MASKED, out={"loss": loss, "dlogits": buf})
+        b = buf.cpu().numpy()
+        assert np.all(b[:, V:] == 7.0), "padding columns written"
+        assert np.all(b[mask == 0] == 7.0), "masked rows written despite SKIP_MASKED"
+        ref = oracle_for(w, d, "rkl_mc", mask)
+        check_loss("pad", loss.cpu().numpy(), ref["loss"],
+                   loss_scale("rkl_mc", ids, tau, beta, ref), rtol_for(w.dtype), mask)
+        keep = mask != 0
+        check_grad("pad", b[keep, :V].astype(np.float64), ref["grad"][keep])
+
+
+def test_topk_full_support_matches_dense_on_gpu():
+    """k = V: renormalised top-k equals the dense KL (App. A.1 with S = V)."""
+    N, V = 6, 256
+    w = synth.Workload("t_kv", N=N, V=V, dtype=synth.F32, estimators=(), k=V, dense_teacher=True,
+                       seed=12)
+    d = synth.generate(w)
+    say("k = V vs dense")
+    logits, teacher = to_dev(d["logits"]), to_dev(d["teacher_logits"])
+    for sparse, dense in (("fkl_topk", "fkl_dense"), ("rkl_topk", "rkl_dense")):
+        a = run_gpu(logits, sparse, d["topk_idx"], d["topk_tau"], None)
+        b = run_gpu(logits, dense, None, None, None, teacher)
+        np.testing.assert_allclose(a["loss"].cpu().numpy(), b["loss"].cpu().numpy(), rtol=1e-4,
+                                   atol=1e-5)
+        np.testing.assert_allclose(a["dlogits"].cpu().numpy(), b["dlogits"].cpu().numpy(),
+                                   atol=1e-5)
+
+
+def test_out_of_range_ids_give_nan_rows_and_are_flagged():
+    V, N = 2048, 6
+    w = synth.Workload("t_bad", N=N, V=V, dtype=synth.BF16, estimators=(), k=8, M=8, seed=3)
+    d = synth.generate(w)
+    bad_rows = [1, 4]
+    say("out-of-range ids")
+    for est in ("rkl_topk", "rkl_mc"):
+        ids, tau, beta = [None if a is None else a.copy() for a in cache_arrays(d, est)]
+        ids[1, 3] = V
+        ids[4, 0] = -5
+        for flags in PATHS.values():
+            out = run_gpu(to_dev(d["logits"]), est, ids, tau, beta, flags=flags)
+            loss = out["loss"].cpu().numpy()
+            g = out["dlogits"].cpu().numpy()
+            good = [r for r in range(N) if r not in bad_rows]
+            assert np.isnan(loss[bad_rows]).all() and np.isfinite(loss[good]).all()
+            assert np.isnan(g[bad_rows]).all() and np.isfinite(g[good]).all()
+        kw = dict(idx=to_dev(ids), teacher_logp=to_dev(tau)) if est in TOPK else dict(
+            sampled_ids=to_dev(ids), teacher_logp=to_dev(tau), behav_logp=to_dev(beta))
+        assert opd.validate_cache(est, V, **kw) == 2
+
+
+def test_validate_cache_counts_each_violation():
+    V, N, k = 1000, 5, 6
+    ids = np.tile(np.arange(k, dtype=np.int32), (N, 1))
+    tau = np.full((N, k), -2.0, np.float32)
+    beta = np.full((N, k), -2.0, np.float32)
+    say("validate cache")
+    assert opd.validate_cache("rkl_topk", V, idx=to_dev(ids), teacher_logp=to_dev(tau)) == 0
+    ids[0, 1] = ids[0, 0]           # one repeated pair
+    ids[2, :3] = 7                  # three equal ids: three pairs
+    tau[3, 2] = np.inf
+    ids[4, 5] = 1000                # out of range
+    assert opd.validate_cache("fkl_topk", V, idx=to_dev(ids), teacher_logp=to_dev(tau)) == 6
+    # MC: repeats are legal; NaN behaviour log-prob is not
+    beta[1, 1] = np.nan
+    assert opd.validate_cache("rkl_mc", V, sampled_ids=to_dev(ids), teacher_logp=to_dev(tau),
+                              behav_logp=to_dev(beta)) == 3
+
+
+def test_nan_logits_propagate_to_their_row_only():
+    w, d, _ = small_inputs("v1000", synth.F32)
+    logits = d["logits"].copy()
+    logits[2, 17] = np.nan
+    say("nan logits")
+    for est in ("rkl_mc", "fkl_dense"):
+        for flags in PATHS.values():
+            teacher = to_dev(d["teacher_logits"]) if est in DENSE else None
+            out = run_gpu(to_dev(logits), est, *cache_arrays(d, est), teacher, flags=flags)
+            loss = out["loss"].cpu().numpy()
+            assert np.isnan(loss[2]) and np.isfinite(np.delete(loss, 2)).all()
+
+
+def test_repeated_calls_are_bitwise_identical():
+    w, d, mask = small_inputs("v151936", synth.BF16)
+    say("determinism")
+    for est in ("rkl_mc", "rkl_topk", "rkl_dense"):
+        for flags in PATHS.values():
+            teacher = to_dev(d["teacher_logits"]) if est in DENSE else None
+            ids, tau, beta = cache_arrays(d, est)
+            logits = to_dev(d["logits"])
+            r = [run_gpu(logits, est, ids, tau, beta, teacher, mask=mask, flags=flags)
+                 for _ in range(3)]
+            for o in r[1:]:
+                assert torch.equal(o["loss"], r[0]["loss"])
+                assert torch.equal(o["dlogits"], r[0]["dlogits"])
+
+
+def test_empty_batch_is_a_noop():
+    say("empty batch")
+    logits = torch.empty((0, 1000), dtype=torch.bfloat16, device=DEV)
+    ids = torch.empty((0, 4), dtype=torch.int32, device=DEV)
+    f = torch.empty((0, 4), dtype=torch.float32, device=DEV)
+    out = opd.loss_fwd_bwd(logits, "rkl_mc", sampled_ids=ids, teacher_logp=f, behav_logp=f)
+    assert out["loss"].numel() == 0
+
+
+# ---------------------------------------------------------------- full-size workloads
+
+FULL = ["n512_v32000_f32_topk16_mc4", "n8192_v151936_bf16_topk32_peaked",
+        "n32768_v151936_bf16_mc1_ragged", "n32768_v151936_bf16_mc16",
+        "n256_v151936_bf16_mc16_splitv", "n16384_v151936_bf16_dense"]
+
+
+@pytest.mark.parametrize("name", FULL)
+def test_parity_full_size(name):
+    """Every row's loss and log-partition against the oracle; the gradient on
+    a sample of rows (first, last, and a seeded spread); the gradient row-sum
+    (zero for every estimator, since softmax ignores a constant shift) on
+    every row."""
+    w = synth.WORKLOADS[name]
+    say("full-size %s: generating" % name)
+    d = synth.generate(w)
+    mask = d["mask"]
+    logits = to_dev(d["logits"])
+    teacher = to_dev(d["teacher_logits"]) if w.dense_teacher else None
+    rng = np.random.default_rng(w.seed)
+    rows = np.unique(np.concatenate([[0, w.N - 1], rng.choice(w.N, min(w.N, 40), replace=False)]))
+    for est in w.estimators:
+        say("full-size %s %s" % (name, est))
+        ids, tau, beta = cache_arrays(d, est)
+        out = run_gpu(logits, est, ids, tau, beta, teacher, mask=mask, want_lse=True,
+                      want_gathered=est not in DENSE)
+        ref = oracle.rows(est, oracle_dtype(w.dtype), d["logits"], w.V, ids=ids, tau=tau,
+                          beta=beta, teacher_logits=d.get("teacher_logits"), mask=mask,
+                          want_grad=False)
+        check_loss(name + "/" + est, out["loss"].cpu().numpy(), ref["loss"],
+                   loss_scale(est, ids, tau, beta, ref), rtol_for(w.dtype), mask)
+        valid = mask != 0
+        np.testing.assert_allclose(out["lse"].cpu().numpy()[valid], ref["lse"][valid], rtol=2e-6)
+        if est not in DENSE:
+            assert np.array_equal(out["gathered"].cpu().numpy().astype(np.float64),
+                                  ref["gathered"])
+        rs = out["dlogits"].double().sum(dim=1).cpu().numpy()
+        assert np.all(np.abs(rs) < 1e-4), "gradient rows must sum to zero"
+        sub = {k: (v[rows] if isinstance(v, np.ndarray) and v.shape[:1] == (w.N,) else v)
+               for k, v in d.items()}
+        s_ids, s_tau, s_beta = cache_arrays(sub, est)
+        ref_s = oracle.rows(est, oracle_dtype(w.dtype), sub["logits"], w.V, ids=s_ids, tau=s_tau,
+                            beta=s_beta, teacher_logits=sub.get("teacher_logits"),
+                            mask=sub["mask"])
+        idx = torch.from_numpy(rows).to(DEV)
+        check_grad(name + "/" + est, dlogits_f64(out["dlogits"].index_select(0, idx)),
+                   ref_s["grad"])
+        del out
+        torch.cuda.empty_cache()
