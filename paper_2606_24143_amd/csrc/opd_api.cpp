@@ -27,7 +27,7 @@ bool est_topk(int32_t e) { return e == OPD_FKL_TOPK || e == OPD_RKL_TOPK; }
 bool est_mc(int32_t e) { return e == OPD_RKL_MC1 || e == OPD_RKL_MC; }
 bool est_dense(int32_t e) { return e == OPD_FKL_DENSE || e == OPD_RKL_DENSE; }
 int elt_bytes(int32_t dt) { return dt == OPD_BF16 ? 2 : 4; }
-int elems_per_vec(int32_t dt) { return 16 / elt_bytes(dt); }
+int elems_per_vec(int32_t) { return opd::kElemsPerVec; }
 
 int check_shape(int64_t N, int64_t V, int64_t ld) {
   if (N < 0 || N > INT32_MAX) return OPD_ERR_SHAPE;
@@ -199,9 +199,9 @@ int opd_loss_fwd_bwd(const void* logits, int32_t dtype, int64_t N, int64_t V, in
     Path path = Path::RowStream;
     // register-resident rows need whole 16-byte vectors
     if (!est_dense(estimator) && tail == epv) {
-      if (nvec <= (int64_t)opd::kSlotsSmall * opd::kRowThreads)
+      if (nvec <= (int64_t)opd::slots_small(dtype) * opd::kRowThreads)
         path = Path::RowResidentSmall;
-      else if (nvec <= (int64_t)opd::kSlotsLarge * opd::kRowThreads)
+      else if (nvec <= (int64_t)opd::slots_large(dtype) * opd::kRowThreads)
         path = Path::RowResidentLarge;
     }
     err = opd::launch_rowwise(a, estimator, dtype, o.dlogits_dtype, path, read_row, s);

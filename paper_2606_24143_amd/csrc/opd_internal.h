@@ -14,10 +14,14 @@ enum Dt : int { F32 = 0, BF16 = 1 };
 constexpr int kKMax = 256;
 // Row-per-workgroup kernels: one 1024-lane workgroup per token row.
 constexpr int kRowThreads = 1024;
+// Every lane works on vectors of 4 consecutive elements.
+constexpr int kElemsPerVec = 4;
 // Resident variants keep the whole logit row in registers between the two
-// sweeps: up to kSlotsLarge 16-byte vectors per lane.
-constexpr int kSlotsSmall = 8;
-constexpr int kSlotsLarge = 19;
+// sweeps: up to 76 VGPRs of packed row data per lane, i.e. 38 bf16 vectors
+// (8 bytes each) or 19 fp32 vectors (16 bytes each); the small variants hold
+// less than half of that for narrow rows.
+constexpr int slots_large(int dt) { return dt == BF16 ? 38 : 19; }
+constexpr int slots_small(int dt) { return dt == BF16 ? 16 : 8; }
 // Split-vocabulary kernels: 256 lanes per (row, chunk) workgroup.
 constexpr int kSplitThreads = 256;
 // Pass-1 partial record per (row, chunk): m, s, m_y, s_y, t_f, t_r, pad, pad.
@@ -28,7 +32,7 @@ struct Args {
   const void* logits;
   const void* teacher;  // dense estimators only
   int64_t N, V, ld;
-  int64_t nvec;         // 16-byte vectors per row covering [0, V)
+  int64_t nvec;         // 4-element vectors per row covering [0, V)
   int tail;             // valid elements in the last vector (== elements per vector if full)
   const int32_t* ids;   // [N, K]
   const float* tau;     // [N, K]

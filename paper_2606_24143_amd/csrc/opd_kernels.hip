@@ -12,7 +12,7 @@
 //   sweep 2  dlogits_j = C * p_theta(j) + spikes at cached ids, or the dense
 //            gradient.
 // The work is HBM-bound (a few VALU operations per byte, no contraction), so
-// the kernels are organised around bytes: 16-byte loads and stores, one read
+// the kernels are organised around bytes: wide coalesced loads and stores, one read
 // of each logit where the row fits in registers, non-temporal hints so the
 // stream does not evict anything useful from L2.
 #include <math.h>
@@ -34,13 +34,19 @@ constexpr float kNegInf = -__builtin_huge_valf();
 constexpr int kFilterBits = 16384;
 constexpr int kFilterWords = kFilterBits / 32;
 
+// Each lane handles vectors of 4 consecutive elements: 8-byte loads of bf16,
+// 16-byte loads of fp32.  The fp32 gradient of a vector is then one 16-byte
+// store, and a wavefront's store instruction covers one contiguous 1 KiB span
+// (a lane holding 8 bf16 would write 32 bytes as two half-filled stores).
 struct InBf16 {
-  static constexpr int EPV = 8;  // elements per 16-byte vector
+  static constexpr int EPV = 4;  // elements per vector
   static constexpr int BYTES = 2;
+  typedef u32x2 Vec;
 };
 struct InF32 {
   static constexpr int EPV = 4;
   static constexpr int BYTES = 4;
+  typedef u32x4 Vec;
 };
 struct OutF32 {
   static constexpr int BYTES = 4;
@@ -58,19 +64,17 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 // ---------------------------------------------------------------- dtype helpers
 
 template <class TI>
-__device__ __forceinline__ void unpack(const u32x4& x, float (&f)[TI::EPV]);
-template <>
-__device__ __forceinline__ void unpack<InBf16>(const u32x4& x, float (&f)[8]) {
+__device__ __forceinline__ void unpack(const typename TI::Vec& x, float (&f)[4]) {
+  if constexpr (TI::BYTES == 2) {
 #pragma unroll
-  for (int d = 0; d < 4; ++d) {
-    f[2 * d] = __uint_as_float(x[d] << 16);           // element 2d: low half
-    f[2 * d + 1] = __uint_as_float(x[d] & 0xFFFF0000u);  // element 2d+1: high half
+    for (int d = 0; d < 2; ++d) {
+      f[2 * d] = __uint_as_float(x[d] << 16);              // element 2d: low half
+      f[2 * d + 1] = __uint_as_float(x[d] & 0xFFFF0000u);  // element 2d+1: high half
+    }
+  } else {
+#pragma unroll
+    for (int d = 0; d < 4; ++d) f[d] = __uint_as_float(x[d]);
   }
-}
-template <>
-__device__ __forceinline__ void unpack<InF32>(const u32x4& x, float (&f)[4]) {
-#pragma unroll
-  for (int d = 0; d < 4; ++d) f[d] = __uint_as_float(x[d]);
 }
 
 template <class TI>
@@ -82,39 +86,46 @@ __device__ __forceinline__ float load_elem(const void* row, int64_t j) {
 }
 
 template <class TI>
-__device__ __forceinline__ u32x4 neg_inf_vec() {
+__device__ __forceinline__ typename TI::Vec neg_inf_vec() {
+  typename TI::Vec x;
   const uint32_t w = TI::BYTES == 2 ? 0xFF80FF80u : 0xFF800000u;
-  return u32x4{w, w, w, w};
+#pragma unroll
+  for (int d = 0; d < (int)(sizeof(x) / 4); ++d) x[d] = w;
+  return x;
 }
 
 // Elements [valid, EPV) of a loaded vector become -inf, so they drop out of
 // the max and the sum without a branch in the hot loop.
 template <class TI>
-__device__ __forceinline__ void mask_tail(u32x4& x, int valid) {
+__device__ __forceinline__ void mask_tail(typename TI::Vec& x, int valid) {
+  if constexpr (TI::BYTES == 2) {
 #pragma unroll
-  for (int d = 0; d < 4; ++d) {
-    if constexpr (TI::BYTES == 2) {
+    for (int d = 0; d < 2; ++d) {
       if (2 * d >= valid)
         x[d] = 0xFF80FF80u;
       else if (2 * d + 1 >= valid)
         x[d] = (x[d] & 0x0000FFFFu) | 0xFF800000u;
-    } else {
-      if (d >= valid) x[d] = 0xFF800000u;
     }
+  } else {
+#pragma unroll
+    for (int d = 0; d < 4; ++d)
+      if (d >= valid) x[d] = 0xFF800000u;
   }
 }
 
 // Empty register barrier: the compiler must assume x changed, so it re-derives
 // fp32 values from the packed row instead of keeping an unpacked copy alive
 // across sweeps (which would double the registers the row occupies).
-__device__ __forceinline__ void keep_packed(u32x4& x) { asm volatile("" : "+v"(x)); }
+template <class VecT>
+__device__ __forceinline__ void keep_packed(VecT& x) { asm volatile("" : "+v"(x)); }
 
-template <class IdxT>
-__device__ __forceinline__ u32x4 ld_nt(const void* row, IdxT v) {
-  return __builtin_nontemporal_load((const u32x4*)row + v);
+template <class TI, class IdxT>
+__device__ __forceinline__ typename TI::Vec ld_nt(const void* row, IdxT v) {
+  return __builtin_nontemporal_load((const typename TI::Vec*)row + v);
 }
-__device__ __forceinline__ u32x4 ld_cached(const void* row, int64_t v) {
-  return ((const u32x4*)row)[v];
+template <class TI, class IdxT>
+__device__ __forceinline__ typename TI::Vec ld_cached(const void* row, IdxT v) {
+  return ((const typename TI::Vec*)row)[v];
 }
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
@@ -123,36 +134,24 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return a | (b << 16);
 }
 
-// Store the EPV gradient values of vector v (elements [v*EPV, v*EPV + valid)).
+// Store the gradient values of vector v (elements [4v, 4v + valid)).
 // IdxT = uint32_t lets the compiler address with a uniform row base plus a
 // 32-bit lane offset instead of a 64-bit address per vector.
 template <class TI, class TO, class IdxT>
-__device__ __forceinline__ void store_vec(void* grow, IdxT v, const float (&g)[TI::EPV],
-                                          int valid) {
-  constexpr int EPV = TI::EPV;
+__device__ __forceinline__ void store_vec(void* grow, IdxT v, const float (&g)[4], int valid) {
   if constexpr (TO::BYTES == 4) {
-    float* p = (float*)grow + v * EPV;
-    if (valid == EPV) {
-#pragma unroll
-      for (int q = 0; q < EPV / 4; ++q)
-        __builtin_nontemporal_store(f32x4{g[4 * q], g[4 * q + 1], g[4 * q + 2], g[4 * q + 3]},
-                                    (f32x4*)p + q);
-    } else {
+    float* p = (float*)grow + v * 4;
+    if (valid == 4)
+      __builtin_nontemporal_store(f32x4{g[0], g[1], g[2], g[3]}, (f32x4*)p);
+    else
       for (int e = 0; e < valid; ++e) p[e] = g[e];
-    }
   } else {
-    uint16_t* p = (uint16_t*)grow + v * EPV;
-    if (valid == EPV) {
-      if constexpr (EPV == 8)
-        __builtin_nontemporal_store(u32x4{pack_bf16x2(g[0], g[1]), pack_bf16x2(g[2], g[3]),
-                                          pack_bf16x2(g[4], g[5]), pack_bf16x2(g[6], g[7])},
-                                    (u32x4*)p);
-      else
-        __builtin_nontemporal_store(u32x2{pack_bf16x2(g[0], g[1]), pack_bf16x2(g[2], g[3])},
-                                    (u32x2*)p);
-    } else {
+    uint16_t* p = (uint16_t*)grow + v * 4;
+    if (valid == 4)
+      __builtin_nontemporal_store(u32x2{pack_bf16x2(g[0], g[1]), pack_bf16x2(g[2], g[3])},
+                                  (u32x2*)p);
+    else
       for (int e = 0; e < valid; ++e) p[e] = __builtin_bit_cast(uint16_t, (__bf16)g[e]);
-    }
   }
 }
 
@@ -262,7 +261,8 @@ __device__ __forceinline__ Stats block_merge(Stats s, Stats* red) {
 
 // Fold one 16-byte vector of z (and y) into a lane's running statistics.
 template <class TI, bool DENSE>
-__device__ __forceinline__ void stats_add(Stats& s, const u32x4& xz, const u32x4& xy) {
+__device__ __forceinline__ void stats_add(Stats& s, const typename TI::Vec& xz,
+                                          const typename TI::Vec& xy) {
   constexpr int EPV = TI::EPV;
   float fz[EPV];
   unpack<TI>(xz, fz);
@@ -467,6 +467,38 @@ __device__ __forceinline__ void finish_row(const Args& a, int64_t row, float L, 
 
 // ---------------------------------------------------------------- row-per-workgroup kernels
 
+// Register slot s of a resident row covers vectors [s*NT, s*NT + NT).  A slot
+// that would run past the row end is moved back to end at it, [nvec - NT,
+// nvec), so every lane loads a vector inside the row; lanes of a moved slot
+// whose vector an earlier slot already holds are masked (slot_owns false).
+// Rows narrower than one slot use base 0 with lane offsets clamped.
+template <int NT>
+__device__ __forceinline__ uint32_t slot_base(int s, uint32_t nvec) {
+  const uint32_t b = (uint32_t)(s * NT);
+  if (b + NT <= nvec) return b;
+  return nvec >= (uint32_t)NT ? nvec - NT : 0u;
+}
+template <int NT>
+__device__ __forceinline__ bool slot_owns(int s, uint32_t base, int tid, uint32_t nvec) {
+  if ((uint32_t)(s * NT + NT) <= nvec) return true;  // a full slot: wave-uniform
+  const uint32_t v = base + (uint32_t)tid;
+  return v >= (uint32_t)(s * NT) && v < nvec;
+}
+
+// Opaque copy: values derived from it in a later sweep are recomputed there
+// (a few scalar and lane operations) instead of being kept live from an
+// earlier sweep, which would cost registers the resident row needs.
+template <class T>
+__device__ __forceinline__ T fresh_s(T x) {
+  asm volatile("" : "+s"(x));
+  return x;
+}
+template <class T>
+__device__ __forceinline__ T fresh_v(T x) {
+  asm volatile("" : "+v"(x));
+  return x;
+}
+
 // One 1024-lane workgroup per token row, the whole row held in registers
 // between the sweeps (NSLOT 16-byte vectors per lane): HBM sees one read of
 // the logits and one write of the gradient.  Requires whole vectors
@@ -500,14 +532,15 @@ __global__ void __launch_bounds__(kRowThreads) k_row_resident(Args a) {
     if (a.beta) b0 = a.beta[row * K + tid];
   }
 
-  u32x4 x[READ ? NSLOT : 1];
+  typename TI::Vec x[READ ? NSLOT : 1];
   if constexpr (READ) {
-    // Unconditional loads (lanes past the row end re-read its last vector
-    // and then discard it), so the wait counts stay exact.
+    // Unconditional loads at a wave-uniform slot base plus one lane offset,
+    // so the wait counts stay exact and one register addresses every slot.
 #pragma unroll
     for (int s = 0; s < NSLOT; ++s) {
-      const uint32_t v = (uint32_t)(s * NT + tid);
-      x[s] = ld_nt(zrow, v < nvec ? v : nvec - 1);
+      const uint32_t b = slot_base<NT>(s, nvec);
+      const uint32_t off = min((uint32_t)tid, nvec - 1 - b);
+      x[s] = ld_nt<TI>((const typename TI::Vec*)zrow + b, off);
     }
   }
   if (tid < 64) {
@@ -537,7 +570,7 @@ __global__ void __launch_bounds__(kRowThreads) k_row_resident(Args a) {
   if constexpr (READ) {
 #pragma unroll
     for (int s = 0; s < NSLOT; ++s)
-      if ((uint32_t)(s * NT + tid) >= nvec) x[s] = neg_inf_vec<TI>();
+      if (!slot_owns<NT>(s, slot_base<NT>(s, nvec), tid, nvec)) x[s] = neg_inf_vec<TI>();
     // sweep 1a: row max (EPV independent chains)
     float mx[EPV];
 #pragma unroll
@@ -586,10 +619,13 @@ __global__ void __launch_bounds__(kRowThreads) k_row_resident(Args a) {
 
   // sweep 2: gradient row
   if constexpr (READ) {
+    const uint32_t nvec2 = fresh_s(nvec);
+    const int tid2 = fresh_v(tid);
 #pragma unroll
     for (int s = 0; s < NSLOT; ++s) {
-      const uint32_t v = (uint32_t)(s * NT + tid);
-      if (v < nvec) {
+      const uint32_t b = slot_base<NT>(s, nvec2);
+      if (slot_owns<NT>(s, b, tid2, nvec2)) {
+        const uint32_t v = b + tid2;
         float g[EPV];
         if constexpr (is_mc(EST)) {
           float f[EPV];
@@ -604,7 +640,7 @@ __global__ void __launch_bounds__(kRowThreads) k_row_resident(Args a) {
         if (bad)
 #pragma unroll
           for (int e = 0; e < EPV; ++e) g[e] = __builtin_nanf("");
-        store_vec<TI, TO>(grow, v, g, EPV);
+        store_vec<TI, TO>((char*)grow + (size_t)b * EPV * TO::BYTES, (uint32_t)tid2, g, EPV);
       }
     }
   } else {
@@ -627,11 +663,11 @@ __device__ __forceinline__ Stats lane_stats(const void* zrow, const void* yrow, 
   Stats s = stats_empty();
   int64_t v = v0 + threadIdx.x;
   for (; v + NT < v1; v += 2 * NT) {
-    u32x4 z0 = ld_cached(zrow, v), z1 = ld_cached(zrow, v + NT);
-    u32x4 y0 = z0, y1 = z1;
+    typename TI::Vec z0 = ld_cached<TI>(zrow, v), z1 = ld_cached<TI>(zrow, v + NT);
+    typename TI::Vec y0 = z0, y1 = z1;
     if constexpr (DENSE) {
-      y0 = ld_cached(yrow, v);
-      y1 = ld_cached(yrow, v + NT);
+      y0 = ld_cached<TI>(yrow, v);
+      y1 = ld_cached<TI>(yrow, v + NT);
     }
     if (tail != EPV && v + NT == nvec - 1) {
       mask_tail<TI>(z1, tail);
@@ -641,8 +677,8 @@ __device__ __forceinline__ Stats lane_stats(const void* zrow, const void* yrow, 
     stats_add<TI, DENSE>(s, z1, y1);
   }
   if (v < v1) {
-    u32x4 z0 = ld_cached(zrow, v), y0 = z0;
-    if constexpr (DENSE) y0 = ld_cached(yrow, v);
+    typename TI::Vec z0 = ld_cached<TI>(zrow, v), y0 = z0;
+    if constexpr (DENSE) y0 = ld_cached<TI>(yrow, v);
     if (tail != EPV && v == nvec - 1) {
       mask_tail<TI>(z0, tail);
       if constexpr (DENSE) mask_tail<TI>(y0, tail);
@@ -673,7 +709,8 @@ __device__ __forceinline__ DenseRow dense_row(const Stats& s) {
 //   forward  g = gamma (p - q);   reverse  g = gamma p ((z - y) - E_p[z - y]),
 // the softmax-Jacobian form of eq. reverse-kl-gradient.
 template <class TI, int EST>
-__device__ __forceinline__ void dense_grad(const u32x4& xz, const u32x4& xy, const DenseRow& d,
+__device__ __forceinline__ void dense_grad(const typename TI::Vec& xz, const typename TI::Vec& xy,
+                                           const DenseRow& d,
                                            float gamma, float (&g)[TI::EPV]) {
   float fz[TI::EPV], fy[TI::EPV];
   unpack<TI>(xz, fz);
@@ -729,7 +766,7 @@ __global__ void __launch_bounds__(kRowThreads) k_row_stream(Args a) {
     }
     for (int64_t v = tid; v < a.nvec; v += NT) {
       float g[EPV];
-      dense_grad<TI, EST>(ld_cached(zrow, v), ld_cached(yrow, v), d, a.gamma, g);
+      dense_grad<TI, EST>(ld_cached<TI>(zrow, v), ld_cached<TI>(yrow, v), d, a.gamma, g);
       store_vec<TI, TO>(grow, v, g, v == a.nvec - 1 ? a.tail : EPV);
     }
   } else {
@@ -742,7 +779,7 @@ __global__ void __launch_bounds__(kRowThreads) k_row_stream(Args a) {
       float g[EPV];
       if constexpr (is_mc(EST)) {
         float f[EPV];
-        unpack<TI>(ld_cached(zrow, v), f);
+        unpack<TI>(ld_cached<TI>(zrow, v), f);
 #pragma unroll
         for (int e = 0; e < EPV; ++e) g[e] = C * fast_exp2(fmaf(f[e], kLog2e, nL));
       } else {
@@ -829,7 +866,7 @@ __global__ void __launch_bounds__(kSplitThreads) k_split_write(Args a) {
     }
     for (int64_t v = v0 + tid; v < v1; v += NT) {
       float g[EPV];
-      dense_grad<TI, EST>(ld_cached(zrow, v), ld_cached(yrow, v), d, a.gamma, g);
+      dense_grad<TI, EST>(ld_cached<TI>(zrow, v), ld_cached<TI>(yrow, v), d, a.gamma, g);
       store_vec<TI, TO>(grow, v, g, v == a.nvec - 1 ? a.tail : EPV);
     }
   } else {
@@ -842,7 +879,7 @@ __global__ void __launch_bounds__(kSplitThreads) k_split_write(Args a) {
       float g[EPV];
       if constexpr (is_mc(EST)) {
         float f[EPV];
-        unpack<TI>(ld_cached(zrow, v), f);
+        unpack<TI>(ld_cached<TI>(zrow, v), f);
 #pragma unroll
         for (int e = 0; e < EPV; ++e) g[e] = C * fast_exp2(fmaf(f[e], kLog2e, nL));
       } else {
@@ -903,9 +940,11 @@ hipError_t row_t(const Args& a, Path path, bool read, hipStream_t s) {
       else
         return hipErrorInvalidValue;
     } else if (path == Path::RowResidentSmall) {
-      hipLaunchKernelGGL((k_row_resident<TI, TO, EST, true, kSlotsSmall>), grid, block, 0, s, a);
+      constexpr int NS = slots_small(TI::BYTES == 2 ? BF16 : F32);
+      hipLaunchKernelGGL((k_row_resident<TI, TO, EST, true, NS>), grid, block, 0, s, a);
     } else if (path == Path::RowResidentLarge) {
-      hipLaunchKernelGGL((k_row_resident<TI, TO, EST, true, kSlotsLarge>), grid, block, 0, s, a);
+      constexpr int NS = slots_large(TI::BYTES == 2 ? BF16 : F32);
+      hipLaunchKernelGGL((k_row_resident<TI, TO, EST, true, NS>), grid, block, 0, s, a);
     } else {
       hipLaunchKernelGGL((k_row_stream<TI, TO, EST, true>), grid, block, 0, s, a);
     }
