@@ -193,7 +193,9 @@ int opd_loss_fwd_bwd(const void* logits, int32_t dtype, int64_t N, int64_t V, in
   const bool read_row = !est_topk(estimator) || lse_out != nullptr;
   hipStream_t s = (hipStream_t)stream;
   hipError_t err;
-  if (plan.split) {
+  if (!read_row) {
+    err = opd::launch_topk_sparse(a, estimator, dtype, o.dlogits_dtype, s);
+  } else if (plan.split) {
     err = opd::launch_split(a, estimator, dtype, o.dlogits_dtype, read_row, s);
   } else {
     Path path = Path::RowStream;

@@ -57,6 +57,7 @@ hipError_t launch_rowwise(const Args& a, int est, int in_dt, int out_dt, Path pa
                           hipStream_t stream);
 hipError_t launch_split(const Args& a, int est, int in_dt, int out_dt, bool read_row,
                         hipStream_t stream);
+hipError_t launch_topk_sparse(const Args& a, int est, int in_dt, int out_dt, hipStream_t stream);
 hipError_t launch_validate(const int32_t* ids, const float* tau, const float* beta, int64_t N,
                            int64_t V, int K, int check_dups, int32_t* violations,
                            hipStream_t stream);
