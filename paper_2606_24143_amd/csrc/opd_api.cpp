@@ -13,8 +13,11 @@ using opd::Args;
 using opd::Path;
 
 // Below this many rows the split-vocabulary path runs (when it has a
-// workspace): N rows alone give too few workgroups to keep 256 CUs streaming.
-constexpr int64_t kSplitMaxRows = 2048;
+// workspace): fewer rows than about half the 256 CUs leave the chip idle.
+// Measured on MI355X (16-sample MC, V = 151,936): split is faster at N = 16
+// and 64, the row-per-workgroup path from N = 128 up (N = 256: 54 us against
+// 64 us, since a row held in registers is read once).
+constexpr int64_t kSplitMaxRows = 128;
 // Workgroups the split path aims for, and its largest chunk count.
 constexpr int64_t kSplitTargetGroups = 8192;
 constexpr int kSplitMaxChunks = 64;
@@ -199,8 +202,8 @@ int opd_loss_fwd_bwd(const void* logits, int32_t dtype, int64_t N, int64_t V, in
     err = opd::launch_split(a, estimator, dtype, o.dlogits_dtype, read_row, s);
   } else {
     Path path = Path::RowStream;
-    // register-resident rows need whole 16-byte vectors
-    if (!est_dense(estimator) && tail == epv) {
+    // register-resident rows need whole vectors
+    if (tail == epv) {
       if (nvec <= (int64_t)opd::slots_small(dtype) * opd::kRowThreads)
         path = Path::RowResidentSmall;
       else if (nvec <= (int64_t)opd::slots_large(dtype) * opd::kRowThreads)

@@ -308,6 +308,44 @@ __device__ __forceinline__ void stats_add(Stats& s, const typename TI::Vec& xz,
   }
 }
 
+// Per-row constants of the dense estimators from the merged statistics.
+struct DenseRow {
+  float Lz, Ly;  // log-partitions of student and teacher rows
+  float ez;      // E_p[z - y]
+  float loss;
+};
+template <int EST>
+__device__ __forceinline__ DenseRow dense_row(const Stats& s) {
+  DenseRow d;
+  d.Lz = s.mz + logf(s.sz);
+  d.Ly = s.my + logf(s.sy);
+  d.ez = s.tr / s.sz;
+  // D_R = E_p[(z - Lz) - (y - Ly)],  D_F = E_q[(y - Ly) - (z - Lz)]
+  d.loss = EST == RKL_DENSE ? d.ez + (d.Ly - d.Lz) : s.tf / s.sy + (d.Lz - d.Ly);
+  return d;
+}
+
+// Gradient values of one vector for the dense estimators:
+//   forward  g = gamma (p - q);   reverse  g = gamma p ((z - y) - E_p[z - y]),
+// the softmax-Jacobian form of eq. reverse-kl-gradient.
+template <class TI, int EST>
+__device__ __forceinline__ void dense_grad(const typename TI::Vec& xz, const typename TI::Vec& xy,
+                                           const DenseRow& d,
+                                           float gamma, float (&g)[TI::EPV]) {
+  float fz[TI::EPV], fy[TI::EPV];
+  unpack<TI>(xz, fz);
+  unpack<TI>(xy, fy);
+  const float nLz = -d.Lz * kLog2e, nLy = -d.Ly * kLog2e;
+#pragma unroll
+  for (int e = 0; e < TI::EPV; ++e) {
+    const float p = fast_exp2(fmaf(fz[e], kLog2e, nLz));
+    if constexpr (EST == FKL_DENSE)
+      g[e] = gamma * (p - fast_exp2(fmaf(fy[e], kLog2e, nLy)));
+    else
+      g[e] = gamma * p * ((fz[e] - fy[e]) - d.ez);
+  }
+}
+
 // ---------------------------------------------------------------- cache, estimator, spikes
 
 struct CacheLds {
@@ -485,6 +523,23 @@ __device__ __forceinline__ bool slot_owns(int s, uint32_t base, int tid, uint32_
   return v >= (uint32_t)(s * NT) && v < nvec;
 }
 
+// Lane offset of this lane's vector within slot s (base b): the lane id for a
+// full slot, clamped to the row end for a moved or narrow one.
+template <int NT>
+__device__ __forceinline__ uint32_t slot_off(int s, uint32_t b, int tid, uint32_t nvec) {
+  if ((uint32_t)(s * NT + NT) <= nvec) return (uint32_t)tid;
+  return min((uint32_t)tid, nvec - 1 - b);
+}
+
+// Empty asm that takes y as an input and claims to modify x: work on x is
+// not started before y has arrived, so the compiler cannot compute the
+// student-only terms of every slot early and hold them until the teacher
+// data lands.
+template <class VecT>
+__device__ __forceinline__ void after(VecT& x, const VecT& y) {
+  asm volatile("" : "+v"(x) : "v"(y));
+}
+
 // Opaque copy: values derived from it in a later sweep are recomputed there
 // (a few scalar and lane operations) instead of being kept live from an
 // earlier sweep, which would cost registers the resident row needs.
@@ -538,8 +593,7 @@ __global__ void __launch_bounds__(kRowThreads) k_row_resident(Args a) {
 #pragma unroll
     for (int s = 0; s < NSLOT; ++s) {
       const uint32_t b = slot_base<NT>(s, nvec);
-      const uint32_t off = min((uint32_t)tid, nvec - 1 - b);
-      x[s] = ld_nt<TI>((const typename TI::Vec*)zrow + b, off);
+      x[s] = ld_nt<TI>((const typename TI::Vec*)zrow + b, slot_off<NT>(s, b, tid, nvec));
     }
   }
   if (tid < 64) {
@@ -643,6 +697,143 @@ __global__ void __launch_bounds__(kRowThreads) k_row_resident(Args a) {
   }
 }
 
+// Dense estimators, student row resident: one 1024-lane workgroup per row
+// holds z in registers (as k_row_resident does) and streams the teacher row
+// y twice, with cached loads.  256 rows in flight keep about 76 MB of
+// teacher rows live, which fits the 256 MB Infinity Cache, so the second
+// read of y can be served from there instead of HBM.
+constexpr int kYAhead = 4;
+
+template <class TI, class TO, int EST, int NSLOT>
+__global__ void __launch_bounds__(kRowThreads) k_row_dense_resident(Args a) {
+  constexpr int NT = kRowThreads, NW = NT / 64, EPV = TI::EPV;
+  typedef typename TI::Vec Vec;
+  __shared__ float s_red[NW];
+  __shared__ Stats s_st[NW];
+  const int tid = threadIdx.x;
+  const int64_t row = blockIdx.x;
+  const void* zrow = (const char*)a.logits + row * a.ld * TI::BYTES;
+  const void* yrow = (const char*)a.teacher + row * a.ld * TI::BYTES;
+  void* grow = (char*)a.dlogits + row * a.ld * TO::BYTES;
+  if (a.mask && a.mask[row] == 0) {
+    masked_row<TI, TO, NT>(a, row, grow, 0, a.nvec, true);
+    return;
+  }
+  const uint32_t nvec = (uint32_t)a.nvec;  // <= NSLOT * NT
+
+  Vec x[NSLOT];
+#pragma unroll
+  for (int s = 0; s < NSLOT; ++s) {
+    const uint32_t b = slot_base<NT>(s, nvec);
+    x[s] = ld_nt<TI>((const Vec*)zrow + b, slot_off<NT>(s, b, tid, nvec));
+  }
+#pragma unroll
+  for (int s = 0; s < NSLOT; ++s)
+    if (!slot_owns<NT>(s, slot_base<NT>(s, nvec), tid, nvec)) x[s] = neg_inf_vec<TI>();
+  // sweep 1a: student max over the registers
+  float mx[EPV];
+#pragma unroll
+  for (int e = 0; e < EPV; ++e) mx[e] = kNegInf;
+#pragma unroll
+  for (int s = 0; s < NSLOT; ++s) {
+    float f[EPV];
+    unpack<TI>(x[s], f);
+#pragma unroll
+    for (int e = 0; e < EPV; ++e) mx[e] = fmaxf(mx[e], f[e]);
+  }
+  float mz = mx[0];
+#pragma unroll
+  for (int e = 1; e < EPV; ++e) mz = fmaxf(mz, mx[e]);
+#pragma unroll
+  for (int s = 0; s < NSLOT; ++s) keep_packed(x[s]);
+  mz = block_max<NW>(mz, s_red);
+
+  // sweep 1b: stream y; student sums at the known max, teacher sums online.
+  // y is prefetched kYAhead slots ahead through a small ring; the scheduling
+  // barriers stop the compiler from hoisting every y load (76 more VGPRs).
+  const float nmz = -mz * kLog2e;
+  Stats st{mz, 0.f, 0.f, kNegInf, 0.f, 0.f};
+  Vec yq[kYAhead];
+  const uint32_t nvec1 = fresh_s(nvec);
+  const int tid1 = fresh_v(tid);
+#pragma unroll
+  for (int j = 0; j < kYAhead && j < NSLOT; ++j) {
+    const uint32_t b = slot_base<NT>(j, nvec1);
+    yq[j] = ld_cached<TI>((const Vec*)yrow + b, slot_off<NT>(j, b, tid1, nvec1));
+  }
+#pragma unroll
+  for (int s = 0; s < NSLOT; ++s) {
+    const uint32_t b = slot_base<NT>(s, nvec1);
+    Vec yv = yq[s % kYAhead];
+    if (s + kYAhead < NSLOT) {
+      const uint32_t bn = slot_base<NT>(s + kYAhead, nvec1);
+      yq[s % kYAhead] = ld_cached<TI>((const Vec*)yrow + bn, slot_off<NT>(s + kYAhead, bn, tid1, nvec1));
+    }
+    if (!slot_owns<NT>(s, b, tid1, nvec1)) yv = neg_inf_vec<TI>();
+    after(x[s], yv);
+    float fz[EPV], fy[EPV];
+    unpack<TI>(x[s], fz);
+    unpack<TI>(yv, fy);
+    float vmy = fy[0];
+#pragma unroll
+    for (int e = 1; e < EPV; ++e) vmy = fmaxf(vmy, fy[e]);
+    const float mny = fmaxf(st.my, vmy);
+    const bool live = mny != kNegInf;  // some teacher entry seen so far is finite
+    const float cy = rescale(st.my, mny);
+    const float nmy = live ? -mny * kLog2e : 0.f;
+    float sy = st.sy * cy, tf = st.tf * cy;
+    // branch-free: entries with zero weight (the -inf tail, or an underflow)
+    // are excluded by selects, since their difference d can be NaN
+#pragma unroll
+    for (int e = 0; e < EPV; ++e) {
+      const float pz = fast_exp2(fmaf(fz[e], kLog2e, nmz));
+      const float py = live ? fast_exp2(fmaf(fy[e], kLog2e, nmy)) : 0.f;
+      const float d = fz[e] - fy[e];
+      st.sz += pz;
+      st.tr += pz != 0.f ? pz * d : 0.f;
+      sy += py;
+      tf -= py != 0.f ? py * d : 0.f;
+    }
+    st.my = mny;
+    st.sy = sy;
+    st.tf = tf;
+    __builtin_amdgcn_sched_barrier(0);
+  }
+#pragma unroll
+  for (int s = 0; s < NSLOT; ++s) keep_packed(x[s]);
+  st = block_merge<true, NW>(st, s_st);
+  const DenseRow d = dense_row<EST>(st);
+  if (tid == 0) {
+    a.loss[row] = d.loss;
+    if (a.lse_out) a.lse_out[row] = d.Lz;
+  }
+
+  // sweep 2: gradient from the resident z and a second read of y
+  const uint32_t nvec2 = fresh_s(nvec);
+  const int tid2 = fresh_v(tid);
+#pragma unroll
+  for (int j = 0; j < kYAhead && j < NSLOT; ++j) {
+    const uint32_t b = slot_base<NT>(j, nvec2);
+    yq[j] = ld_cached<TI>((const Vec*)yrow + b, slot_off<NT>(j, b, tid2, nvec2));
+  }
+#pragma unroll
+  for (int s = 0; s < NSLOT; ++s) {
+    const uint32_t b = slot_base<NT>(s, nvec2);
+    const Vec yv = yq[s % kYAhead];
+    if (s + kYAhead < NSLOT) {
+      const uint32_t bn = slot_base<NT>(s + kYAhead, nvec2);
+      yq[s % kYAhead] = ld_cached<TI>((const Vec*)yrow + bn, slot_off<NT>(s + kYAhead, bn, tid2, nvec2));
+    }
+    after(x[s], yv);
+    if (slot_owns<NT>(s, b, tid2, nvec2)) {
+      float g[EPV];
+      dense_grad<TI, EST>(x[s], yv, d, a.gamma, g);
+      store_vec<TI, TO>((char*)grow + (size_t)b * EPV * TO::BYTES, (uint32_t)tid2, g, EPV);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
 // Sweep-1 statistics of vectors [v0, v1) of a row, one lane's share
 // (stride NT), with two loads in flight per step.
 template <class TI, bool DENSE, int NT>
@@ -675,44 +866,6 @@ __device__ __forceinline__ Stats lane_stats(const void* zrow, const void* yrow, 
     stats_add<TI, DENSE>(s, z0, y0);
   }
   return s;
-}
-
-// Per-row constants of the dense estimators from the merged statistics.
-struct DenseRow {
-  float Lz, Ly;  // log-partitions of student and teacher rows
-  float ez;      // E_p[z - y]
-  float loss;
-};
-template <int EST>
-__device__ __forceinline__ DenseRow dense_row(const Stats& s) {
-  DenseRow d;
-  d.Lz = s.mz + logf(s.sz);
-  d.Ly = s.my + logf(s.sy);
-  d.ez = s.tr / s.sz;
-  // D_R = E_p[(z - Lz) - (y - Ly)],  D_F = E_q[(y - Ly) - (z - Lz)]
-  d.loss = EST == RKL_DENSE ? d.ez + (d.Ly - d.Lz) : s.tf / s.sy + (d.Lz - d.Ly);
-  return d;
-}
-
-// Gradient values of one vector for the dense estimators:
-//   forward  g = gamma (p - q);   reverse  g = gamma p ((z - y) - E_p[z - y]),
-// the softmax-Jacobian form of eq. reverse-kl-gradient.
-template <class TI, int EST>
-__device__ __forceinline__ void dense_grad(const typename TI::Vec& xz, const typename TI::Vec& xy,
-                                           const DenseRow& d,
-                                           float gamma, float (&g)[TI::EPV]) {
-  float fz[TI::EPV], fy[TI::EPV];
-  unpack<TI>(xz, fz);
-  unpack<TI>(xy, fy);
-  const float nLz = -d.Lz * kLog2e, nLy = -d.Ly * kLog2e;
-#pragma unroll
-  for (int e = 0; e < TI::EPV; ++e) {
-    const float p = fast_exp2(fmaf(fz[e], kLog2e, nLz));
-    if constexpr (EST == FKL_DENSE)
-      g[e] = gamma * (p - fast_exp2(fmaf(fy[e], kLog2e, nLy)));
-    else
-      g[e] = gamma * p * ((fz[e] - fy[e]) - d.ez);
-  }
 }
 
 // One 1024-lane workgroup per row, streaming: sweep 1 reads the row(s),
@@ -986,7 +1139,15 @@ template <class TI, class TO, int EST>
 hipError_t row_t(const Args& a, Path path, bool read, hipStream_t s) {
   const dim3 grid((unsigned)a.N), block(kRowThreads);
   if constexpr (is_dense(EST)) {
-    hipLaunchKernelGGL((k_row_stream<TI, TO, EST>), grid, block, 0, s, a);
+    if (path == Path::RowResidentSmall) {
+      constexpr int NS = slots_small(TI::BYTES == 2 ? BF16 : F32);
+      hipLaunchKernelGGL((k_row_dense_resident<TI, TO, EST, NS>), grid, block, 0, s, a);
+    } else if (path == Path::RowResidentLarge) {
+      constexpr int NS = slots_large(TI::BYTES == 2 ? BF16 : F32);
+      hipLaunchKernelGGL((k_row_dense_resident<TI, TO, EST, NS>), grid, block, 0, s, a);
+    } else {
+      hipLaunchKernelGGL((k_row_stream<TI, TO, EST>), grid, block, 0, s, a);
+    }
   } else {
     if (!read) {
       return hipErrorInvalidValue;  // the write-only top-k form runs launch_topk_sparse

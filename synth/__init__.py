@@ -126,7 +126,7 @@ MC1_RAGGED = Workload("n32768_v151936_bf16_mc1_ragged", N=32768, V=151936, dtype
                       sigma_behaviour=0.5, rollout_len=2048, len_lo=256, len_hi=2048, seed=1003)
 MC16 = Workload("n32768_v151936_bf16_mc16", N=32768, V=151936, dtype=BF16, estimators=("rkl_mc",),
                 M=16, sigma_student=3.0, sigma_teacher=1.0, sigma_behaviour=0.5, seed=1004)
-MC16_SMALLN = MC16.replace(name="n256_v151936_bf16_mc16_splitv", N=256)
+MC16_SMALLN = MC16.replace(name="n256_v151936_bf16_mc16_smallbatch", N=256)
 DENSE = Workload("n16384_v151936_bf16_dense", N=16384, V=151936, dtype=BF16,
                  estimators=("fkl_dense", "rkl_dense"), sigma_student=3.0, sigma_teacher=1.0,
                  dense_teacher=True, seed=1005)

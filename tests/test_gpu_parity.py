@@ -272,7 +272,7 @@ def test_empty_batch_is_a_noop():
 
 FULL = ["n512_v32000_f32_topk16_mc4", "n8192_v151936_bf16_topk32_peaked",
         "n32768_v151936_bf16_mc1_ragged", "n32768_v151936_bf16_mc16",
-        "n256_v151936_bf16_mc16_splitv", "n16384_v151936_bf16_dense"]
+        "n256_v151936_bf16_mc16_smallbatch", "n16384_v151936_bf16_dense"]
 
 
 @pytest.mark.parametrize("name", FULL)
@@ -289,11 +289,16 @@ def test_parity_full_size(name):
     teacher = to_dev(d["teacher_logits"]) if w.dense_teacher else None
     rng = np.random.default_rng(w.seed)
     rows = np.unique(np.concatenate([[0, w.N - 1], rng.choice(w.N, min(w.N, 40), replace=False)]))
-    for est in w.estimators:
-        say("full-size %s %s" % (name, est))
+    # the default path (what the benchmark times); small batches also run the
+    # split-vocabulary path
+    runs = [(est, 0) for est in w.estimators]
+    if w.N <= 1024:
+        runs += [(est, opd.FLAG_FORCE_SPLITV) for est in w.estimators]
+    for est, flags in runs:
+        say("full-size %s %s flags=%d" % (name, est, flags))
         ids, tau, beta = cache_arrays(d, est)
         out = run_gpu(logits, est, ids, tau, beta, teacher, mask=mask, want_lse=True,
-                      want_gathered=est not in DENSE)
+                      want_gathered=est not in DENSE, flags=flags)
         ref = oracle.rows(est, oracle_dtype(w.dtype), d["logits"], w.V, ids=ids, tau=tau,
                           beta=beta, teacher_logits=d.get("teacher_logits"), mask=mask,
                           want_grad=False)
@@ -304,7 +309,7 @@ def test_parity_full_size(name):
         if est not in DENSE:
             assert np.array_equal(out["gathered"].cpu().numpy().astype(np.float64),
                                   ref["gathered"])
-        rs = out["dlogits"].double().sum(dim=1).cpu().numpy()
+        rs = out["dlogits"].sum(dim=1, dtype=torch.float64).cpu().numpy()
         assert np.all(np.abs(rs) < 1e-4), "gradient rows must sum to zero"
         sub = {k: (v[rows] if isinstance(v, np.ndarray) and v.shape[:1] == (w.N,) else v)
                for k, v in d.items()}
