@@ -22,9 +22,11 @@ _SRC = os.path.join(_HERE, "opd_oracle.c")
 _LIB_PATH = os.path.join(_HERE, "liboracle.so")
 
 ESTIMATORS = {"fkl_topk": 0, "rkl_topk": 1, "rkl_mc1": 2, "rkl_mc": 3, "fkl_dense": 4,
-              "rkl_dense": 5}
+              "rkl_dense": 5, "rkl_mc_clip": 6, "rkl_mc_old": 7, "rkl_mc_old_clip": 8,
+              "rkl_mc_nois": 9}
 DENSE = ("fkl_dense", "rkl_dense")
-MC = ("rkl_mc1", "rkl_mc")
+MC = ("rkl_mc1", "rkl_mc", "rkl_mc_clip", "rkl_mc_old", "rkl_mc_old_clip", "rkl_mc_nois")
+CLIP_EPS = 0.2  # the paper's PPO clip range (App. B, Table 3)
 F32, BF16 = 0, 1
 
 
@@ -49,10 +51,11 @@ def lib():
         P = ctypes.c_void_p
         i64 = ctypes.c_int64
         L.oracle_row.argtypes = [ctypes.c_int, P, P, i64, P, P, P, ctypes.c_int, ctypes.c_double,
-                                 ctypes.c_int, P, P, P, P]
+                                 ctypes.c_double, ctypes.c_int, P, P, P, P]
         L.oracle_row.restype = ctypes.c_int
         L.oracle_rows.argtypes = [ctypes.c_int, ctypes.c_int, P, P, i64, i64, i64, P, P, P,
-                                  ctypes.c_int, P, ctypes.c_double, P, P, P, P, ctypes.c_int]
+                                  ctypes.c_int, P, ctypes.c_double, ctypes.c_double, P, P, P, P,
+                                  ctypes.c_int]
         L.oracle_rows.restype = ctypes.c_int
         L.oracle_max_threads.restype = ctypes.c_int
         _lib = L
@@ -64,7 +67,7 @@ def _p(a):
 
 
 def row(est: str, z, ids=None, tau=None, beta=None, y=None, gamma: float = 1.0,
-        valid: bool = True, want_grad: bool = True):
+        valid: bool = True, want_grad: bool = True, eps: float = CLIP_EPS):
     """One token row in double.  Returns (loss, grad or None, lse, gathered or None)."""
     z = np.ascontiguousarray(z, np.float64)
     V = z.size
@@ -82,7 +85,7 @@ def row(est: str, z, ids=None, tau=None, beta=None, y=None, gamma: float = 1.0,
     grad = np.zeros(V, np.float64) if want_grad else None
     gathered = np.zeros(K, np.float64) if K else None
     rc = lib().oracle_row(ESTIMATORS[est], _p(z), _p(y), V, _p(ids), _p(tau), _p(beta), K, gamma,
-                          int(valid), _p(loss), _p(grad), _p(lse), _p(gathered))
+                          eps, int(valid), _p(loss), _p(grad), _p(lse), _p(gathered))
     if rc != 0:
         raise ValueError("oracle_row rejected its arguments (%d)" % rc)
     return float(loss[0]), grad, float(lse[0]), gathered
@@ -90,7 +93,7 @@ def row(est: str, z, ids=None, tau=None, beta=None, y=None, gamma: float = 1.0,
 
 def rows(est: str, dtype: int, logits: np.ndarray, V: int, *, ids=None, tau=None, beta=None,
          teacher_logits=None, mask=None, gamma: float = 1.0, want_grad: bool = True,
-         nthreads: int = 0) -> dict:
+         nthreads: int = 0, eps: float = CLIP_EPS) -> dict:
     """Rows of stored inputs: logits [n, ld] (uint16 bf16 bits or float32)."""
     logits = np.ascontiguousarray(logits)
     n, ld = logits.shape
@@ -107,7 +110,7 @@ def rows(est: str, dtype: int, logits: np.ndarray, V: int, *, ids=None, tau=None
     out["grad"] = np.zeros((n, V), np.float64) if want_grad else None
     out["gathered"] = np.zeros((n, K), np.float64) if K else None
     rc = lib().oracle_rows(ESTIMATORS[est], dtype, _p(logits), _p(teacher_logits), n, V, ld,
-                           _p(ids), _p(tau), _p(beta), K, _p(mask), gamma, _p(out["loss"]),
+                           _p(ids), _p(tau), _p(beta), K, _p(mask), gamma, eps, _p(out["loss"]),
                            _p(out["grad"]), _p(out["lse"]), _p(out["gathered"]), nthreads)
     if rc != 0:
         raise ValueError("oracle_rows rejected its arguments (%d)" % rc)

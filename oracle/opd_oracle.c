@@ -106,6 +106,79 @@ static void mc_rkl(const double* z, int64_t V, double L, const int32_t* ids, con
 }
 
 /*
+ * The rest of the two-by-two surrogate family of Sec. 5.1 (the equation
+ * block of the ablation), over behaviour samples a_i ~ p_old:
+ *   rho_i     = p_theta(a_i) / p_old(a_i),  rho_bar_i = clip(rho_i, 1 - eps, 1 + eps)
+ *   A_old(a)  = log q(a) - log p_old(a)     (rollout-time advantage)
+ *   A_theta(a) = log q(a) - log p_theta(a)  (recomputed under the current student)
+ *   noclip:  L = -(1/m) sum_i rho_i sg(A_i)
+ *   clip:    L = -(1/m) sum_i min(rho_i sg(A_i), rho_bar_i sg(A_i))
+ * With A held fixed, d rho_i / d z_j = rho_i (1[j = a_i] - p_j).  Where the
+ * min selects the clipped term and the clip is active, that term does not
+ * depend on z, so the sample contributes nothing; where it selects the
+ * unclipped term (ties, i.e. rho inside the clip range, count as unclipped:
+ * there both terms are the same function of z) it contributes
+ * -(1/m) A_i rho_i (1[j = a_i] - p_j).
+ */
+static void mc_surrogate(int theta_adv, int clip, const double* z, int64_t V, double L,
+                         const int32_t* ids, const double* tau, const double* beta, int M,
+                         double eps, double gamma, double* loss, double* grad) {
+  double total = 0.0; /* sum_i of the surrogate terms */
+  double c = 0.0;     /* (1/m) sum_i A_i rho_i over samples whose unclipped term is selected */
+  for (int i = 0; i < M; ++i) {
+    const double logp = z[ids[i]] - L;
+    const double A = theta_adv ? tau[i] - logp : tau[i] - beta[i];
+    const double rho = exp(logp - beta[i]);
+    const double rho_bar = fmin(fmax(rho, 1.0 - eps), 1.0 + eps);
+    const double unclipped = rho * A, clipped = rho_bar * A;
+    if (!clip || unclipped <= clipped) {
+      total += unclipped;
+      c += A * rho;
+    } else {
+      total += clipped;
+    }
+  }
+  *loss = -total / (double)M;
+  c /= (double)M;
+  if (!grad) return;
+  for (int64_t j = 0; j < V; ++j) grad[j] = gamma * c * exp(z[j] - L);
+  for (int i = 0; i < M; ++i) {
+    const double logp = z[ids[i]] - L;
+    const double A = theta_adv ? tau[i] - logp : tau[i] - beta[i];
+    const double rho = exp(logp - beta[i]);
+    const double rho_bar = fmin(fmax(rho, 1.0 - eps), 1.0 + eps);
+    if (!clip || rho * A <= rho_bar * A) grad[ids[i]] -= gamma * A * rho / (double)M;
+  }
+}
+
+/*
+ * MC without importance sampling, the ablation of App. F: the behaviour
+ * samples are used as if they had been drawn from p_theta, i.e. the
+ * on-policy estimator of App. A.2, -(1/m) sum_i A_theta(a_i) grad log p_theta(a_i),
+ * applied to p_old samples.  Its surrogate is
+ *   L = -(1/m) sum_i sg(A_theta(a_i)) log p_theta(a_i),
+ * with gradient -(1/m) sum_i A_i (1[j = a_i] - p_j).
+ */
+static void mc_no_is(const double* z, int64_t V, double L, const int32_t* ids, const double* tau,
+                     int M, double gamma, double* loss, double* grad) {
+  double total = 0.0, c = 0.0;
+  for (int i = 0; i < M; ++i) {
+    const double logp = z[ids[i]] - L;
+    const double A = tau[i] - logp;
+    total += A * logp;
+    c += A;
+  }
+  *loss = -total / (double)M;
+  c /= (double)M;
+  if (!grad) return;
+  for (int64_t j = 0; j < V; ++j) grad[j] = gamma * c * exp(z[j] - L);
+  for (int i = 0; i < M; ++i) {
+    const double A = tau[i] - (z[ids[i]] - L);
+    grad[ids[i]] -= gamma * A / (double)M;
+  }
+}
+
+/*
  * Dense full-vocabulary KL (Sec. 3):
  *   D_F = sum_a q (log q - log p_theta),   dD_F/dz_j = p_j - q_j;
  *   D_R = sum_a p_theta (log p_theta - log q),
@@ -133,13 +206,16 @@ static void dense_kl(int reverse, const double* z, const double* y, int64_t V, d
 }
 
 int oracle_row(int est, const double* z, const double* y, int64_t V, const int32_t* ids,
-               const double* tau, const double* beta, int K, double gamma, int valid,
+               const double* tau, const double* beta, int K, double gamma, double eps, int valid,
                double* loss, double* grad, double* lse, double* gathered) {
   const int dense = est == ORACLE_FKL_DENSE || est == ORACLE_RKL_DENSE;
-  if (!z || !loss || V < 1 || est < ORACLE_FKL_TOPK || est > ORACLE_RKL_DENSE) return -1;
+  const int mc = est == ORACLE_RKL_MC || est == ORACLE_RKL_MC1 || est >= ORACLE_RKL_MC_CLIP;
+  const int clip = est == ORACLE_RKL_MC_CLIP || est == ORACLE_RKL_MC_OLD_CLIP;
+  if (!z || !loss || V < 1 || est < ORACLE_FKL_TOPK || est > ORACLE_RKL_MC_NOIS) return -1;
   if (dense && !y) return -1;
   if (!dense && (K < 1 || !ids || !tau)) return -1;
-  if ((est == ORACLE_RKL_MC || est == ORACLE_RKL_MC1) && !beta) return -1;
+  if (mc && est != ORACLE_RKL_MC_NOIS && !beta) return -1;
+  if (clip && !(eps > 0.0 && isfinite(eps))) return -1;
   if (est == ORACLE_RKL_MC1 && K != 1) return -1;
   if (!dense)
     for (int i = 0; i < K; ++i)
@@ -163,6 +239,16 @@ int oracle_row(int est, const double* z, const double* y, int64_t V, const int32
     case ORACLE_RKL_MC: mc_rkl(z, V, L, ids, tau, beta, K, gamma, loss, grad); break;
     case ORACLE_FKL_DENSE: dense_kl(0, z, y, V, L, gamma, loss, grad); break;
     case ORACLE_RKL_DENSE: dense_kl(1, z, y, V, L, gamma, loss, grad); break;
+    case ORACLE_RKL_MC_CLIP:
+      mc_surrogate(1, 1, z, V, L, ids, tau, beta, K, eps, gamma, loss, grad);
+      break;
+    case ORACLE_RKL_MC_OLD:
+      mc_surrogate(0, 0, z, V, L, ids, tau, beta, K, eps, gamma, loss, grad);
+      break;
+    case ORACLE_RKL_MC_OLD_CLIP:
+      mc_surrogate(0, 1, z, V, L, ids, tau, beta, K, eps, gamma, loss, grad);
+      break;
+    case ORACLE_RKL_MC_NOIS: mc_no_is(z, V, L, ids, tau, K, gamma, loss, grad); break;
   }
   return 0;
 }
@@ -188,8 +274,8 @@ int oracle_max_threads(void) {
 
 int oracle_rows(int est, int dtype, const void* logits, const void* teacher_logits, int64_t n_rows,
                 int64_t V, int64_t ld, const int32_t* ids, const float* tau, const float* beta,
-                int K, const uint8_t* mask, double gamma, double* loss, double* grad, double* lse,
-                double* gathered, int nthreads) {
+                int K, const uint8_t* mask, double gamma, double eps, double* loss, double* grad,
+                double* lse, double* gathered, int nthreads) {
   const int dense = est == ORACLE_FKL_DENSE || est == ORACLE_RKL_DENSE;
   if (!logits || !loss || n_rows < 0 || V < 1 || ld < V) return -1;
   if (dtype != ORACLE_F32 && dtype != ORACLE_BF16) return -1;
@@ -222,7 +308,7 @@ int oracle_rows(int est, int dtype, const void* logits, const void* teacher_logi
           b[i] = beta ? (double)beta[r * K + i] : 0.0;
         }
         const int rc = oracle_row(est, z, y, V, dense ? NULL : ids + r * K, t, beta ? b : NULL,
-                                  K, gamma, mask ? mask[r] != 0 : 1, loss + r,
+                                  K, gamma, eps, mask ? mask[r] != 0 : 1, loss + r,
                                   grad ? grad + r * V : NULL, lse ? lse + r : NULL,
                                   gathered && !dense ? gathered + r * K : NULL);
         if (rc) {

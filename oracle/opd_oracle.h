@@ -18,7 +18,11 @@ enum {
   ORACLE_RKL_MC1 = 2,   /* one-sample MC, A_theta, no clip (Sec. 5.1, L_theta^noclip) */
   ORACLE_RKL_MC = 3,    /* m-sample MC average (Sec. 6.2; App. E) */
   ORACLE_FKL_DENSE = 4, /* full-vocabulary forward KL (Sec. 3, eq. dense-forward-kl) */
-  ORACLE_RKL_DENSE = 5  /* full-vocabulary reverse KL (Sec. 3, eq. dense-reverse-kl) */
+  ORACLE_RKL_DENSE = 5, /* full-vocabulary reverse KL (Sec. 3, eq. dense-reverse-kl) */
+  ORACLE_RKL_MC_CLIP = 6,     /* L_theta^clip (Sec. 5.1, two-by-two ablation) */
+  ORACLE_RKL_MC_OLD = 7,      /* L_old^noclip (Sec. 5.1) */
+  ORACLE_RKL_MC_OLD_CLIP = 8, /* L_old^clip, the PPO-style adaptation (Sec. 5.1) */
+  ORACLE_RKL_MC_NOIS = 9      /* MC without importance sampling (App. F ablation) */
 };
 
 enum { ORACLE_F32 = 0, ORACLE_BF16 = 1 };
@@ -29,11 +33,12 @@ enum { ORACLE_F32 = 0, ORACLE_BF16 = 1 };
  *   tau[K]    teacher log-probs log q(a|s) at ids (full-vocabulary normalised)
  *   beta[K]   behaviour log-probs log p_old(a|s) at ids (MC only, else NULL)
  *   gamma     gradient scale; valid = 0 marks a padded token
+ *   eps       clip range of the clipped surrogates (ignored otherwise)
  * Outputs: *loss, grad[V] (nullable), *lse (log-partition of z; nullable),
  * gathered[K] = z at ids (nullable).  Returns 0, or -1 on bad arguments
  * (id out of range, K < 1, missing input). */
 int oracle_row(int est, const double* z, const double* y, int64_t V, const int32_t* ids,
-               const double* tau, const double* beta, int K, double gamma, int valid,
+               const double* tau, const double* beta, int K, double gamma, double eps, int valid,
                double* loss, double* grad, double* lse, double* gathered);
 
 /* Rows of stored inputs (fp32, or bf16 bit patterns widened exactly), rows
@@ -43,8 +48,8 @@ int oracle_row(int est, const double* z, const double* y, int64_t V, const int32
  * (nullable).  Returns 0 or the first row error. */
 int oracle_rows(int est, int dtype, const void* logits, const void* teacher_logits, int64_t n_rows,
                 int64_t V, int64_t ld, const int32_t* ids, const float* tau, const float* beta,
-                int K, const uint8_t* mask, double gamma, double* loss, double* grad, double* lse,
-                double* gathered, int nthreads);
+                int K, const uint8_t* mask, double gamma, double eps, double* loss, double* grad,
+                double* lse, double* gathered, int nthreads);
 
 /* Number of threads oracle_rows uses for nthreads = 0. */
 int oracle_max_threads(void);

@@ -376,3 +376,141 @@ def test_rejects_bad_arguments():
         oracle.row("rkl_mc1", z, ids=[0, 1], tau=[0.0, 0.0], beta=[0.0, 0.0])  # MC1 needs M = 1
     with pytest.raises(ValueError):
         oracle.row("rkl_mc", z, ids=[0], tau=[0.0])  # MC needs behaviour log-probs
+
+
+# ---------------------------------------------------------------- surrogate family (Sec. 5.1) and App. F
+
+THETA_ADV = ("rkl_mc", "rkl_mc_clip", "rkl_mc_nois")
+
+
+def away_from_clip_kinks(z, ids, beta, eps, margin=1e-3):
+    rho = np.exp(log_softmax(z)[ids] - beta)
+    return np.all(np.abs(rho - (1 + eps)) > margin) and np.all(np.abs(rho - (1 - eps)) > margin)
+
+
+@pytest.mark.parametrize("est", ["rkl_mc_clip", "rkl_mc_old", "rkl_mc_old_clip", "rkl_mc_nois"])
+@pytest.mark.parametrize("seed", range(4))
+def test_surrogate_family_gradients_match_finite_differences(est, seed):
+    """Each surrogate is differentiated with its advantage held fixed.
+    A_theta is frozen as before; A_old = log q - log p_old does not depend on
+    the student, so plain finite differences apply.  Samples sit away from the
+    clip boundaries, where the min is not differentiable."""
+    rng = np.random.default_rng(600 + seed)
+    V, M, eps = 12, 7, 0.2
+    for _ in range(100):
+        z, _, _, ids, tau, beta = mc_inputs(rng, V, M, stale=0.9)
+        if away_from_clip_kinks(z, ids, beta, eps):
+            break
+    _, g, _, _ = oracle.row(est, z, ids=ids, tau=tau, beta=beta, eps=eps)
+    lp0 = log_softmax(z)[ids]
+
+    def f(zz):
+        t = tau + (log_softmax(zz)[ids] - lp0) if est in THETA_ADV else tau
+        return oracle.row(est, zz, ids=ids, tau=t, beta=beta, eps=eps, want_grad=False)[0]
+
+    np.testing.assert_allclose(g, fd_grad(f, z), atol=1e-8, rtol=0)
+
+
+@pytest.mark.parametrize("adv", ["theta", "old"])
+def test_clip_is_inert_when_eps_is_huge_or_ratios_are_inside(adv):
+    """The clipped surrogate equals the unclipped one when no ratio leaves
+    [1 - eps, 1 + eps] (Sec. 3, eq. ppo-style-surrogate)."""
+    clip, noclip = ("rkl_mc_clip", "rkl_mc") if adv == "theta" else ("rkl_mc_old_clip",
+                                                                       "rkl_mc_old")
+    rng = np.random.default_rng(13)
+    V, M = 20, 9
+    z, _, _, ids, tau, beta = mc_inputs(rng, V, M, stale=1.5)
+    a = oracle.row(clip, z, ids=ids, tau=tau, beta=beta, eps=1e9)
+    b = oracle.row(noclip, z, ids=ids, tau=tau, beta=beta)
+    assert a[0] == pytest.approx(b[0], rel=1e-14, abs=1e-15)
+    np.testing.assert_allclose(a[1], b[1], rtol=1e-13, atol=1e-15)
+    # behaviour log-probs within 0.05 of the student's: every rho within [0.95, 1.05]
+    beta2 = log_softmax(z)[ids] + rng.uniform(-0.05, 0.05, M)
+    rho = np.exp(log_softmax(z)[ids] - beta2)
+    assert np.all(np.abs(rho - 1) < 0.2)
+    a = oracle.row(clip, z, ids=ids, tau=tau, beta=beta2, eps=0.2)
+    b = oracle.row(noclip, z, ids=ids, tau=tau, beta=beta2)
+    assert a[0] == pytest.approx(b[0], rel=1e-14, abs=1e-15)
+    np.testing.assert_allclose(a[1], b[1], rtol=1e-13, atol=1e-15)
+
+
+@pytest.mark.parametrize("sign", [1.0, -1.0])
+def test_ppo_clip_stops_the_gradient_outside_the_trust_region(sign):
+    """One sample, advantage A: for A > 0 and rho > 1 + eps, or A < 0 and
+    rho < 1 - eps, the min selects the constant clipped term, so the loss is
+    -rho_bar A and the gradient is exactly zero; on the other side of the
+    range the unclipped term is selected and the gradient is nonzero."""
+    V, eps = 6, 0.2
+    z = np.array([0.3, -1.0, 2.0, 0.5, -0.2, 1.1])
+    lp = log_softmax(z)
+    a = 2
+    for est in ("rkl_mc_old_clip", "rkl_mc_clip"):
+        # choose beta so rho = 1.5 (A > 0 case) or rho = 0.5 (A < 0 case)
+        rho = 1.5 if sign > 0 else 0.5
+        beta = lp[a] - np.log(rho)
+        # choose tau so the advantage has the wanted sign, whichever advantage is used
+        tau = (beta if est == "rkl_mc_old_clip" else lp[a]) + sign * 0.7
+        loss, g, _, _ = oracle.row(est, z, ids=[a], tau=[tau], beta=[beta], eps=eps)
+        A = tau - (beta if est == "rkl_mc_old_clip" else lp[a])
+        rho_bar = min(max(rho, 1 - eps), 1 + eps)
+        assert loss == pytest.approx(-rho_bar * A, rel=1e-12)
+        assert not np.any(g)
+        # mirrored ratio: the unclipped term is the smaller one, gradient flows
+        rho2 = 0.5 if sign > 0 else 1.5
+        beta2 = lp[a] - np.log(rho2)
+        tau2 = (beta2 if est == "rkl_mc_old_clip" else lp[a]) + sign * 0.7
+        loss2, g2, _, _ = oracle.row(est, z, ids=[a], tau=[tau2], beta=[beta2], eps=eps)
+        A2 = tau2 - (beta2 if est == "rkl_mc_old_clip" else lp[a])
+        assert loss2 == pytest.approx(-rho2 * A2, rel=1e-12)
+        assert np.max(np.abs(g2)) > 0.1
+
+
+def test_on_policy_samples_collapse_the_family():
+    """With behaviour = current student (rho = 1, A_old = A_theta), every
+    member of the family gives the same gradient, and the no-IS estimator
+    (App. F) is the plain score-function estimator of App. A.2."""
+    rng = np.random.default_rng(14)
+    V, M = 16, 5
+    z, y = rand_logits(rng, V), rand_logits(rng, V)
+    ids = rng.choice(V, M)
+    lp, lq = log_softmax(z), log_softmax(y)
+    base = oracle.row("rkl_mc", z, ids=ids, tau=lq[ids], beta=lp[ids])
+    for est in ("rkl_mc_clip", "rkl_mc_old", "rkl_mc_old_clip", "rkl_mc_nois"):
+        r = oracle.row(est, z, ids=ids, tau=lq[ids], beta=lp[ids])
+        np.testing.assert_allclose(r[1], base[1], rtol=1e-12, atol=1e-14)
+        if est != "rkl_mc_nois":
+            assert r[0] == pytest.approx(base[0], rel=1e-12)
+    # no-IS surrogate value: -(1/M) sum_i A_i log p(a_i), independent of beta
+    A = lq[ids] - lp[ids]
+    r = oracle.row("rkl_mc_nois", z, ids=ids, tau=lq[ids], beta=lp[ids] + 3.0)
+    assert r[0] == pytest.approx(-(A * lp[ids]).mean(), rel=1e-12)
+
+
+def test_only_the_current_advantage_gives_the_exact_identity():
+    """Sec. 5.1: with A_theta the old-to-current IS surrogate averages to D_R
+    exactly; the rollout-time advantage A_old does not (negative control),
+    nor does dropping the ratio (App. F)."""
+    rng = np.random.default_rng(15)
+    V = 6
+    z, y = rand_logits(rng, V), rand_logits(rng, V)
+    b = z + rng.normal(0, 1.0, V)
+    lq, lb = log_softmax(y), log_softmax(b)
+    pold = np.exp(lb)
+    d_loss, d_grad, _, _ = oracle.row("rkl_dense", z, y=y)
+    e = {}
+    for est in ("rkl_mc1", "rkl_mc_old", "rkl_mc_nois"):
+        gl, gg = 0.0, np.zeros(V)
+        for a in range(V):
+            l, g, _, _ = oracle.row(est, z, ids=[a], tau=[lq[a]], beta=[lb[a]])
+            gl += pold[a] * l
+            gg += pold[a] * g
+        e[est] = (gl, gg)
+    np.testing.assert_allclose(e["rkl_mc1"][1], d_grad, atol=1e-13)
+    assert np.max(np.abs(e["rkl_mc_old"][1] - d_grad)) > 1e-3
+    assert np.max(np.abs(e["rkl_mc_nois"][1] - d_grad)) > 1e-3
+
+
+def test_clip_rejects_a_non_positive_eps():
+    z = np.zeros(4)
+    with pytest.raises(ValueError):
+        oracle.row("rkl_mc_clip", z, ids=[1], tau=[0.0], beta=[0.0], eps=0.0)
