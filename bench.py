@@ -55,6 +55,8 @@ def algorithmic_bytes(w, est: str, n_valid: int, n_masked: int) -> int:
     out_b = 4
     V = w.V
     K = w.k if est in ("fkl_topk", "rkl_topk") else (1 if est == "rkl_mc1" else w.M)
+    # the MC family reads ids and teacher log-probs, and behaviour log-probs
+    # except the no-IS ablation
     if est in ("fkl_topk", "rkl_topk"):
         row_read = K * in_b                 # only the cached logits are needed
         cache = K * (4 + 4)
@@ -63,7 +65,7 @@ def algorithmic_bytes(w, est: str, n_valid: int, n_masked: int) -> int:
         cache = 0
     else:
         row_read = V * in_b
-        cache = K * (4 + 4 + 4)
+        cache = K * (4 + 4 + (0 if est == "rkl_mc_nois" else 4))
     return n_valid * (row_read + cache) + (n_valid + n_masked) * (V * out_b + 4)
 
 
@@ -96,7 +98,7 @@ def cpu_baseline(w, est, d, rows: int, threads: int, chunk: int = 512):
         ids = tau = beta = None
         if est in ("fkl_topk", "rkl_topk"):
             ids, tau = d["topk_idx"][r0:r1], d["topk_tau"][r0:r1]
-        elif est in ("rkl_mc", "rkl_mc1"):
+        elif est.startswith("rkl_mc"):
             m = 1 if est == "rkl_mc1" else w.M
             ids = np.ascontiguousarray(d["mc_ids"][r0:r1, :m])
             tau = np.ascontiguousarray(d["mc_tau"][r0:r1, :m])
@@ -161,7 +163,7 @@ def main():
     kw = {}
     if est in ("fkl_topk", "rkl_topk"):
         kw = dict(idx=dev_t(d["topk_idx"]), teacher_logp=dev_t(d["topk_tau"]))
-    elif est in ("rkl_mc", "rkl_mc1"):
+    elif est.startswith("rkl_mc"):
         m = 1 if est == "rkl_mc1" else w.M
         kw = dict(sampled_ids=dev_t(d["mc_ids"][:, :m]), teacher_logp=dev_t(d["mc_tau"][:, :m]),
                   behav_logp=dev_t(d["mc_beta"][:, :m]))

@@ -38,7 +38,7 @@
 extern "C" {
 #endif
 
-#define OPD_VERSION 1
+#define OPD_VERSION 2
 /* Largest cached support size k, and largest sample count M. */
 #define OPD_K_MAX 256
 
@@ -52,7 +52,8 @@ typedef enum opd_status {
   OPD_ERR_WORKSPACE = -6, /* split-vocabulary path forced with a missing or short workspace */
   OPD_ERR_ESTIMATOR = -7, /* unknown estimator */
   OPD_ERR_FLAGS = -8,     /* unknown or contradictory flag bits */
-  OPD_ERR_HIP = -9        /* a HIP runtime call or kernel launch failed */
+  OPD_ERR_HIP = -9,       /* a HIP runtime call or kernel launch failed */
+  OPD_ERR_PARAM = -10     /* invalid scalar option (clip_eps of a clipped estimator) */
 } opd_status;
 
 /*
@@ -83,6 +84,23 @@ typedef enum opd_status {
  *               (Sec. 3, eq. dense-forward-kl): gradient p_theta - q.
  * OPD_RKL_DENSE Full-vocabulary reverse KL (Sec. 3, eq. dense-reverse-kl and
  *               eq. reverse-kl-gradient): gradient p_j ((log p_j - log q_j) - D_R).
+ *
+ * The remaining members of the surrogate ablation of Sec. 5.1, on the same
+ * M behaviour samples as OPD_RKL_MC.  With rho_bar = clip(rho, 1 - eps,
+ * 1 + eps), eps = opts->clip_eps, and A_old = log q - log p_old (rollout-time,
+ * from teacher_logp and behav_logp):
+ * OPD_RKL_MC_CLIP      L_theta^clip = -(1/M) sum_i min(rho_i A_theta,i, rho_bar_i A_theta,i)
+ * OPD_RKL_MC_OLD       L_old^noclip = -(1/M) sum_i rho_i A_old,i
+ * OPD_RKL_MC_OLD_CLIP  L_old^clip   = -(1/M) sum_i min(rho_i A_old,i, rho_bar_i A_old,i),
+ *                      the PPO-style adaptation
+ * The advantage is a stop-gradient weight.  Where the min selects the
+ * clipped term outside [1 - eps, 1 + eps] the sample contributes no gradient;
+ * ties (rho inside the range) count as unclipped.
+ * OPD_RKL_MC_NOIS      MC without importance sampling (the App. F ablation):
+ *                      the samples are used as if drawn from p_theta,
+ *                      L = -(1/M) sum_i sg(A_theta,i) log p_theta(a_i), gradient
+ *                      -(1/M) sum_i A_theta,i (1[j = a_i] - p_j).  behav_logp
+ *                      is not read (may be NULL).
  */
 typedef enum opd_estimator {
   OPD_FKL_TOPK = 0,
@@ -90,7 +108,11 @@ typedef enum opd_estimator {
   OPD_RKL_MC1 = 2,
   OPD_RKL_MC = 3,
   OPD_FKL_DENSE = 4,
-  OPD_RKL_DENSE = 5
+  OPD_RKL_DENSE = 5,
+  OPD_RKL_MC_CLIP = 6,
+  OPD_RKL_MC_OLD = 7,
+  OPD_RKL_MC_OLD_CLIP = 8,
+  OPD_RKL_MC_NOIS = 9
 } opd_estimator;
 
 typedef enum opd_dtype { OPD_F32 = 0, OPD_BF16 = 1 } opd_dtype;
@@ -105,8 +127,8 @@ typedef enum opd_dtype { OPD_F32 = 0, OPD_BF16 = 1 } opd_dtype;
  * Row-major device arrays; which fields are read depends on the estimator.
  *   idx            [N, k] int32  top-k support S (top-k estimators); ids must
  *                  be distinct within a row (opd_validate_cache checks this)
- *   sampled_ids    [N, M] int32  behaviour-policy samples a_i ~ p_old (MC
- *                  estimators); repeats allowed
+ *   sampled_ids    [N, M] int32  behaviour-policy samples a_i ~ p_old (the
+ *                  MC estimators, OPD_RKL_MC1 and OPD_RKL_MC_*); repeats allowed
  *   teacher_logp   [N, k] or [N, M] fp32  log q(a|s) at idx / sampled_ids,
  *                  normalised over the full vocabulary (the top-k estimators
  *                  renormalise on S, so any per-row constant cancels there)
@@ -130,12 +152,16 @@ typedef struct opd_cache {
  *               are a choice of gamma.
  * dlogits_dtype OPD_F32 (default) or OPD_BF16 (round to nearest even).
  * flags         OPD_FLAG_* bits.
- * A NULL opts pointer means {1.0f, OPD_F32, 0}.
+ * clip_eps      clip range eps of the clipped estimators; must be positive
+ *               and finite for them (the paper uses 0.2, App. B, Table 3);
+ *               ignored otherwise.
+ * A NULL opts pointer means {1.0f, OPD_F32, 0, 0.2f}.
  */
 typedef struct opd_opts {
   float grad_scale;
   int32_t dlogits_dtype;
   uint32_t flags;
+  float clip_eps;
 } opd_opts;
 
 /*

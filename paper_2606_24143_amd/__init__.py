@@ -4,10 +4,10 @@ The computation lives in ``libopd.so`` (hand-written HIP kernels behind the C
 ABI of ``include/opd.h``); this package is its thin Python binding.  PyTorch
 provides device memory and streams only.
 """
-from ._binding import (EXPORTS, ESTIMATORS, FLAG_FORCE_ROWWISE, FLAG_FORCE_SPLITV,
-                       FLAG_SKIP_MASKED, K_MAX, LIB_PATH, OpdCache, OpdError, OpdOpts, lib,
+from ._binding import (DENSE, ESTIMATORS, EXPORTS, FLAG_FORCE_ROWWISE, FLAG_FORCE_SPLITV,
+                       FLAG_SKIP_MASKED, K_MAX, LIB_PATH, TOPK, OpdCache, OpdError, OpdOpts, lib,
                        loss_fwd_bwd, status_string, validate_cache, version, workspace_bytes)
 
-__all__ = ["EXPORTS", "ESTIMATORS", "FLAG_FORCE_ROWWISE", "FLAG_FORCE_SPLITV", "FLAG_SKIP_MASKED",
-           "K_MAX", "LIB_PATH", "OpdCache", "OpdError", "OpdOpts", "lib", "loss_fwd_bwd",
-           "status_string", "validate_cache", "version", "workspace_bytes"]
+__all__ = ["DENSE", "ESTIMATORS", "EXPORTS", "FLAG_FORCE_ROWWISE", "FLAG_FORCE_SPLITV",
+           "FLAG_SKIP_MASKED", "K_MAX", "LIB_PATH", "TOPK", "OpdCache", "OpdError", "OpdOpts", "lib",
+           "loss_fwd_bwd", "status_string", "validate_cache", "version", "workspace_bytes"]

@@ -19,7 +19,10 @@ LIB_PATH = os.path.join(_PKG, "libopd.so")
 
 # opd_estimator, opd_dtype, flags (include/opd.h)
 ESTIMATORS = {"fkl_topk": 0, "rkl_topk": 1, "rkl_mc1": 2, "rkl_mc": 3, "fkl_dense": 4,
-              "rkl_dense": 5}
+              "rkl_dense": 5, "rkl_mc_clip": 6, "rkl_mc_old": 7, "rkl_mc_old_clip": 8,
+              "rkl_mc_nois": 9}
+TOPK = ("fkl_topk", "rkl_topk")
+DENSE = ("fkl_dense", "rkl_dense")
 F32, BF16 = 0, 1
 FLAG_SKIP_MASKED = 1
 FLAG_FORCE_ROWWISE = 2
@@ -28,7 +31,7 @@ K_MAX = 256
 
 STATUS = {0: "OPD_OK", -1: "OPD_ERR_NULL", -2: "OPD_ERR_SHAPE", -3: "OPD_ERR_SUPPORT",
           -4: "OPD_ERR_DTYPE", -5: "OPD_ERR_ALIGN", -6: "OPD_ERR_WORKSPACE",
-          -7: "OPD_ERR_ESTIMATOR", -8: "OPD_ERR_FLAGS", -9: "OPD_ERR_HIP"}
+          -7: "OPD_ERR_ESTIMATOR", -8: "OPD_ERR_FLAGS", -9: "OPD_ERR_HIP", -10: "OPD_ERR_PARAM"}
 
 # every symbol include/opd.h declares
 EXPORTS = ("opd_loss_fwd_bwd", "opd_workspace_bytes", "opd_validate_cache", "opd_status_string",
@@ -50,7 +53,7 @@ class OpdCache(ctypes.Structure):
 
 class OpdOpts(ctypes.Structure):
     _fields_ = [("grad_scale", ctypes.c_float), ("dlogits_dtype", ctypes.c_int32),
-                ("flags", ctypes.c_uint32)]
+                ("flags", ctypes.c_uint32), ("clip_eps", ctypes.c_float)]
 
 
 _lib = None
@@ -118,8 +121,8 @@ def workspace_bytes(N: int, V: int, dtype: int, estimator: str, k: int = 0, M: i
 def loss_fwd_bwd(logits: torch.Tensor, estimator: str, *, idx=None, sampled_ids=None,
                  teacher_logp=None, behav_logp=None, teacher_logits=None, mask=None,
                  grad_scale: float = 1.0, dlogits_dtype=torch.float32, flags: int = 0,
-                 want_lse: bool = False, want_gathered: bool = False, workspace=None,
-                 out=None, stream=None):
+                 clip_eps: float = 0.2, want_lse: bool = False, want_gathered: bool = False,
+                 workspace=None, out=None, stream=None):
     """One fused forward+backward call of opd_loss_fwd_bwd.
 
     logits: [N, V] device tensor (a row-strided view of an [N, ld] buffer is
@@ -143,16 +146,16 @@ def loss_fwd_bwd(logits: torch.Tensor, estimator: str, *, idx=None, sampled_ids=
         _rowmajor(teacher_logits, "teacher_logits")
     cache = OpdCache(_ptr(idx), _ptr(sampled_ids), _ptr(teacher_logp), _ptr(behav_logp),
                      _ptr(teacher_logits))
-    opts = OpdOpts(grad_scale, odt, flags)
+    opts = OpdOpts(grad_scale, odt, flags, clip_eps)
     if out is not None:
         loss, dbuf = out["loss"], out["dlogits"]
     else:
         loss = torch.empty(N, dtype=torch.float32, device=dev)
         dbuf = torch.empty((N, ld), dtype=dlogits_dtype, device=dev)
     lse = torch.empty(N, dtype=torch.float32, device=dev) if want_lse else None
-    K = k if estimator in ("fkl_topk", "rkl_topk") else M
+    K = k if estimator in TOPK else M
     gathered = (torch.empty((N, max(K, 1)), dtype=torch.float32, device=dev)
-                if want_gathered and estimator not in ("fkl_dense", "rkl_dense") else None)
+                if want_gathered and estimator not in DENSE else None)
     if workspace is None:
         nbytes = workspace_bytes(N, V, dt, estimator, k, M, flags)
         workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev) if nbytes else None
@@ -179,8 +182,8 @@ def validate_cache(estimator: str, V: int, *, idx=None, sampled_ids=None, teache
     dev = (ids if ids is not None else teacher_logp).device
     counter = torch.zeros(1, dtype=torch.int32, device=dev)
     cache = OpdCache(_ptr(idx), _ptr(sampled_ids), _ptr(teacher_logp), _ptr(behav_logp), None)
-    k = K if estimator in ("fkl_topk", "rkl_topk") else 0
-    M = K if estimator in ("rkl_mc1", "rkl_mc") else 0
+    k = K if estimator in TOPK else 0
+    M = K if estimator not in TOPK and estimator not in DENSE else 0
     rc = lib().opd_validate_cache(ctypes.byref(cache), ESTIMATORS[estimator], N, V, k, M,
                                   _ptr(counter), _stream(stream))
     if rc != 0:

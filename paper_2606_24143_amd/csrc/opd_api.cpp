@@ -25,9 +25,23 @@ constexpr int kSplitMaxChunks = 64;
 constexpr uint32_t kKnownFlags =
     OPD_FLAG_SKIP_MASKED | OPD_FLAG_FORCE_ROWWISE | OPD_FLAG_FORCE_SPLITV;
 
-bool valid_est(int32_t e) { return e >= OPD_FKL_TOPK && e <= OPD_RKL_DENSE; }
+bool valid_est(int32_t e) { return e >= OPD_FKL_TOPK && e <= OPD_RKL_MC_NOIS; }
 bool est_topk(int32_t e) { return e == OPD_FKL_TOPK || e == OPD_RKL_TOPK; }
-bool est_mc(int32_t e) { return e == OPD_RKL_MC1 || e == OPD_RKL_MC; }
+bool est_mc(int32_t e) { return e == OPD_RKL_MC1 || e == OPD_RKL_MC || e >= OPD_RKL_MC_CLIP; }
+bool est_clip(int32_t e) { return e == OPD_RKL_MC_CLIP || e == OPD_RKL_MC_OLD_CLIP; }
+
+int mc_variant(int32_t e) {
+  switch (e) {
+    case OPD_RKL_MC_CLIP: return opd::MC_THETA_CLIP;
+    case OPD_RKL_MC_OLD: return opd::MC_OLD;
+    case OPD_RKL_MC_OLD_CLIP: return opd::MC_OLD_CLIP;
+    case OPD_RKL_MC_NOIS: return opd::MC_NO_IS;
+  }
+  return opd::MC_THETA;
+}
+
+// The kernel family an estimator runs (every MC estimator runs the RKL_MC kernels).
+int kernel_est(int32_t e) { return est_mc(e) ? (int)opd::RKL_MC : (int)e; }
 bool est_dense(int32_t e) { return e == OPD_FKL_DENSE || e == OPD_RKL_DENSE; }
 int elt_bytes(int32_t dt) { return dt == OPD_BF16 ? 2 : 4; }
 int elems_per_vec(int32_t) { return opd::kElemsPerVec; }
@@ -109,6 +123,7 @@ const char* opd_status_string(int status) {
     case OPD_ERR_ESTIMATOR: return "unknown estimator";
     case OPD_ERR_FLAGS: return "unknown or contradictory flags";
     case OPD_ERR_HIP: return "HIP runtime error";
+    case OPD_ERR_PARAM: return "invalid scalar option (clip_eps)";
   }
   return "unknown status";
 }
@@ -128,12 +143,13 @@ int opd_loss_fwd_bwd(const void* logits, int32_t dtype, int64_t N, int64_t V, in
                      float* lse_out, float* gathered_out, void* workspace,
                      size_t workspace_bytes, void* stream) {
   if (!valid_est(estimator)) return OPD_ERR_ESTIMATOR;
-  const opd_opts o = opts ? *opts : opd_opts{1.0f, OPD_F32, 0u};
+  const opd_opts o = opts ? *opts : opd_opts{1.0f, OPD_F32, 0u, 0.2f};
   if (dtype != OPD_F32 && dtype != OPD_BF16) return OPD_ERR_DTYPE;
   if (o.dlogits_dtype != OPD_F32 && o.dlogits_dtype != OPD_BF16) return OPD_ERR_DTYPE;
   if (int rc = check_flags(o.flags)) return rc;
   if (int rc = check_shape(N, V, ld)) return rc;
   if (int rc = check_support(estimator, V, k, M)) return rc;
+  if (est_clip(estimator) && !(o.clip_eps > 0.0f && o.clip_eps <= 3.0e38f)) return OPD_ERR_PARAM;
   if (N == 0) return OPD_OK;
 
   if (!logits || !cache || !loss || !dlogits) return OPD_ERR_NULL;
@@ -144,7 +160,8 @@ int opd_loss_fwd_bwd(const void* logits, int32_t dtype, int64_t N, int64_t V, in
     ids = cache->idx;
     K = k;
   } else if (est_mc(estimator)) {
-    if (!cache->sampled_ids || !cache->teacher_logp || !cache->behav_logp) return OPD_ERR_NULL;
+    if (!cache->sampled_ids || !cache->teacher_logp) return OPD_ERR_NULL;
+    if (estimator != OPD_RKL_MC_NOIS && !cache->behav_logp) return OPD_ERR_NULL;
     ids = cache->sampled_ids;
     K = M;
   } else {
@@ -179,8 +196,10 @@ int opd_loss_fwd_bwd(const void* logits, int32_t dtype, int64_t N, int64_t V, in
   a.tail = tail;
   a.ids = ids;
   a.tau = est_dense(estimator) ? nullptr : cache->teacher_logp;
-  a.beta = est_mc(estimator) ? cache->behav_logp : nullptr;
+  a.beta = est_mc(estimator) && estimator != OPD_RKL_MC_NOIS ? cache->behav_logp : nullptr;
   a.K = K;
+  a.mc_variant = mc_variant(estimator);
+  a.clip_eps = o.clip_eps;
   a.mask = mask;
   a.gamma = o.grad_scale;
   a.skip_masked = (o.flags & OPD_FLAG_SKIP_MASKED) ? 1 : 0;
@@ -197,9 +216,9 @@ int opd_loss_fwd_bwd(const void* logits, int32_t dtype, int64_t N, int64_t V, in
   hipStream_t s = (hipStream_t)stream;
   hipError_t err;
   if (!read_row) {
-    err = opd::launch_topk_sparse(a, estimator, dtype, o.dlogits_dtype, s);
+    err = opd::launch_topk_sparse(a, kernel_est(estimator), dtype, o.dlogits_dtype, s);
   } else if (plan.split) {
-    err = opd::launch_split(a, estimator, dtype, o.dlogits_dtype, read_row, s);
+    err = opd::launch_split(a, kernel_est(estimator), dtype, o.dlogits_dtype, read_row, s);
   } else {
     Path path = Path::RowStream;
     // register-resident rows need whole vectors
@@ -209,7 +228,7 @@ int opd_loss_fwd_bwd(const void* logits, int32_t dtype, int64_t N, int64_t V, in
       else if (nvec <= (int64_t)opd::slots_large(dtype) * opd::kRowThreads)
         path = Path::RowResidentLarge;
     }
-    err = opd::launch_rowwise(a, estimator, dtype, o.dlogits_dtype, path, read_row, s);
+    err = opd::launch_rowwise(a, kernel_est(estimator), dtype, o.dlogits_dtype, path, read_row, s);
   }
   return err == hipSuccess ? OPD_OK : OPD_ERR_HIP;
 }
@@ -222,11 +241,12 @@ int opd_validate_cache(const opd_cache* cache, int32_t estimator, int64_t N, int
   if (est_dense(estimator) || N == 0) return OPD_OK;
   if (!cache || !violations) return OPD_ERR_NULL;
   const bool topk = est_topk(estimator);
+  const bool uses_beta = !topk && estimator != OPD_RKL_MC_NOIS;
   const int32_t* ids = topk ? cache->idx : cache->sampled_ids;
-  if (!ids || !cache->teacher_logp || (!topk && !cache->behav_logp)) return OPD_ERR_NULL;
+  if (!ids || !cache->teacher_logp || (uses_beta && !cache->behav_logp)) return OPD_ERR_NULL;
   const hipError_t err =
-      opd::launch_validate(ids, cache->teacher_logp, topk ? nullptr : cache->behav_logp, N, V,
-                           topk ? k : M, topk ? 1 : 0, violations, (hipStream_t)stream);
+      opd::launch_validate(ids, cache->teacher_logp, uses_beta ? cache->behav_logp : nullptr, N,
+                           V, topk ? k : M, topk ? 1 : 0, violations, (hipStream_t)stream);
   return err == hipSuccess ? OPD_OK : OPD_ERR_HIP;
 }
 

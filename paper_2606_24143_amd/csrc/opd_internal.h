@@ -9,6 +9,8 @@
 namespace opd {
 
 enum Est : int { FKL_TOPK = 0, RKL_TOPK = 1, RKL_MC1 = 2, RKL_MC = 3, FKL_DENSE = 4, RKL_DENSE = 5 };
+// Per-sample weight of the Monte-Carlo family (all run the RKL_MC kernels).
+enum McVariant : int { MC_THETA = 0, MC_THETA_CLIP = 1, MC_OLD = 2, MC_OLD_CLIP = 3, MC_NO_IS = 4 };
 enum Dt : int { F32 = 0, BF16 = 1 };
 
 constexpr int kKMax = 256;
@@ -36,8 +38,10 @@ struct Args {
   int tail;             // valid elements in the last vector (== elements per vector if full)
   const int32_t* ids;   // [N, K]
   const float* tau;     // [N, K]
-  const float* beta;    // [N, K] (MC only)
+  const float* beta;    // [N, K] (MC only; NULL for MC_NO_IS)
   int K;
+  int mc_variant;       // McVariant of the MC estimators
+  float clip_eps;
   const uint8_t* mask;  // nullable
   float gamma;
   int skip_masked;

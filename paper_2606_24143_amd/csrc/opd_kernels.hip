@@ -381,26 +381,53 @@ __device__ __forceinline__ void load_cache(const Args& a, int64_t row, const voi
 
 // Wave 0: the estimator arithmetic of one row.  gmu = gamma for a valid row.
 // Writes the spike weights and C into LDS and returns the loss (lane-uniform).
+// `variant` selects the per-sample weight of the Monte-Carlo family.
 template <int EST>
-__device__ __forceinline__ float estimate(int K, float L, float gmu, CacheLds& c) {
+__device__ __forceinline__ float estimate(int K, float L, float gmu, int variant, float eps,
+                                          CacheLds& c) {
   const int lane = threadIdx.x & 63;
   if constexpr (is_mc(EST)) {
-    // L_m = -(1/M) sum_i rho_i sg(A_i), A_i = tau_i - log p_theta(a_i),
-    // rho_i = p_theta(a_i) / p_old(a_i)  (Sec. 5.1 L_theta^noclip; App. E)
-    float acc = 0.f;
+    // Surrogates of Sec. 5.1 over behaviour samples a_i ~ p_old:
+    //   -(1/M) sum_i rho_i sg(A_i)                       (noclip)
+    //   -(1/M) sum_i min(rho_i sg(A_i), rho_bar_i sg(A_i)) (clip)
+    // with A = A_theta = tau - log p_theta (recomputed here) or A_old = tau - beta,
+    // rho = p_theta / p_old; and the App. F ablation without the ratio,
+    //   -(1/M) sum_i sg(A_theta,i) log p_theta(a_i).
+    // The per-sample gradient weight w_i multiplies (1[j = a_i] - p_j); a clipped
+    // term selected outside [1 - eps, 1 + eps] has w_i = 0.
+    const bool old_adv = variant == MC_OLD || variant == MC_OLD_CLIP;
+    const bool clip = variant == MC_THETA_CLIP || variant == MC_OLD_CLIP;
+    const bool no_is = variant == MC_NO_IS;
+    float acc_w = 0.f, acc_term = 0.f;
     for (int i = lane; i < K; i += 64) {
       const float lp = c.z[i] - L;
-      const float A = c.t[i] - lp;
-      const float rho = expf(lp - c.b[i]);
-      const float w = rho * A;
+      const float A = old_adv ? c.t[i] - c.b[i] : c.t[i] - lp;
+      float w, term;
+      if (no_is) {
+        w = A;
+        term = A * lp;
+      } else {
+        const float rho = expf(lp - c.b[i]);
+        w = rho * A;
+        term = w;
+        if (clip) {
+          const float clipped = fminf(fmaxf(rho, 1.f - eps), 1.f + eps) * A;
+          if (!(w <= clipped)) {
+            term = clipped;
+            w = 0.f;
+          }
+        }
+      }
       c.w[i] = w;
-      acc += w;
+      acc_w += w;
+      acc_term += term;
     }
     const float inv_m = 1.0f / (float)K;
-    const float cc = wave_sum(acc) * inv_m;
+    const float cw = wave_sum(acc_w) * inv_m;
+    const float total = wave_sum(acc_term) * inv_m;
     for (int i = lane; i < K; i += 64) c.w[i] = -gmu * c.w[i] * inv_m;
-    if (lane == 0) c.C = gmu * cc;
-    return -cc;
+    if (lane == 0) c.C = gmu * cw;
+    return -total;
   } else {
     // renormalised restricted KL on S (Sec. 3; App. A.1): the full-vocabulary
     // normaliser cancels, so only the K gathered logits enter
@@ -491,7 +518,7 @@ template <class TI, int EST>
 __device__ __forceinline__ void finish_row(const Args& a, int64_t row, float L, bool writer,
                                            CacheLds& c) {
   const int lane = threadIdx.x & 63;
-  const float loss = estimate<EST>(a.K, L, a.gamma, c);
+  const float loss = estimate<EST>(a.K, L, a.gamma, a.mc_variant, a.clip_eps, c);
   set_filter<TI::EPV>(a.K, c);
   if (writer) {
     if (lane == 0) {
@@ -1072,7 +1099,7 @@ __global__ void __launch_bounds__(64 * kSparseRowsPerBlock) k_topk_sparse(Args a
   }
   // every LDS entry a lane reads below was written by that same lane
   load_cache<TI>(a, row, zrow, c);
-  const float loss = estimate<EST>(K, 0.f, a.gamma, c);
+  const float loss = estimate<EST>(K, 0.f, a.gamma, 0, 0.f, c);
   const bool bad = c.bad != 0;
   if (lane == 0) a.loss[row] = bad ? __builtin_nanf("") : loss;
   if (a.gathered_out)

@@ -124,9 +124,10 @@ TOPK32 = Workload("n8192_v151936_bf16_topk32_peaked", N=8192, V=151936, dtype=BF
 MC1_RAGGED = Workload("n32768_v151936_bf16_mc1_ragged", N=32768, V=151936, dtype=BF16,
                       estimators=("rkl_mc1",), M=1, sigma_student=3.0, sigma_teacher=1.0,
                       sigma_behaviour=0.5, rollout_len=2048, len_lo=256, len_hi=2048, seed=1003)
-MC16 = Workload("n32768_v151936_bf16_mc16", N=32768, V=151936, dtype=BF16, estimators=("rkl_mc",),
+MC16 = Workload("n32768_v151936_bf16_mc16", N=32768, V=151936, dtype=BF16,
+                estimators=("rkl_mc", "rkl_mc_clip", "rkl_mc_old", "rkl_mc_old_clip", "rkl_mc_nois"),
                 M=16, sigma_student=3.0, sigma_teacher=1.0, sigma_behaviour=0.5, seed=1004)
-MC16_SMALLN = MC16.replace(name="n256_v151936_bf16_mc16_smallbatch", N=256)
+MC16_SMALLN = MC16.replace(name="n256_v151936_bf16_mc16_smallbatch", N=256, estimators=("rkl_mc",))
 DENSE = Workload("n16384_v151936_bf16_dense", N=16384, V=151936, dtype=BF16,
                  estimators=("fkl_dense", "rkl_dense"), sigma_student=3.0, sigma_teacher=1.0,
                  dense_teacher=True, seed=1005)

@@ -5,8 +5,10 @@ comparison at the stated tolerances.
 Tolerances (per token loss): |gpu - ref| <= rtol * (|ref| + s), rtol = 1e-5
 for fp32 logits and 1e-3 for bf16 logits (fp32 accumulation).  s is the
 natural magnitude of the terms the loss sums: 1 for the top-k and dense KLs
-(their weights sum to one), and (1/M) sum_i rho_i (|A_i| + 1) for the MC
-surrogate, whose value can cancel to near zero while its terms do not.
+(their weights sum to one), (1/M) sum_i rho_i (|A_i| + 1) for the MC
+surrogates (A_theta or A_old), whose value can cancel to near zero while their
+terms do not, and (1/M) sum_i (|A_i| + |log p_i| + 1) for the surrogate
+without importance ratios, whose terms are products A_i log p_i.
 Gradient: |gpu - ref| <= 1e-4 for fp32 output; bf16 output adds one bf16 ulp
 (2^-8 relative).  Gathered logits are compared bit for bit.
 """
@@ -23,7 +25,8 @@ import synth
 
 DEV = torch.device("cuda:0")
 TOPK = ("fkl_topk", "rkl_topk")
-MC = ("rkl_mc1", "rkl_mc")
+MC = ("rkl_mc1", "rkl_mc", "rkl_mc_clip", "rkl_mc_old", "rkl_mc_old_clip", "rkl_mc_nois")
+MC_FAMILY = ("rkl_mc_clip", "rkl_mc_old", "rkl_mc_old_clip", "rkl_mc_nois")
 DENSE = ("fkl_dense", "rkl_dense")
 
 
@@ -69,8 +72,12 @@ def loss_scale(est, ids, tau, beta, ref):
     if est not in MC:
         return np.ones(n)
     lp = ref["gathered"] - ref["lse"][:, None]
-    A = tau.astype(np.float64) - lp
-    rho = np.exp(lp - beta.astype(np.float64))
+    tau = tau.astype(np.float64)
+    if est == "rkl_mc_nois":
+        return (np.abs(tau - lp) + np.abs(lp) + 1.0).mean(axis=1)
+    beta = beta.astype(np.float64)
+    A = tau - beta if est in ("rkl_mc_old", "rkl_mc_old_clip") else tau - lp
+    rho = np.exp(lp - beta)
     return (rho * (np.abs(A) + 1.0)).mean(axis=1)
 
 

@@ -17,6 +17,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "opd.h")
 
 OK, NULL, SHAPE, SUPPORT, DTYPE, ALIGN, WORKSPACE, ESTIMATOR, FLAGS = 0, -1, -2, -3, -4, -5, -6, -7, -8
+PARAM = -10
 FAKE = 0x10000  # 16-byte aligned placeholder address, never dereferenced
 
 
@@ -44,7 +45,7 @@ def test_version_matches_header():
 
 
 def test_status_strings():
-    for code in range(-9, 1):
+    for code in range(-10, 1):
         s = opd.status_string(code)
         assert s and s != "unknown status"
     assert opd.status_string(-100) == "unknown status"
@@ -68,7 +69,7 @@ def call(logits=FAKE, dtype=1, N=4, V=1024, ld=None, cache="mc", est=3, k=16, M=
 
 
 @pytest.mark.parametrize("kw,code", [
-    (dict(est=6), ESTIMATOR),
+    (dict(est=10), ESTIMATOR),
     (dict(est=-1), ESTIMATOR),
     (dict(dtype=2), DTYPE),
     (dict(opts=OpdOpts(1.0, 7, 0)), DTYPE),
@@ -101,6 +102,11 @@ def call(logits=FAKE, dtype=1, N=4, V=1024, ld=None, cache="mc", est=3, k=16, M=
     (dict(V=1020), ALIGN),                       # bf16 rows of 2040 bytes
     (dict(dtype=0, V=1022), ALIGN),              # fp32 rows of 4088 bytes
     (dict(dtype=0, V=1020, opts=OpdOpts(1.0, 1, 0)), ALIGN),  # bf16 gradient rows of 2040 bytes
+    (dict(est=6, opts=OpdOpts(1.0, 0, 0, 0.0)), PARAM),     # clipped surrogate, eps = 0
+    (dict(est=8, opts=OpdOpts(1.0, 0, 0, -0.2)), PARAM),
+    (dict(est=6, opts=OpdOpts(1.0, 0, 0, float("inf"))), PARAM),
+    (dict(est=7, cache=OpdCache(None, FAKE, FAKE, None, None)), NULL),  # A_old needs behav_logp
+    (dict(est=9, M=0), SUPPORT),
     (dict(N=8, opts=OpdOpts(1.0, 0, 4)), WORKSPACE),  # split path forced, no workspace
     (dict(N=8, opts=OpdOpts(1.0, 0, 4), ws=FAKE, ws_bytes=16), WORKSPACE),
 ])
@@ -135,7 +141,7 @@ def test_workspace_sizing():
 def test_validate_cache_argument_errors():
     L = opd.lib()
     c = OpdCache(FAKE, None, FAKE, None, None)
-    assert L.opd_validate_cache(ctypes.byref(c), 9, 4, 100, 4, 0, FAKE, None) == ESTIMATOR
+    assert L.opd_validate_cache(ctypes.byref(c), 10, 4, 100, 4, 0, FAKE, None) == ESTIMATOR
     assert L.opd_validate_cache(ctypes.byref(c), 0, 4, 1, 4, 0, FAKE, None) == SHAPE
     assert L.opd_validate_cache(ctypes.byref(c), 0, 4, 100, 0, 0, FAKE, None) == SUPPORT
     assert L.opd_validate_cache(ctypes.byref(c), 0, 4, 100, 4, 0, None, None) == NULL

@@ -16,7 +16,7 @@ import torch
 import oracle
 import paper_2606_24143_amd as opd
 import synth
-from gpu_common import (DENSE, DEV, MC, TOPK, cache_arrays, check_grad, check_loss,
+from gpu_common import (DENSE, DEV, MC, MC_FAMILY, TOPK, cache_arrays, check_grad, check_loss,
                         dlogits_f64, loss_scale, oracle_dtype, rtol_for, run_gpu, say, to_dev)
 
 pytestmark = pytest.mark.gpu
@@ -60,11 +60,11 @@ def compare(name, w, d, est, out, ref, mask=None, bf16_out=False):
         assert np.array_equal(g, ref["gathered"]), name + ": gathered logits not bit-exact"
 
 
-def oracle_for(w, d, est, mask, gamma=1.0):
+def oracle_for(w, d, est, mask, gamma=1.0, eps=0.2):
     ids, tau, beta = cache_arrays(d, est)
     return oracle.rows(est, oracle_dtype(w.dtype), d["logits"], w.V, ids=ids, tau=tau, beta=beta,
                        teacher_logits=d.get("teacher_logits") if est in DENSE else None,
-                       mask=mask, gamma=gamma)
+                       mask=mask, gamma=gamma, eps=eps)
 
 
 @pytest.mark.parametrize("path", list(PATHS))
@@ -117,6 +117,33 @@ def test_support_sizes(est, K):
         compare("%s/K=%d" % (est, K), w, d, est, out, oracle_for(w, d, est, None))
         if est in TOPK and K == 1:
             assert not out["loss"].any() and not out["dlogits"].any()
+
+
+@pytest.mark.parametrize("eps", [0.02, 0.2, 1e9])
+@pytest.mark.parametrize("est", ["rkl_mc_clip", "rkl_mc_old_clip"])
+def test_clipped_surrogates_across_clip_ranges(est, eps):
+    """A stale behaviour policy puts ratios on both sides of the clip range,
+    so both branches of the min run; a huge eps reduces to the unclipped form."""
+    V = 4096
+    w = synth.Workload("t_clip", N=33, V=V, dtype=synth.BF16, estimators=(est,), M=24,
+                       sigma_student=2.0, sigma_behaviour=1.2, seed=77)
+    d = synth.generate(w)
+    say("clip %s eps=%g" % (est, eps))
+    ids, tau, beta = cache_arrays(d, est)
+    for flags in PATHS.values():
+        out = run_gpu(to_dev(d["logits"]), est, ids, tau, beta, flags=flags, clip_eps=eps,
+                      want_gathered=True, want_lse=True)
+        compare("%s/eps=%g" % (est, eps), w, d, est, out, oracle_for(w, d, est, None, eps=eps))
+
+
+def test_no_is_estimator_needs_no_behaviour_logprobs():
+    w, d, mask = small_inputs("v32000", synth.BF16)
+    say("no-IS without behav_logp")
+    ids, tau, _ = cache_arrays(d, "rkl_mc_nois")
+    out = opd.loss_fwd_bwd(to_dev(d["logits"]), "rkl_mc_nois", sampled_ids=to_dev(ids),
+                           teacher_logp=to_dev(tau), mask=to_dev(mask))
+    torch.cuda.synchronize()
+    compare("nois", w, d, "rkl_mc_nois", out, oracle_for(w, d, "rkl_mc_nois", mask), mask)
 
 
 def test_mc_duplicate_samples_accumulate():
