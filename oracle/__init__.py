@@ -23,7 +23,8 @@ _LIB_PATH = os.path.join(_HERE, "liboracle.so")
 
 ESTIMATORS = {"fkl_topk": 0, "rkl_topk": 1, "rkl_mc1": 2, "rkl_mc": 3, "fkl_dense": 4,
               "rkl_dense": 5, "rkl_mc_clip": 6, "rkl_mc_old": 7, "rkl_mc_old_clip": 8,
-              "rkl_mc_nois": 9}
+              "rkl_mc_nois": 9, "fkl_topk_trunc": 10, "rkl_topk_trunc": 11}
+TOPK = ("fkl_topk", "rkl_topk", "fkl_topk_trunc", "rkl_topk_trunc")
 DENSE = ("fkl_dense", "rkl_dense")
 MC = ("rkl_mc1", "rkl_mc", "rkl_mc_clip", "rkl_mc_old", "rkl_mc_old_clip", "rkl_mc_nois")
 CLIP_EPS = 0.2  # the paper's PPO clip range (App. B, Table 3)

@@ -106,6 +106,39 @@ static void mc_rkl(const double* z, int64_t V, double L, const int32_t* ids, con
 }
 
 /*
+ * Truncated top-k KL: the dense KL of Sec. 3 with the sum over actions cut to
+ * the cached support S and no renormalisation (p_theta and q keep their
+ * full-vocabulary normalisers):
+ *   forward  sum_{a in S} q(a) (log q(a) - log p_theta(a)),
+ *            d/dz_j = Z_q^S p_j - q_j 1[j in S];
+ *   reverse  sum_{a in S} p_theta(a) (log p_theta(a) - log q(a)),
+ *            d/dz_j = p_j 1[j in S] (log p_j - log q_j + 1)
+ *                     - p_j sum_{a in S} p(a) (log p(a) - log q(a) + 1).
+ * Unlike the renormalised forms, the gradient is dense (every p_j moves).
+ */
+static void topk_truncated(int reverse, const double* z, int64_t V, double L, const int32_t* ids,
+                           const double* tau, int K, double gamma, double* loss, double* grad) {
+  double kl = 0.0, mass = 0.0;
+  for (int i = 0; i < K; ++i) {
+    const double logp = z[ids[i]] - L;
+    if (reverse) {
+      kl += exp(logp) * (logp - tau[i]);
+      mass += exp(logp) * (logp - tau[i] + 1.0);
+    } else {
+      kl += exp(tau[i]) * (tau[i] - logp);
+      mass += exp(tau[i]);
+    }
+  }
+  *loss = kl;
+  if (!grad) return;
+  for (int64_t j = 0; j < V; ++j) grad[j] = gamma * (reverse ? -mass : mass) * exp(z[j] - L);
+  for (int i = 0; i < K; ++i) {
+    const double logp = z[ids[i]] - L;
+    grad[ids[i]] += reverse ? gamma * exp(logp) * (logp - tau[i] + 1.0) : -gamma * exp(tau[i]);
+  }
+}
+
+/*
  * The rest of the two-by-two surrogate family of Sec. 5.1 (the equation
  * block of the ablation), over behaviour samples a_i ~ p_old:
  *   rho_i     = p_theta(a_i) / p_old(a_i),  rho_bar_i = clip(rho_i, 1 - eps, 1 + eps)
@@ -209,9 +242,10 @@ int oracle_row(int est, const double* z, const double* y, int64_t V, const int32
                const double* tau, const double* beta, int K, double gamma, double eps, int valid,
                double* loss, double* grad, double* lse, double* gathered) {
   const int dense = est == ORACLE_FKL_DENSE || est == ORACLE_RKL_DENSE;
-  const int mc = est == ORACLE_RKL_MC || est == ORACLE_RKL_MC1 || est >= ORACLE_RKL_MC_CLIP;
+  const int mc = est == ORACLE_RKL_MC || est == ORACLE_RKL_MC1 ||
+                 (est >= ORACLE_RKL_MC_CLIP && est <= ORACLE_RKL_MC_NOIS);
   const int clip = est == ORACLE_RKL_MC_CLIP || est == ORACLE_RKL_MC_OLD_CLIP;
-  if (!z || !loss || V < 1 || est < ORACLE_FKL_TOPK || est > ORACLE_RKL_MC_NOIS) return -1;
+  if (!z || !loss || V < 1 || est < ORACLE_FKL_TOPK || est > ORACLE_RKL_TOPK_TRUNC) return -1;
   if (dense && !y) return -1;
   if (!dense && (K < 1 || !ids || !tau)) return -1;
   if (mc && est != ORACLE_RKL_MC_NOIS && !beta) return -1;
@@ -249,6 +283,8 @@ int oracle_row(int est, const double* z, const double* y, int64_t V, const int32
       mc_surrogate(0, 1, z, V, L, ids, tau, beta, K, eps, gamma, loss, grad);
       break;
     case ORACLE_RKL_MC_NOIS: mc_no_is(z, V, L, ids, tau, K, gamma, loss, grad); break;
+    case ORACLE_FKL_TOPK_TRUNC: topk_truncated(0, z, V, L, ids, tau, K, gamma, loss, grad); break;
+    case ORACLE_RKL_TOPK_TRUNC: topk_truncated(1, z, V, L, ids, tau, K, gamma, loss, grad); break;
   }
   return 0;
 }

@@ -22,7 +22,9 @@ enum {
   ORACLE_RKL_MC_CLIP = 6,     /* L_theta^clip (Sec. 5.1, two-by-two ablation) */
   ORACLE_RKL_MC_OLD = 7,      /* L_old^noclip (Sec. 5.1) */
   ORACLE_RKL_MC_OLD_CLIP = 8, /* L_old^clip, the PPO-style adaptation (Sec. 5.1) */
-  ORACLE_RKL_MC_NOIS = 9      /* MC without importance sampling (App. F ablation) */
+  ORACLE_RKL_MC_NOIS = 9,     /* MC without importance sampling (App. F ablation) */
+  ORACLE_FKL_TOPK_TRUNC = 10, /* forward KL summed over S, full-vocabulary normalisers */
+  ORACLE_RKL_TOPK_TRUNC = 11  /* reverse KL summed over S, full-vocabulary normalisers */
 };
 
 enum { ORACLE_F32 = 0, ORACLE_BF16 = 1 };

@@ -514,3 +514,64 @@ def test_clip_rejects_a_non_positive_eps():
     z = np.zeros(4)
     with pytest.raises(ValueError):
         oracle.row("rkl_mc_clip", z, ids=[1], tau=[0.0], beta=[0.0], eps=0.0)
+
+
+# ---------------------------------------------------------------- truncated top-k
+
+
+@pytest.mark.parametrize("est", ["fkl_topk_trunc", "rkl_topk_trunc"])
+@pytest.mark.parametrize("seed", range(3))
+def test_truncated_topk_gradient_matches_finite_differences(est, seed):
+    rng = np.random.default_rng(700 + seed)
+    V, k = 14, 5
+    z, y = rand_logits(rng, V), rand_logits(rng, V)
+    ids = rng.choice(V, size=k, replace=False)
+    tau = log_softmax(y)[ids]
+    _, g, _, _ = oracle.row(est, z, ids=ids, tau=tau, gamma=0.5)
+    fd = fd_grad(lambda zz: oracle.row(est, zz, ids=ids, tau=tau, want_grad=False)[0], z)
+    np.testing.assert_allclose(g, 0.5 * fd, atol=1e-8, rtol=0)
+
+
+def test_truncated_topk_with_full_support_is_dense():
+    rng = np.random.default_rng(16)
+    V = 19
+    z, y = rand_logits(rng, V), rand_logits(rng, V)
+    ids = rng.permutation(V)
+    tau = log_softmax(y)[ids]
+    for trunc, dense in (("fkl_topk_trunc", "fkl_dense"), ("rkl_topk_trunc", "rkl_dense")):
+        a = oracle.row(trunc, z, ids=ids, tau=tau)
+        b = oracle.row(dense, z, y=y)
+        assert a[0] == pytest.approx(b[0], rel=1e-12, abs=1e-14)
+        np.testing.assert_allclose(a[1], b[1], atol=1e-14, rtol=1e-11)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_truncated_and_renormalised_topk_are_tied_by_the_support_masses(seed):
+    """With Z_p = p(S) and Z_q = q(S), splitting each log-ratio into the
+    renormalised one plus log(Z_q / Z_p) gives
+      sum_S q (log q - log p) = Z_q KL(q~ || p~) + Z_q log(Z_q / Z_p),
+      sum_S p (log p - log q) = Z_p KL(p~ || q~) + Z_p log(Z_p / Z_q)."""
+    rng = np.random.default_rng(800 + seed)
+    V, k = 40, 7
+    z, y = rand_logits(rng, V, 2.5), rand_logits(rng, V, 2.5)
+    ids = rng.choice(V, size=k, replace=False)
+    lq = log_softmax(y)
+    tau = lq[ids]
+    Zp = softmax(z)[ids].sum()
+    Zq = np.exp(lq[ids]).sum()
+    f_t = oracle.row("fkl_topk_trunc", z, ids=ids, tau=tau, want_grad=False)[0]
+    f_r = oracle.row("fkl_topk", z, ids=ids, tau=tau, want_grad=False)[0]
+    r_t = oracle.row("rkl_topk_trunc", z, ids=ids, tau=tau, want_grad=False)[0]
+    r_r = oracle.row("rkl_topk", z, ids=ids, tau=tau, want_grad=False)[0]
+    assert f_t == pytest.approx(Zq * f_r + Zq * np.log(Zq / Zp), rel=1e-11, abs=1e-14)
+    assert r_t == pytest.approx(Zp * r_r + Zp * np.log(Zp / Zq), rel=1e-11, abs=1e-14)
+
+
+def test_truncated_forward_topk_can_be_negative():
+    """Without renormalisation the restricted forward sum is not a KL: it is
+    negative when the teacher puts less mass on S than the student does."""
+    z = np.array([3.0, 0.0, 0.0, 0.0])
+    y = np.array([0.0, 1.0, 1.0, 1.0])
+    ids = np.array([0])
+    loss = oracle.row("fkl_topk_trunc", z, ids=ids, tau=log_softmax(y)[ids], want_grad=False)[0]
+    assert loss < 0
