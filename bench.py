@@ -33,6 +33,8 @@ PEAK_HBM_GBS = 8000.0
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2606_24143_amd", "csrc", f)
                   for f in ("opd_kernels.hip", "opd_api.cpp", "opd_internal.h")]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+# estimators that read the top-k cache (renormalised and truncated)
+SUPPORT = ("fkl_topk", "rkl_topk", "fkl_topk_trunc", "rkl_topk_trunc")
 
 
 def log(msg: str):
@@ -54,11 +56,14 @@ def algorithmic_bytes(w, est: str, n_valid: int, n_masked: int) -> int:
     in_b = 2 if w.dtype == 1 else 4
     out_b = 4
     V = w.V
-    K = w.k if est in ("fkl_topk", "rkl_topk") else (1 if est == "rkl_mc1" else w.M)
+    K = w.k if est in SUPPORT else (1 if est == "rkl_mc1" else w.M)
     # the MC family reads ids and teacher log-probs, and behaviour log-probs
     # except the no-IS ablation
     if est in ("fkl_topk", "rkl_topk"):
         row_read = K * in_b                 # only the cached logits are needed
+        cache = K * (4 + 4)
+    elif est in SUPPORT:                    # truncated top-k: dense gradient, row read
+        row_read = V * in_b
         cache = K * (4 + 4)
     elif est in ("fkl_dense", "rkl_dense"):
         row_read = 2 * V * in_b             # student and teacher rows
@@ -96,7 +101,7 @@ def cpu_baseline(w, est, d, rows: int, threads: int, chunk: int = 512):
     for r0 in range(0, n, chunk):
         r1 = min(n, r0 + chunk)
         ids = tau = beta = None
-        if est in ("fkl_topk", "rkl_topk"):
+        if est in SUPPORT:
             ids, tau = d["topk_idx"][r0:r1], d["topk_tau"][r0:r1]
         elif est.startswith("rkl_mc"):
             m = 1 if est == "rkl_mc1" else w.M
@@ -161,7 +166,7 @@ def main():
 
     logits = dev_t(d["logits"])
     kw = {}
-    if est in ("fkl_topk", "rkl_topk"):
+    if est in SUPPORT:
         kw = dict(idx=dev_t(d["topk_idx"]), teacher_logp=dev_t(d["topk_tau"]))
     elif est.startswith("rkl_mc"):
         m = 1 if est == "rkl_mc1" else w.M

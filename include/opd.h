@@ -101,6 +101,17 @@ typedef enum opd_status {
  *                      L = -(1/M) sum_i sg(A_theta,i) log p_theta(a_i), gradient
  *                      -(1/M) sum_i A_theta,i (1[j = a_i] - p_j).  behav_logp
  *                      is not read (may be NULL).
+ *
+ * Truncated top-k: the dense KLs of Sec. 3 with the action sum cut to the
+ * cached support S = {idx[t, 0..k)} and no renormalisation (p_theta and q keep
+ * their full-vocabulary normalisers, so teacher_logp must be normalised over
+ * the full vocabulary).  Not a KL in general (can be negative); the gradient
+ * is dense, so the row is read.
+ * OPD_FKL_TOPK_TRUNC   sum_S q (log q - log p_theta);
+ *                      dloss/dz_j = Z_q^S p_j - q_j 1[j in S], Z_q^S = q(S)
+ * OPD_RKL_TOPK_TRUNC   sum_S p_theta (log p_theta - log q);
+ *                      dloss/dz_j = p_j 1[j in S](log p_j - log q_j + 1)
+ *                                   - p_j sum_S p (log p - log q + 1)
  */
 typedef enum opd_estimator {
   OPD_FKL_TOPK = 0,
@@ -112,7 +123,9 @@ typedef enum opd_estimator {
   OPD_RKL_MC_CLIP = 6,
   OPD_RKL_MC_OLD = 7,
   OPD_RKL_MC_OLD_CLIP = 8,
-  OPD_RKL_MC_NOIS = 9
+  OPD_RKL_MC_NOIS = 9,
+  OPD_FKL_TOPK_TRUNC = 10,
+  OPD_RKL_TOPK_TRUNC = 11
 } opd_estimator;
 
 typedef enum opd_dtype { OPD_F32 = 0, OPD_BF16 = 1 } opd_dtype;
@@ -125,8 +138,9 @@ typedef enum opd_dtype { OPD_F32 = 0, OPD_BF16 = 1 } opd_dtype;
 /*
  * The teacher-score cache of N tokens (Sec. 4.1, Stage 1 and Stage 2).
  * Row-major device arrays; which fields are read depends on the estimator.
- *   idx            [N, k] int32  top-k support S (top-k estimators); ids must
- *                  be distinct within a row (opd_validate_cache checks this)
+ *   idx            [N, k] int32  top-k support S (the top-k estimators, renormalised
+ *                  and truncated); ids must be distinct within a row
+ *                  (opd_validate_cache checks this)
  *   sampled_ids    [N, M] int32  behaviour-policy samples a_i ~ p_old (the
  *                  MC estimators, OPD_RKL_MC1 and OPD_RKL_MC_*); repeats allowed
  *   teacher_logp   [N, k] or [N, M] fp32  log q(a|s) at idx / sampled_ids,

@@ -20,8 +20,9 @@ LIB_PATH = os.path.join(_PKG, "libopd.so")
 # opd_estimator, opd_dtype, flags (include/opd.h)
 ESTIMATORS = {"fkl_topk": 0, "rkl_topk": 1, "rkl_mc1": 2, "rkl_mc": 3, "fkl_dense": 4,
               "rkl_dense": 5, "rkl_mc_clip": 6, "rkl_mc_old": 7, "rkl_mc_old_clip": 8,
-              "rkl_mc_nois": 9}
-TOPK = ("fkl_topk", "rkl_topk")
+              "rkl_mc_nois": 9, "fkl_topk_trunc": 10, "rkl_topk_trunc": 11}
+# estimators that read the top-k cache (idx, k)
+TOPK = ("fkl_topk", "rkl_topk", "fkl_topk_trunc", "rkl_topk_trunc")
 DENSE = ("fkl_dense", "rkl_dense")
 F32, BF16 = 0, 1
 FLAG_SKIP_MASKED = 1

@@ -25,9 +25,15 @@ constexpr int kSplitMaxChunks = 64;
 constexpr uint32_t kKnownFlags =
     OPD_FLAG_SKIP_MASKED | OPD_FLAG_FORCE_ROWWISE | OPD_FLAG_FORCE_SPLITV;
 
-bool valid_est(int32_t e) { return e >= OPD_FKL_TOPK && e <= OPD_RKL_MC_NOIS; }
+bool valid_est(int32_t e) { return e >= OPD_FKL_TOPK && e <= OPD_RKL_TOPK_TRUNC; }
+// renormalised top-k: only the k cached logits are needed
 bool est_topk(int32_t e) { return e == OPD_FKL_TOPK || e == OPD_RKL_TOPK; }
-bool est_mc(int32_t e) { return e == OPD_RKL_MC1 || e == OPD_RKL_MC || e >= OPD_RKL_MC_CLIP; }
+bool est_trunc(int32_t e) { return e == OPD_FKL_TOPK_TRUNC || e == OPD_RKL_TOPK_TRUNC; }
+// every estimator that reads the top-k cache (idx, k)
+bool est_support(int32_t e) { return est_topk(e) || est_trunc(e); }
+bool est_mc(int32_t e) {
+  return e == OPD_RKL_MC1 || e == OPD_RKL_MC || (e >= OPD_RKL_MC_CLIP && e <= OPD_RKL_MC_NOIS);
+}
 bool est_clip(int32_t e) { return e == OPD_RKL_MC_CLIP || e == OPD_RKL_MC_OLD_CLIP; }
 
 int mc_variant(int32_t e) {
@@ -36,12 +42,15 @@ int mc_variant(int32_t e) {
     case OPD_RKL_MC_OLD: return opd::MC_OLD;
     case OPD_RKL_MC_OLD_CLIP: return opd::MC_OLD_CLIP;
     case OPD_RKL_MC_NOIS: return opd::MC_NO_IS;
+    case OPD_FKL_TOPK_TRUNC: return opd::TRUNC_FKL;
+    case OPD_RKL_TOPK_TRUNC: return opd::TRUNC_RKL;
   }
   return opd::MC_THETA;
 }
 
-// The kernel family an estimator runs (every MC estimator runs the RKL_MC kernels).
-int kernel_est(int32_t e) { return est_mc(e) ? (int)opd::RKL_MC : (int)e; }
+// The kernel family an estimator runs: the MC family and the truncated top-k
+// KLs run the RKL_MC kernels (dense coefficient plus spikes).
+int kernel_est(int32_t e) { return est_mc(e) || est_trunc(e) ? (int)opd::RKL_MC : (int)e; }
 bool est_dense(int32_t e) { return e == OPD_FKL_DENSE || e == OPD_RKL_DENSE; }
 int elt_bytes(int32_t dt) { return dt == OPD_BF16 ? 2 : 4; }
 int elems_per_vec(int32_t) { return opd::kElemsPerVec; }
@@ -54,7 +63,7 @@ int check_shape(int64_t N, int64_t V, int64_t ld) {
 }
 
 int check_support(int32_t est, int64_t V, int32_t k, int32_t M) {
-  if (est_topk(est)) {
+  if (est_support(est)) {
     const int64_t kmax = V < OPD_K_MAX ? V : OPD_K_MAX;
     if (k < 1 || k > kmax) return OPD_ERR_SUPPORT;
   } else if (est_mc(est)) {
@@ -155,7 +164,7 @@ int opd_loss_fwd_bwd(const void* logits, int32_t dtype, int64_t N, int64_t V, in
   if (!logits || !cache || !loss || !dlogits) return OPD_ERR_NULL;
   const int32_t* ids = nullptr;
   int K = 0;
-  if (est_topk(estimator)) {
+  if (est_support(estimator)) {
     if (!cache->idx || !cache->teacher_logp) return OPD_ERR_NULL;
     ids = cache->idx;
     K = k;
@@ -211,7 +220,7 @@ int opd_loss_fwd_bwd(const void* logits, int32_t dtype, int64_t N, int64_t V, in
   a.P = plan.P;
   a.chunk_vec = plan.chunk_vec;
 
-  // The top-k estimators need the row itself only for lse_out.
+  // The renormalised top-k estimators need the row itself only for lse_out.
   const bool read_row = !est_topk(estimator) || lse_out != nullptr;
   hipStream_t s = (hipStream_t)stream;
   hipError_t err;
@@ -240,7 +249,7 @@ int opd_validate_cache(const opd_cache* cache, int32_t estimator, int64_t N, int
   if (int rc = check_support(estimator, V, k, M)) return rc;
   if (est_dense(estimator) || N == 0) return OPD_OK;
   if (!cache || !violations) return OPD_ERR_NULL;
-  const bool topk = est_topk(estimator);
+  const bool topk = est_support(estimator);
   const bool uses_beta = !topk && estimator != OPD_RKL_MC_NOIS;
   const int32_t* ids = topk ? cache->idx : cache->sampled_ids;
   if (!ids || !cache->teacher_logp || (uses_beta && !cache->behav_logp)) return OPD_ERR_NULL;

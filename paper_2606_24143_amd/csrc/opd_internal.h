@@ -9,8 +9,17 @@
 namespace opd {
 
 enum Est : int { FKL_TOPK = 0, RKL_TOPK = 1, RKL_MC1 = 2, RKL_MC = 3, FKL_DENSE = 4, RKL_DENSE = 5 };
-// Per-sample weight of the Monte-Carlo family (all run the RKL_MC kernels).
-enum McVariant : int { MC_THETA = 0, MC_THETA_CLIP = 1, MC_OLD = 2, MC_OLD_CLIP = 3, MC_NO_IS = 4 };
+// Estimators that run the RKL_MC kernels (a dense coefficient of p_theta plus
+// spikes at the cached ids): the Monte-Carlo family and the truncated top-k KLs.
+enum McVariant : int {
+  MC_THETA = 0,
+  MC_THETA_CLIP = 1,
+  MC_OLD = 2,
+  MC_OLD_CLIP = 3,
+  MC_NO_IS = 4,
+  TRUNC_FKL = 5,
+  TRUNC_RKL = 6
+};
 enum Dt : int { F32 = 0, BF16 = 1 };
 
 constexpr int kKMax = 256;

@@ -395,6 +395,35 @@ __device__ __forceinline__ float estimate(int K, float L, float gmu, int variant
     //   -(1/M) sum_i sg(A_theta,i) log p_theta(a_i).
     // The per-sample gradient weight w_i multiplies (1[j = a_i] - p_j); a clipped
     // term selected outside [1 - eps, 1 + eps] has w_i = 0.
+    if (variant == TRUNC_FKL || variant == TRUNC_RKL) {
+      // Truncated top-k (the dense KL summed over S, full-vocabulary
+      // normalisers; Sec. 3): forward: C = Z_q^S, spikes -q_i;
+      // reverse: u_i = p_i (log p_i - log q_i + 1), C = -sum u_i, spikes u_i.
+      const bool rev = variant == TRUNC_RKL;
+      float acc_c = 0.f, acc_kl = 0.f;
+      for (int i = lane; i < K; i += 64) {
+        const float lp = c.z[i] - L;
+        float spike, cterm, kl;
+        if (rev) {
+          const float p = expf(lp);
+          spike = p * ((lp - c.t[i]) + 1.f);
+          cterm = -spike;
+          kl = p * (lp - c.t[i]);
+        } else {
+          const float q = expf(c.t[i]);
+          spike = -q;
+          cterm = q;
+          kl = q * (c.t[i] - lp);
+        }
+        c.w[i] = gmu * spike;
+        acc_c += cterm;
+        acc_kl += kl;
+      }
+      const float cc = wave_sum(acc_c);
+      const float kl = wave_sum(acc_kl);
+      if (lane == 0) c.C = gmu * cc;
+      return kl;
+    }
     const bool old_adv = variant == MC_OLD || variant == MC_OLD_CLIP;
     const bool clip = variant == MC_THETA_CLIP || variant == MC_OLD_CLIP;
     const bool no_is = variant == MC_NO_IS;

@@ -119,8 +119,9 @@ SMALL_F32 = Workload("n512_v32000_f32_topk16_mc4", N=512, V=32000, dtype=F32,
                      estimators=("fkl_topk", "rkl_topk", "rkl_mc1", "rkl_mc"), k=16, M=4,
                      sigma_student=2.0, sigma_teacher=1.0, sigma_behaviour=0.3, seed=1001)
 TOPK32 = Workload("n8192_v151936_bf16_topk32_peaked", N=8192, V=151936, dtype=BF16,
-                  estimators=("fkl_topk", "rkl_topk"), k=32, sigma_student=3.0, boost_prob=0.01,
-                  boost_value=8.0, sigma_teacher=1.0, seed=1002)
+                  estimators=("fkl_topk", "rkl_topk", "fkl_topk_trunc", "rkl_topk_trunc"), k=32,
+                  sigma_student=3.0, boost_prob=0.01, boost_value=8.0, sigma_teacher=1.0,
+                  seed=1002)
 MC1_RAGGED = Workload("n32768_v151936_bf16_mc1_ragged", N=32768, V=151936, dtype=BF16,
                       estimators=("rkl_mc1",), M=1, sigma_student=3.0, sigma_teacher=1.0,
                       sigma_behaviour=0.5, rollout_len=2048, len_lo=256, len_hi=2048, seed=1003)

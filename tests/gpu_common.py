@@ -24,7 +24,9 @@ import paper_2606_24143_amd as opd
 import synth
 
 DEV = torch.device("cuda:0")
-TOPK = ("fkl_topk", "rkl_topk")
+TOPK = ("fkl_topk", "rkl_topk")             # renormalised on S
+TRUNC = ("fkl_topk_trunc", "rkl_topk_trunc")  # truncated, full-vocabulary normalisers
+SUPPORT = TOPK + TRUNC                        # every estimator reading the top-k cache
 MC = ("rkl_mc1", "rkl_mc", "rkl_mc_clip", "rkl_mc_old", "rkl_mc_old_clip", "rkl_mc_nois")
 MC_FAMILY = ("rkl_mc_clip", "rkl_mc_old", "rkl_mc_old_clip", "rkl_mc_nois")
 DENSE = ("fkl_dense", "rkl_dense")
@@ -43,7 +45,7 @@ def to_dev(a: np.ndarray, dtype: int = None) -> torch.Tensor:
 
 def cache_arrays(d: dict, est: str, M: int = None):
     """(ids, tau, beta) numpy arrays of the cache an estimator reads."""
-    if est in TOPK:
+    if est in SUPPORT:
         return d["topk_idx"], d["topk_tau"], None
     if est in MC:
         m = 1 if est == "rkl_mc1" else (M or d["mc_ids"].shape[1])
@@ -54,7 +56,7 @@ def cache_arrays(d: dict, est: str, M: int = None):
 
 def run_gpu(logits_dev, est, ids, tau, beta, teacher_dev=None, mask=None, **kw):
     cache = {}
-    if est in TOPK:
+    if est in SUPPORT:
         cache = dict(idx=to_dev(ids), teacher_logp=to_dev(tau))
     elif est in MC:
         cache = dict(sampled_ids=to_dev(ids), teacher_logp=to_dev(tau), behav_logp=to_dev(beta))

@@ -69,7 +69,9 @@ def call(logits=FAKE, dtype=1, N=4, V=1024, ld=None, cache="mc", est=3, k=16, M=
 
 
 @pytest.mark.parametrize("kw,code", [
-    (dict(est=10), ESTIMATOR),
+    (dict(est=12), ESTIMATOR),
+    (dict(est=10, cache="topk", k=0), SUPPORT),
+    (dict(est=11, cache=OpdCache(None, FAKE, FAKE, FAKE, None)), NULL),
     (dict(est=-1), ESTIMATOR),
     (dict(dtype=2), DTYPE),
     (dict(opts=OpdOpts(1.0, 7, 0)), DTYPE),
@@ -141,7 +143,7 @@ def test_workspace_sizing():
 def test_validate_cache_argument_errors():
     L = opd.lib()
     c = OpdCache(FAKE, None, FAKE, None, None)
-    assert L.opd_validate_cache(ctypes.byref(c), 10, 4, 100, 4, 0, FAKE, None) == ESTIMATOR
+    assert L.opd_validate_cache(ctypes.byref(c), 12, 4, 100, 4, 0, FAKE, None) == ESTIMATOR
     assert L.opd_validate_cache(ctypes.byref(c), 0, 4, 1, 4, 0, FAKE, None) == SHAPE
     assert L.opd_validate_cache(ctypes.byref(c), 0, 4, 100, 0, 0, FAKE, None) == SUPPORT
     assert L.opd_validate_cache(ctypes.byref(c), 0, 4, 100, 4, 0, None, None) == NULL

@@ -16,12 +16,12 @@ import torch
 import oracle
 import paper_2606_24143_amd as opd
 import synth
-from gpu_common import (DENSE, DEV, MC, MC_FAMILY, TOPK, cache_arrays, check_grad, check_loss,
+from gpu_common import (DENSE, DEV, MC, SUPPORT, TOPK, TRUNC, cache_arrays, check_grad, check_loss,
                         dlogits_f64, loss_scale, oracle_dtype, rtol_for, run_gpu, say, to_dev)
 
 pytestmark = pytest.mark.gpu
 
-ALL = TOPK + MC + DENSE
+ALL = TOPK + TRUNC + MC + DENSE
 SHAPES = {  # name: (N, V, ld)
     "v1000": (37, 1000, 1000),
     "v3001_tail": (19, 3001, 3008),
@@ -102,7 +102,7 @@ def test_parity_bf16_gradient_output(shape, est):
 
 
 @pytest.mark.parametrize("K", [1, 2, 63, 64, 65, 100, 256])
-@pytest.mark.parametrize("est", ["fkl_topk", "rkl_topk", "rkl_mc"])
+@pytest.mark.parametrize("est", ["fkl_topk", "rkl_topk", "rkl_topk_trunc", "rkl_mc"])
 def test_support_sizes(est, K):
     """k and M from 1 to the maximum, across the 64-entry wavefront boundary."""
     V = 4096
@@ -235,7 +235,7 @@ def test_out_of_range_ids_give_nan_rows_and_are_flagged():
             good = [r for r in range(N) if r not in bad_rows]
             assert np.isnan(loss[bad_rows]).all() and np.isfinite(loss[good]).all()
             assert np.isnan(g[bad_rows]).all() and np.isfinite(g[good]).all()
-        kw = dict(idx=to_dev(ids), teacher_logp=to_dev(tau)) if est in TOPK else dict(
+        kw = dict(idx=to_dev(ids), teacher_logp=to_dev(tau)) if est in SUPPORT else dict(
             sampled_ids=to_dev(ids), teacher_logp=to_dev(tau), behav_logp=to_dev(beta))
         assert opd.validate_cache(est, V, **kw) == 2
 
