@@ -759,13 +759,19 @@ __global__ void __launch_bounds__(kRowThreads) k_row_resident(Args a) {
 // teacher rows live, which fits the 256 MB Infinity Cache, so the second
 // read of y can be served from there instead of HBM.
 constexpr int kYAhead = 4;
+// LDS that holds the first teacher slots between the sweeps: only the rest
+// of the teacher row is read a second time.
+constexpr int kYLdsBytes = 144 * 1024;
 
 template <class TI, class TO, int EST, int NSLOT>
 __global__ void __launch_bounds__(kRowThreads) k_row_dense_resident(Args a) {
   constexpr int NT = kRowThreads, NW = NT / 64, EPV = TI::EPV;
   typedef typename TI::Vec Vec;
+  constexpr int YL_CAP = kYLdsBytes / (NT * (int)sizeof(Vec));
+  constexpr int YL = YL_CAP < NSLOT ? YL_CAP : NSLOT;  // teacher slots kept in LDS
   __shared__ float s_red[NW];
   __shared__ Stats s_st[NW];
+  __shared__ Vec s_y[YL][NT];
   const int tid = threadIdx.x;
   const int64_t row = blockIdx.x;
   const void* zrow = (const char*)a.logits + row * a.ld * TI::BYTES;
@@ -825,6 +831,7 @@ __global__ void __launch_bounds__(kRowThreads) k_row_dense_resident(Args a) {
       const uint32_t bn = slot_base<NT>(s + kYAhead, nvec1);
       yq[s % kYAhead] = ld_cached<TI>((const Vec*)yrow + bn, slot_off<NT>(s + kYAhead, bn, tid1, nvec1));
     }
+    if (s < YL) s_y[s][tid1] = yv;  // kept for sweep 2 (each lane reads back its own entry)
     if (!slot_owns<NT>(s, b, tid1, nvec1)) yv = neg_inf_vec<TI>();
     after(x[s], yv);
     float fz[EPV], fy[EPV];
@@ -864,21 +871,28 @@ __global__ void __launch_bounds__(kRowThreads) k_row_dense_resident(Args a) {
     if (a.lse_out) a.lse_out[row] = d.Lz;
   }
 
-  // sweep 2: gradient from the resident z and a second read of y
+  // sweep 2: gradient from the resident z; y from LDS for the first YL slots,
+  // a second read for the rest
   const uint32_t nvec2 = fresh_s(nvec);
   const int tid2 = fresh_v(tid);
 #pragma unroll
-  for (int j = 0; j < kYAhead && j < NSLOT; ++j) {
-    const uint32_t b = slot_base<NT>(j, nvec2);
-    yq[j] = ld_cached<TI>((const Vec*)yrow + b, slot_off<NT>(j, b, tid2, nvec2));
+  for (int j = 0; j < kYAhead && YL + j < NSLOT; ++j) {
+    const uint32_t b = slot_base<NT>(YL + j, nvec2);
+    yq[j] = ld_cached<TI>((const Vec*)yrow + b, slot_off<NT>(YL + j, b, tid2, nvec2));
   }
 #pragma unroll
   for (int s = 0; s < NSLOT; ++s) {
     const uint32_t b = slot_base<NT>(s, nvec2);
-    const Vec yv = yq[s % kYAhead];
-    if (s + kYAhead < NSLOT) {
-      const uint32_t bn = slot_base<NT>(s + kYAhead, nvec2);
-      yq[s % kYAhead] = ld_cached<TI>((const Vec*)yrow + bn, slot_off<NT>(s + kYAhead, bn, tid2, nvec2));
+    Vec yv;
+    if (s < YL) {
+      yv = s_y[s][tid2];
+    } else {
+      yv = yq[(s - YL) % kYAhead];
+      if (s + kYAhead < NSLOT) {
+        const uint32_t bn = slot_base<NT>(s + kYAhead, nvec2);
+        yq[(s - YL) % kYAhead] =
+            ld_cached<TI>((const Vec*)yrow + bn, slot_off<NT>(s + kYAhead, bn, tid2, nvec2));
+      }
     }
     after(x[s], yv);
     if (slot_owns<NT>(s, b, tid2, nvec2)) {
