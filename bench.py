@@ -31,7 +31,7 @@ if ROOT not in sys.path:
 
 PEAK_HBM_GBS = 8000.0
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2606_24143_amd", "csrc", f)
-                  for f in ("opd_kernels.hip", "opd_api.cpp", "opd_internal.h")]
+                  for f in ("opd_kernels.hip", "opd_api.cpp", "opd_internal.h", "opd_device.h")]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 # estimators that read the top-k cache (renormalised and truncated)
 SUPPORT = ("fkl_topk", "rkl_topk", "fkl_topk_trunc", "rkl_topk_trunc")

@@ -10,7 +10,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libopd.so")
 SOURCES = [os.path.join(CSRC, "opd_kernels.hip"), os.path.join(CSRC, "opd_api.cpp")]
-HEADERS = [os.path.join(CSRC, "opd_internal.h"), os.path.join(ROOT, "include", "opd.h")]
+HEADERS = [os.path.join(CSRC, "opd_internal.h"), os.path.join(CSRC, "opd_device.h"),
+           os.path.join(ROOT, "include", "opd.h")]
 
 # -packed-fp32-ops: no v_pk_* fp32 arithmetic in device code.
 HIPCC_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++20", "-fPIC", "-shared",

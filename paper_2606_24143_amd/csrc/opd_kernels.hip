@@ -17,296 +17,20 @@
 // stream does not evict anything useful from L2.
 #include <math.h>
 
-#include "opd_internal.h"
+#include "opd_device.h"
 
 namespace opd {
 namespace {
 
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-
-constexpr float kLog2e = 1.4426950408889634f;
-constexpr float kNegInf = -__builtin_huge_valf();
 // Spike filter: one bit per 16-byte vector index (mod kFilterBits).  A set
 // bit sends that vector through the exact K-entry check; false positives
 // only cost the check.
 constexpr int kFilterBits = 16384;
 constexpr int kFilterWords = kFilterBits / 32;
 
-// Each lane handles vectors of 4 consecutive elements: 8-byte loads of bf16,
-// 16-byte loads of fp32.  The fp32 gradient of a vector is then one 16-byte
-// store, and a wavefront's store instruction covers one contiguous 1 KiB span
-// (a lane holding 8 bf16 would write 32 bytes as two half-filled stores).
-struct InBf16 {
-  static constexpr int EPV = 4;  // elements per vector
-  static constexpr int BYTES = 2;
-  typedef u32x2 Vec;
-};
-struct InF32 {
-  static constexpr int EPV = 4;
-  static constexpr int BYTES = 4;
-  typedef u32x4 Vec;
-};
-struct OutF32 {
-  static constexpr int BYTES = 4;
-};
-struct OutBf16 {
-  static constexpr int BYTES = 2;
-};
-
 constexpr bool is_mc(int e) { return e == RKL_MC || e == RKL_MC1; }
 constexpr bool is_dense(int e) { return e == FKL_DENSE || e == RKL_DENSE; }
 constexpr bool is_topk(int e) { return e == FKL_TOPK || e == RKL_TOPK; }
-
-__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
-
-// ---------------------------------------------------------------- dtype helpers
-
-template <class TI>
-__device__ __forceinline__ void unpack(const typename TI::Vec& x, float (&f)[4]) {
-  if constexpr (TI::BYTES == 2) {
-#pragma unroll
-    for (int d = 0; d < 2; ++d) {
-      f[2 * d] = __uint_as_float(x[d] << 16);              // element 2d: low half
-      f[2 * d + 1] = __uint_as_float(x[d] & 0xFFFF0000u);  // element 2d+1: high half
-    }
-  } else {
-#pragma unroll
-    for (int d = 0; d < 4; ++d) f[d] = __uint_as_float(x[d]);
-  }
-}
-
-template <class TI>
-__device__ __forceinline__ float load_elem(const void* row, int64_t j) {
-  if constexpr (TI::BYTES == 2)
-    return __uint_as_float((uint32_t)((const uint16_t*)row)[j] << 16);
-  else
-    return ((const float*)row)[j];
-}
-
-template <class TI>
-__device__ __forceinline__ typename TI::Vec neg_inf_vec() {
-  typename TI::Vec x;
-  const uint32_t w = TI::BYTES == 2 ? 0xFF80FF80u : 0xFF800000u;
-#pragma unroll
-  for (int d = 0; d < (int)(sizeof(x) / 4); ++d) x[d] = w;
-  return x;
-}
-
-// Elements [valid, EPV) of a loaded vector become -inf, so they drop out of
-// the max and the sum without a branch in the hot loop.
-template <class TI>
-__device__ __forceinline__ void mask_tail(typename TI::Vec& x, int valid) {
-  if constexpr (TI::BYTES == 2) {
-#pragma unroll
-    for (int d = 0; d < 2; ++d) {
-      if (2 * d >= valid)
-        x[d] = 0xFF80FF80u;
-      else if (2 * d + 1 >= valid)
-        x[d] = (x[d] & 0x0000FFFFu) | 0xFF800000u;
-    }
-  } else {
-#pragma unroll
-    for (int d = 0; d < 4; ++d)
-      if (d >= valid) x[d] = 0xFF800000u;
-  }
-}
-
-// Empty register barrier: the compiler must assume x changed, so it re-derives
-// fp32 values from the packed row instead of keeping an unpacked copy alive
-// across sweeps (which would double the registers the row occupies).
-template <class VecT>
-__device__ __forceinline__ void keep_packed(VecT& x) { asm volatile("" : "+v"(x)); }
-
-template <class TI, class IdxT>
-__device__ __forceinline__ typename TI::Vec ld_nt(const void* row, IdxT v) {
-  return __builtin_nontemporal_load((const typename TI::Vec*)row + v);
-}
-template <class TI, class IdxT>
-__device__ __forceinline__ typename TI::Vec ld_cached(const void* row, IdxT v) {
-  return ((const typename TI::Vec*)row)[v];
-}
-
-__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  const uint32_t a = __builtin_bit_cast(uint16_t, (__bf16)lo);
-  const uint32_t b = __builtin_bit_cast(uint16_t, (__bf16)hi);
-  return a | (b << 16);
-}
-
-// Store the gradient values of vector v (elements [4v, 4v + valid)).
-// IdxT = uint32_t lets the compiler address with a uniform row base plus a
-// 32-bit lane offset instead of a 64-bit address per vector.
-template <class TI, class TO, class IdxT>
-__device__ __forceinline__ void store_vec(void* grow, IdxT v, const float (&g)[4], int valid) {
-  if constexpr (TO::BYTES == 4) {
-    float* p = (float*)grow + v * 4;
-    if (valid == 4)
-      __builtin_nontemporal_store(f32x4{g[0], g[1], g[2], g[3]}, (f32x4*)p);
-    else
-      for (int e = 0; e < valid; ++e) p[e] = g[e];
-  } else {
-    uint16_t* p = (uint16_t*)grow + v * 4;
-    if (valid == 4)
-      __builtin_nontemporal_store(u32x2{pack_bf16x2(g[0], g[1]), pack_bf16x2(g[2], g[3])},
-                                  (u32x2*)p);
-    else
-      for (int e = 0; e < valid; ++e) p[e] = __builtin_bit_cast(uint16_t, (__bf16)g[e]);
-  }
-}
-
-// ---------------------------------------------------------------- reductions
-// Butterfly reductions: every lane ends with the same value (each pairwise
-// step is commutative), and the order is fixed, so results are reproducible.
-
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-  return v;
-}
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
-}
-
-template <int NW>
-__device__ __forceinline__ float block_max(float v, float* red) {
-  v = wave_max(v);
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
-  __syncthreads();
-  float r = red[0];
-#pragma unroll
-  for (int w = 1; w < NW; ++w) r = fmaxf(r, red[w]);
-  __syncthreads();
-  return r;
-}
-template <int NW>
-__device__ __forceinline__ float block_sum(float v, float* red) {
-  v = wave_sum(v);
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
-  __syncthreads();
-  float r = red[0];
-#pragma unroll
-  for (int w = 1; w < NW; ++w) r += red[w];
-  __syncthreads();
-  return r;
-}
-
-// Running (max, sum of exp(x - max)) statistics of a row, plus, for the dense
-// estimators, those of the teacher row and the two cross sums
-//   tr = sum_j e^{z_j - mz} (z_j - y_j),   tf = sum_j e^{y_j - my} (y_j - z_j),
-// which give E_p[z - y] = tr / sz and E_q[y - z] = tf / sy.
-struct Stats {
-  float mz, sz, tr;
-  float my, sy, tf;
-};
-
-__device__ __forceinline__ Stats stats_empty() { return Stats{kNegInf, 0.f, 0.f, kNegInf, 0.f, 0.f}; }
-
-// factor exp(m_old - m_new) for rescaling a running sum; 0 for an empty sum.
-__device__ __forceinline__ float rescale(float m_old, float m_new) {
-  return m_old == kNegInf ? 0.f : fast_exp2((m_old - m_new) * kLog2e);
-}
-
-template <bool DENSE>
-__device__ __forceinline__ Stats stats_merge(const Stats& a, const Stats& b) {
-  Stats r;
-  r.mz = fmaxf(a.mz, b.mz);
-  {
-    const float fa = rescale(a.mz, r.mz), fb = rescale(b.mz, r.mz);
-    r.sz = a.sz * fa + b.sz * fb;
-    r.tr = DENSE ? a.tr * fa + b.tr * fb : 0.f;
-  }
-  if constexpr (DENSE) {
-    r.my = fmaxf(a.my, b.my);
-    const float fa = rescale(a.my, r.my), fb = rescale(b.my, r.my);
-    r.sy = a.sy * fa + b.sy * fb;
-    r.tf = a.tf * fa + b.tf * fb;
-  } else {
-    r.my = kNegInf;
-    r.sy = 0.f;
-    r.tf = 0.f;
-  }
-  return r;
-}
-
-template <bool DENSE>
-__device__ __forceinline__ Stats wave_merge(Stats s) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) {
-    Stats t;
-    t.mz = __shfl_xor(s.mz, o, 64);
-    t.sz = __shfl_xor(s.sz, o, 64);
-    t.tr = __shfl_xor(s.tr, o, 64);
-    t.my = __shfl_xor(s.my, o, 64);
-    t.sy = __shfl_xor(s.sy, o, 64);
-    t.tf = __shfl_xor(s.tf, o, 64);
-    s = stats_merge<DENSE>(s, t);
-  }
-  return s;
-}
-
-template <bool DENSE, int NW>
-__device__ __forceinline__ Stats block_merge(Stats s, Stats* red) {
-  s = wave_merge<DENSE>(s);
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
-  __syncthreads();
-  Stats r = red[0];
-#pragma unroll
-  for (int w = 1; w < NW; ++w) r = stats_merge<DENSE>(r, red[w]);
-  __syncthreads();
-  return r;
-}
-
-// Fold one 16-byte vector of z (and y) into a lane's running statistics.
-template <class TI, bool DENSE>
-__device__ __forceinline__ void stats_add(Stats& s, const typename TI::Vec& xz,
-                                          const typename TI::Vec& xy) {
-  constexpr int EPV = TI::EPV;
-  float fz[EPV];
-  unpack<TI>(xz, fz);
-  float vm = fz[0];
-#pragma unroll
-  for (int e = 1; e < EPV; ++e) vm = fmaxf(vm, fz[e]);
-  if constexpr (!DENSE) {
-    const float mn = fmaxf(s.mz, vm);
-    if (mn != kNegInf) {
-      float acc = s.sz * rescale(s.mz, mn);
-      const float nm = -mn * kLog2e;
-#pragma unroll
-      for (int e = 0; e < EPV; ++e) acc += fast_exp2(fmaf(fz[e], kLog2e, nm));
-      s.sz = acc;
-      s.mz = mn;
-    }
-  } else {
-    float fy[EPV];
-    unpack<TI>(xy, fy);
-    float vmy = fy[0];
-#pragma unroll
-    for (int e = 1; e < EPV; ++e) vmy = fmaxf(vmy, fy[e]);
-    const float mnz = fmaxf(s.mz, vm), mny = fmaxf(s.my, vmy);
-    if (mnz != kNegInf && mny != kNegInf) {
-      const float cz = rescale(s.mz, mnz), cy = rescale(s.my, mny);
-      float sz = s.sz * cz, tr = s.tr * cz, sy = s.sy * cy, tf = s.tf * cy;
-      const float nmz = -mnz * kLog2e, nmy = -mny * kLog2e;
-#pragma unroll
-      for (int e = 0; e < EPV; ++e) {
-        const float pz = fast_exp2(fmaf(fz[e], kLog2e, nmz));
-        const float py = fast_exp2(fmaf(fy[e], kLog2e, nmy));
-        const float d = fz[e] - fy[e];
-        // tail elements are -inf in both rows: their weight is 0 but d is
-        // NaN, so they are excluded explicitly
-        if (pz != 0.f) tr = fmaf(pz, d, tr);
-        if (py != 0.f) tf = fmaf(py, -d, tf);
-        sz += pz;
-        sy += py;
-      }
-      s.mz = mnz; s.sz = sz; s.tr = tr;
-      s.my = mny; s.sy = sy; s.tf = tf;
-    }
-  }
-}
 
 // Per-row constants of the dense estimators from the merged statistics.
 struct DenseRow {
@@ -519,6 +243,41 @@ __device__ __forceinline__ void apply_spikes(IdxT v, float (&g)[EPV], int K, con
   }
 }
 
+// Exact spike map of a resident row: bit s of spk[s >> 5][lane] is set when
+// the vector that lane holds in register slot s carries a spike.  Wave 0
+// marks the K cached ids after the estimator has run; sweep 2 then tests one
+// bit per slot instead of looking every vector up.
+template <int NT>
+__device__ __forceinline__ void mark_spike_slots(int K, uint32_t nvec, const CacheLds& c,
+                                                 uint32_t (*spk)[NT]) {
+  const uint32_t full = nvec / NT;  // slots that are not moved back
+  for (int i = threadIdx.x & 63; i < K; i += 64) {
+    const int id = c.id[i];
+    if (id < 0) continue;
+    const uint32_t v = (uint32_t)id / 4u;
+    const uint32_t s = v < full * NT ? v / NT : full;
+    const uint32_t lane = v - slot_base<NT>((int)s, nvec);
+    atomicOr(&spk[s >> 5][lane], 1u << (s & 31));
+  }
+}
+
+// Add the spikes that fall inside vector v (a vector known to hold at least
+// one), in ascending cache order.
+template <int EPV>
+__device__ __forceinline__ void add_spikes(uint32_t v, float (&g)[EPV], int K, const CacheLds& c) {
+  const int base = (int)(v * EPV);
+#pragma unroll 1
+  for (int i = 0; i < K; ++i) {
+    const uint32_t off = (uint32_t)(c.id[i] - base);
+    if (off < (uint32_t)EPV) {
+      const float w = c.w[i];
+#pragma unroll
+      for (int e = 0; e < EPV; ++e)
+        if (off == (uint32_t)e) g[e] += w;
+    }
+  }
+}
+
 // A masked token: zero its gradient vectors [v0, v1) (unless told to skip)
 // and, if `writer`, its per-token outputs.
 template <class TI, class TO, int NT>
@@ -543,12 +302,12 @@ __device__ void masked_row(const Args& a, int64_t row, void* grow, int64_t v0, i
 }
 
 // Wave 0 after the statistics are known: estimator, spikes, per-token outputs.
-template <class TI, int EST>
+template <class TI, int EST, bool FILTER = true>
 __device__ __forceinline__ void finish_row(const Args& a, int64_t row, float L, bool writer,
                                            CacheLds& c) {
   const int lane = threadIdx.x & 63;
   const float loss = estimate<EST>(a.K, L, a.gamma, a.mc_variant, a.clip_eps, c);
-  set_filter<TI::EPV>(a.K, c);
+  if constexpr (FILTER) set_filter<TI::EPV>(a.K, c);
   if (writer) {
     if (lane == 0) {
       a.loss[row] = c.bad ? __builtin_nanf("") : loss;
@@ -561,55 +320,6 @@ __device__ __forceinline__ void finish_row(const Args& a, int64_t row, float L, 
 
 // ---------------------------------------------------------------- row-per-workgroup kernels
 
-// Register slot s of a resident row covers vectors [s*NT, s*NT + NT).  A slot
-// that would run past the row end is moved back to end at it, [nvec - NT,
-// nvec), so every lane loads a vector inside the row; lanes of a moved slot
-// whose vector an earlier slot already holds are masked (slot_owns false).
-// Rows narrower than one slot use base 0 with lane offsets clamped.
-template <int NT>
-__device__ __forceinline__ uint32_t slot_base(int s, uint32_t nvec) {
-  const uint32_t b = (uint32_t)(s * NT);
-  if (b + NT <= nvec) return b;
-  return nvec >= (uint32_t)NT ? nvec - NT : 0u;
-}
-template <int NT>
-__device__ __forceinline__ bool slot_owns(int s, uint32_t base, int tid, uint32_t nvec) {
-  if ((uint32_t)(s * NT + NT) <= nvec) return true;  // a full slot: wave-uniform
-  const uint32_t v = base + (uint32_t)tid;
-  return v >= (uint32_t)(s * NT) && v < nvec;
-}
-
-// Lane offset of this lane's vector within slot s (base b): the lane id for a
-// full slot, clamped to the row end for a moved or narrow one.
-template <int NT>
-__device__ __forceinline__ uint32_t slot_off(int s, uint32_t b, int tid, uint32_t nvec) {
-  if ((uint32_t)(s * NT + NT) <= nvec) return (uint32_t)tid;
-  return min((uint32_t)tid, nvec - 1 - b);
-}
-
-// Empty asm that takes y as an input and claims to modify x: work on x is
-// not started before y has arrived, so the compiler cannot compute the
-// student-only terms of every slot early and hold them until the teacher
-// data lands.
-template <class VecT>
-__device__ __forceinline__ void after(VecT& x, const VecT& y) {
-  asm volatile("" : "+v"(x) : "v"(y));
-}
-
-// Opaque copy: values derived from it in a later sweep are recomputed there
-// (a few scalar and lane operations) instead of being kept live from an
-// earlier sweep, which would cost registers the resident row needs.
-template <class T>
-__device__ __forceinline__ T fresh_s(T x) {
-  asm volatile("" : "+s"(x));
-  return x;
-}
-template <class T>
-__device__ __forceinline__ T fresh_v(T x) {
-  asm volatile("" : "+v"(x));
-  return x;
-}
-
 // One 1024-lane workgroup per token row, the whole row held in registers
 // between the sweeps (NSLOT 16-byte vectors per lane): HBM sees one read of
 // the logits and one write of the gradient.  Requires whole vectors
@@ -620,6 +330,8 @@ __global__ void __launch_bounds__(kRowThreads) k_row_resident(Args a) {
   static_assert(!is_dense(EST), "dense estimators stream two rows");
   __shared__ float s_red[NW];
   __shared__ CacheLds c;
+  __shared__ uint32_t s_spk[2][NT];
+  static_assert(NSLOT <= 64, "spike map holds 64 slots");
   const int tid = threadIdx.x;
   const int64_t row = blockIdx.x;
   const void* zrow = (const char*)a.logits + row * a.ld * TI::BYTES;
@@ -628,7 +340,8 @@ __global__ void __launch_bounds__(kRowThreads) k_row_resident(Args a) {
     masked_row<TI, TO, NT>(a, row, grow, 0, a.nvec, true);
     return;
   }
-  for (int w = tid; w < kFilterWords; w += NT) c.filter[w] = 0u;
+  s_spk[0][tid] = 0u;
+  s_spk[1][tid] = 0u;
   const uint32_t nvec = (uint32_t)a.nvec;  // <= NSLOT * NT
   const int K = a.K;
 
@@ -677,9 +390,12 @@ __global__ void __launch_bounds__(kRowThreads) k_row_resident(Args a) {
 
   float L;
   {
+    // only a slot that reaches past the row end has lanes to mask (a
+    // wave-uniform test, so full slots cost no lane work)
 #pragma unroll
     for (int s = 0; s < NSLOT; ++s)
-      if (!slot_owns<NT>(s, slot_base<NT>(s, nvec), tid, nvec)) x[s] = neg_inf_vec<TI>();
+      if ((uint32_t)(s * NT + NT) > nvec && !slot_owns<NT>(s, slot_base<NT>(s, nvec), tid, nvec))
+        x[s] = neg_inf_vec<TI>();
     // sweep 1a: row max (EPV independent chains)
     float mx[EPV];
 #pragma unroll
@@ -718,36 +434,45 @@ __global__ void __launch_bounds__(kRowThreads) k_row_resident(Args a) {
     L = m + logf(ssum);
   }
 
-  if (tid < 64) finish_row<TI, EST>(a, row, L, true, c);
+  if (tid < 64) {
+    finish_row<TI, EST, false>(a, row, L, true, c);
+    mark_spike_slots<NT>(K, nvec, c, s_spk);
+  }
   __syncthreads();
-  const float C = c.C;
+  // A row with an id outside [0, V) becomes NaN through its coefficient (MC:
+  // C * p) or its fill value (top-k), with no per-element test.
   const bool bad = c.bad != 0;
+  const float C = bad ? __builtin_nanf("") : c.C;
+  const float g0 = bad ? __builtin_nanf("") : 0.f;
   const float nL = -L * kLog2e;
 
   // sweep 2: gradient row
   {
     const uint32_t nvec2 = fresh_s(nvec);
     const int tid2 = fresh_v(tid);
+    const uint32_t spk_lo = s_spk[0][tid2], spk_hi = s_spk[1][tid2];
+    auto grad_vec = [&](const typename TI::Vec& xs, int s, uint32_t b) {
+      float g[EPV];
+      if constexpr (is_mc(EST)) {
+        float f[EPV];
+        unpack<TI>(xs, f);
+#pragma unroll
+        for (int e = 0; e < EPV; ++e) g[e] = C * fast_exp2(fmaf(f[e], kLog2e, nL));
+      } else {
+#pragma unroll
+        for (int e = 0; e < EPV; ++e) g[e] = g0;
+      }
+      if ((((s < 32 ? spk_lo : spk_hi) >> (s & 31)) & 1u) != 0u)
+        add_spikes<EPV>(b + (uint32_t)tid2, g, K, c);
+      store_vec<TI, TO>((char*)grow + (size_t)b * EPV * TO::BYTES, (uint32_t)tid2, g, EPV);
+    };
 #pragma unroll
     for (int s = 0; s < NSLOT; ++s) {
-      const uint32_t b = slot_base<NT>(s, nvec2);
-      if (slot_owns<NT>(s, b, tid2, nvec2)) {
-        const uint32_t v = b + tid2;
-        float g[EPV];
-        if constexpr (is_mc(EST)) {
-          float f[EPV];
-          unpack<TI>(x[s], f);
-#pragma unroll
-          for (int e = 0; e < EPV; ++e) g[e] = C * fast_exp2(fmaf(f[e], kLog2e, nL));
-        } else {
-#pragma unroll
-          for (int e = 0; e < EPV; ++e) g[e] = 0.f;
-        }
-        apply_spikes<EPV>(v, g, K, c);
-        if (bad)
-#pragma unroll
-          for (int e = 0; e < EPV; ++e) g[e] = __builtin_nanf("");
-        store_vec<TI, TO>((char*)grow + (size_t)b * EPV * TO::BYTES, (uint32_t)tid2, g, EPV);
+      if ((uint32_t)(s * NT + NT) <= nvec2) {  // a full slot: every lane owns its vector
+        grad_vec(x[s], s, (uint32_t)(s * NT));
+      } else {
+        const uint32_t b = slot_base<NT>(s, nvec2);
+        if (slot_owns<NT>(s, b, tid2, nvec2)) grad_vec(x[s], s, b);
       }
     }
   }
