@@ -59,6 +59,17 @@ def lib():
                                   ctypes.c_int]
         L.oracle_rows.restype = ctypes.c_int
         L.oracle_max_threads.restype = ctypes.c_int
+        L.oracle_cdf.argtypes = [P, i64, P]
+        L.oracle_cdf.restype = ctypes.c_int
+        L.oracle_sample_row.argtypes = [P, i64, P, ctypes.c_int, P, P, P]
+        L.oracle_sample_row.restype = ctypes.c_int
+        L.oracle_topk_row.argtypes = [ctypes.c_int, P, i64, ctypes.c_int, P, P, P]
+        L.oracle_topk_row.restype = ctypes.c_int
+        L.oracle_score_row.argtypes = [P, i64, P, ctypes.c_int, P, P]
+        L.oracle_score_row.restype = ctypes.c_int
+        L.oracle_cache_rows.argtypes = [ctypes.c_int, ctypes.c_int, P, i64, i64, i64, ctypes.c_int,
+                                        P, P, P, P, P, ctypes.c_int]
+        L.oracle_cache_rows.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -120,3 +131,75 @@ def rows(est: str, dtype: int, logits: np.ndarray, V: int, *, ids=None, tau=None
 
 def max_threads() -> int:
     return int(lib().oracle_max_threads())
+
+
+# ---------------------------------------------------------------- cache building
+# Stage 1 (rollout draws and their log-probs, or a top-k support) and Stage 2
+# (teacher scoring) of Sec. 4.1.
+
+CACHE_OPS = {"sample": 0, "topk": 1, "score": 2}
+
+
+def cdf(z) -> np.ndarray:
+    """F[j] = sum_{l <= j} softmax(z)_l, summed in index order, in double."""
+    z = np.ascontiguousarray(z, np.float64)
+    F = np.zeros(z.size, np.float64)
+    if lib().oracle_cdf(_p(z), z.size, _p(F)) != 0:
+        raise ValueError("oracle_cdf rejected its arguments")
+    return F
+
+
+def sample_row(z, u):
+    """Draws by inversion at float32 uniforms u.  Returns (ids, logp, lse)."""
+    z = np.ascontiguousarray(z, np.float64)
+    u = np.ascontiguousarray(u, np.float32)
+    ids = np.zeros(u.size, np.int32)
+    logp = np.zeros(u.size, np.float64)
+    lse = np.zeros(1, np.float64)
+    if lib().oracle_sample_row(_p(z), z.size, _p(u), u.size, _p(ids), _p(logp), _p(lse)) != 0:
+        raise ValueError("oracle_sample_row rejected its arguments")
+    return ids, logp, float(lse[0])
+
+
+def topk_row(row, k: int, dtype: int = F32):
+    """Top-k of one stored row (float32 values, or uint16 bf16 bits with dtype=BF16).
+    Returns (idx, logp, lse)."""
+    row = np.ascontiguousarray(row, np.uint16 if dtype == BF16 else np.float32)
+    idx = np.zeros(k, np.int32)
+    logp = np.zeros(k, np.float64)
+    lse = np.zeros(1, np.float64)
+    if lib().oracle_topk_row(dtype, _p(row), row.size, k, _p(idx), _p(logp), _p(lse)) != 0:
+        raise ValueError("oracle_topk_row rejected its arguments")
+    return idx, logp, float(lse[0])
+
+
+def score_row(z, ids):
+    """log softmax(z) at ids.  Returns (logp, lse)."""
+    z = np.ascontiguousarray(z, np.float64)
+    ids = np.ascontiguousarray(ids, np.int32)
+    logp = np.zeros(ids.size, np.float64)
+    lse = np.zeros(1, np.float64)
+    if lib().oracle_score_row(_p(z), z.size, _p(ids), ids.size, _p(logp), _p(lse)) != 0:
+        raise ValueError("oracle_score_row rejected its arguments")
+    return logp, float(lse[0])
+
+
+def cache_rows(op: str, dtype: int, logits: np.ndarray, V: int, K: int, *, uniforms=None,
+               ids=None, mask=None, nthreads: int = 0) -> dict:
+    """Rows of stored inputs for op "sample" (uniforms [n, K]), "topk" (K = k) or
+    "score" (ids [n, K]).  Returns {"ids", "logp", "lse"}."""
+    logits = np.ascontiguousarray(logits)
+    n, ld = logits.shape
+    if op == "score":
+        out_ids = np.ascontiguousarray(ids, np.int32).copy()
+    else:
+        out_ids = np.zeros((n, K), np.int32)
+    u = None if uniforms is None else np.ascontiguousarray(uniforms, np.float32)
+    mask = None if mask is None else np.ascontiguousarray(mask, np.uint8)
+    logp = np.zeros((n, K), np.float64)
+    lse = np.zeros(n, np.float64)
+    rc = lib().oracle_cache_rows(CACHE_OPS[op], dtype, _p(logits), n, V, ld, K, _p(u), _p(mask),
+                                 _p(out_ids), _p(logp), _p(lse), nthreads)
+    if rc != 0:
+        raise ValueError("oracle_cache_rows rejected its arguments (%d)" % rc)
+    return {"ids": out_ids, "logp": logp, "lse": lse}

@@ -362,3 +362,206 @@ int oracle_rows(int est, int dtype, const void* logits, const void* teacher_logi
   }
   return err;
 }
+
+/* ------------------------------------------------------------------------
+ * Building the cache (Sec. 4.1, Stage 1 "Student rollout" and Stage 2
+ * "Teacher scoring").  Rollout draws actions from the stale student p_old at
+ * temperature 1 with no top-p or top-k truncation (App. B, Table 3) and
+ * stores their rollout-time log-probs; a top-k support is the k most probable
+ * actions (S_old = TopK(p_old, k), Sec. 5, "Sparse top-k"); teacher scoring
+ * evaluates log q on the cached actions.
+ * ------------------------------------------------------------------------ */
+
+/* Cumulative distribution of softmax(z) in index order:
+ * F[j] = sum_{l <= j} exp(z_l - L), summed left to right. */
+int oracle_cdf(const double* z, int64_t V, double* F) {
+  if (!z || !F || V < 1) return -1;
+  const double L = log_partition(z, V);
+  double acc = 0.0;
+  for (int64_t j = 0; j < V; ++j) {
+    acc += exp(z[j] - L);
+    F[j] = acc;
+  }
+  return 0;
+}
+
+/*
+ * M iid draws from softmax(z) by inversion, one per uniform u_i in [0, 1):
+ * a_i is the first index whose cumulative probability exceeds u_i.  Should
+ * rounding leave u_i at or above the last cumulative value, a_i is the last
+ * index of nonzero probability.  logp_i = log softmax(z)[a_i], the rollout-time
+ * log-probability the cache stores.  A uniform outside [0, 1) (or NaN), or a
+ * row whose softmax is undefined (a NaN or +inf logit, or every logit -inf),
+ * gives a_i = -1 and logp_i = NaN.
+ */
+int oracle_sample_row(const double* z, int64_t V, const float* u, int M, int32_t* ids,
+                      double* logp, double* lse) {
+  if (!z || !u || !ids || V < 1 || M < 1) return -1;
+  const double L = log_partition(z, V);
+  if (lse) *lse = L;
+  const int defined = isfinite(L);
+  double* F = defined ? (double*)malloc(sizeof(double) * (size_t)V) : NULL;
+  if (defined && !F) return -2;
+  int64_t last = -1; /* last index of nonzero probability */
+  if (defined) {
+    oracle_cdf(z, V, F);
+    for (int64_t j = V - 1; j >= 0 && last < 0; --j)
+      if (exp(z[j] - L) > 0.0) last = j;
+  }
+  for (int i = 0; i < M; ++i) {
+    const double ui = (double)u[i];
+    int64_t a = -1;
+    if (defined && ui >= 0.0 && ui < 1.0) {
+      for (int64_t j = 0; j < V; ++j)
+        if (F[j] > ui) {
+          a = j;
+          break;
+        }
+      if (a < 0) a = last;
+    }
+    ids[i] = (int32_t)a;
+    if (logp) logp[i] = a >= 0 ? z[a] - L : NAN;
+  }
+  free(F);
+  return 0;
+}
+
+/* Sort key of one stored logit: the IEEE-754 total order of its bits, with
+ * -0 taken as +0 (so equal values tie); bf16 is widened first.  Larger key =
+ * larger value; +NaN sorts above +inf and -NaN below -inf. */
+static uint32_t order_key(int dtype, const void* base, int64_t off) {
+  uint32_t bits;
+  if (dtype == ORACLE_BF16)
+    bits = (uint32_t)((const uint16_t*)base)[off] << 16;
+  else
+    memcpy(&bits, (const float*)base + off, 4);
+  if (bits == 0x80000000u) bits = 0u;
+  return (bits & 0x80000000u) ? ~bits : (bits | 0x80000000u);
+}
+
+typedef struct {
+  uint32_t key;
+  int32_t j;
+} ranked;
+
+/* Descending value, then ascending index. */
+static int rank_cmp(const void* pa, const void* pb) {
+  const ranked* a = (const ranked*)pa;
+  const ranked* b = (const ranked*)pb;
+  if (a->key != b->key) return a->key > b->key ? -1 : 1;
+  return a->j < b->j ? -1 : (a->j > b->j ? 1 : 0);
+}
+
+/*
+ * The k largest logits of one stored row (raw fp32 or bf16 bits), in
+ * descending order, equal values by ascending index: TopK(softmax(z), k),
+ * since softmax is monotone.  logp_i = log softmax(z)[idx_i].
+ */
+int oracle_topk_row(int dtype, const void* row, int64_t V, int k, int32_t* idx, double* logp,
+                    double* lse) {
+  if (!row || !idx || V < 1 || k < 1 || k > V) return -1;
+  ranked* r = (ranked*)malloc(sizeof(ranked) * (size_t)V);
+  double* z = (double*)malloc(sizeof(double) * (size_t)V);
+  if (!r || !z) {
+    free(r);
+    free(z);
+    return -2;
+  }
+  for (int64_t j = 0; j < V; ++j) {
+    r[j].key = order_key(dtype, row, j);
+    r[j].j = (int32_t)j;
+    z[j] = widen(dtype, row, j);
+  }
+  qsort(r, (size_t)V, sizeof(ranked), rank_cmp);
+  const double L = log_partition(z, V);
+  if (lse) *lse = L;
+  for (int i = 0; i < k; ++i) {
+    idx[i] = r[i].j;
+    if (logp) logp[i] = z[r[i].j] - L;
+  }
+  free(r);
+  free(z);
+  return 0;
+}
+
+/* Full-vocabulary log-probabilities log softmax(z)[a_i] at given actions
+ * (teacher scoring of a cache, or rollout log-probs of a support); an id
+ * outside [0, V) gives NaN. */
+int oracle_score_row(const double* z, int64_t V, const int32_t* ids, int K, double* logp,
+                     double* lse) {
+  if (!z || !ids || !logp || V < 1 || K < 1) return -1;
+  const double L = log_partition(z, V);
+  if (lse) *lse = L;
+  for (int i = 0; i < K; ++i) logp[i] = (ids[i] >= 0 && ids[i] < V) ? z[ids[i]] - L : NAN;
+  return 0;
+}
+
+/*
+ * Batch drivers over stored rows ([n_rows, ld], fp32 or bf16 bits), `nthreads`
+ * threads (0 = all).  A masked row (mask[r] == 0) gets ids/idx 0, logp 0 and
+ * lse 0 and is not read.
+ *   op 0  sampling:  aux_in = uniforms [n_rows, K] float; ids [n_rows, K] out
+ *   op 1  top-k:     ids [n_rows, K] out (K = k)
+ *   op 2  scoring:   ids [n_rows, K] in
+ * logp [n_rows, K] and lse [n_rows] are nullable outputs.
+ */
+int oracle_cache_rows(int op, int dtype, const void* logits, int64_t n_rows, int64_t V, int64_t ld,
+                      int K, const float* uniforms, const uint8_t* mask, int32_t* ids,
+                      double* logp, double* lse, int nthreads) {
+  if (!logits || !ids || n_rows < 0 || V < 1 || ld < V || K < 1) return -1;
+  if (dtype != ORACLE_F32 && dtype != ORACLE_BF16) return -1;
+  if (op < 0 || op > 2 || (op == 0 && !uniforms) || (op == 1 && K > V)) return -1;
+  int err = 0;
+  if (nthreads <= 0) nthreads = oracle_max_threads();
+#ifdef _OPENMP
+#pragma omp parallel num_threads(nthreads)
+#endif
+  {
+    double* z = (double*)malloc(sizeof(double) * (size_t)V);
+    double* lp = (double*)malloc(sizeof(double) * (size_t)K);
+    if (!z || !lp) {
+#ifdef _OPENMP
+#pragma omp atomic write
+#endif
+      err = -2;
+    } else {
+#ifdef _OPENMP
+#pragma omp for schedule(dynamic, 1)
+#endif
+      for (int64_t r = 0; r < n_rows; ++r) {
+        int32_t* rid = ids + r * K;
+        double L = 0.0;
+        int rc = 0;
+        if (mask && mask[r] == 0) {
+          for (int i = 0; i < K; ++i) {
+            if (op != 2) rid[i] = 0;
+            lp[i] = 0.0;
+          }
+        } else {
+          if (op != 1)
+            for (int64_t j = 0; j < V; ++j) z[j] = widen(dtype, logits, r * ld + j);
+          if (op == 0)
+            rc = oracle_sample_row(z, V, uniforms + r * K, K, rid, lp, &L);
+          else if (op == 1)
+            rc = oracle_topk_row(dtype, (const char*)logits +
+                                            (size_t)(r * ld) * (dtype == ORACLE_BF16 ? 2 : 4),
+                                 V, K, rid, lp, &L);
+          else
+            rc = oracle_score_row(z, V, rid, K, lp, &L);
+        }
+        if (logp)
+          for (int i = 0; i < K; ++i) logp[r * K + i] = lp[i];
+        if (lse) lse[r] = L;
+        if (rc) {
+#ifdef _OPENMP
+#pragma omp atomic write
+#endif
+          err = rc;
+        }
+      }
+    }
+    free(z);
+    free(lp);
+  }
+  return err;
+}

@@ -53,6 +53,24 @@ int oracle_rows(int est, int dtype, const void* logits, const void* teacher_logi
                 int K, const uint8_t* mask, double gamma, double eps, double* loss, double* grad,
                 double* lse, double* gathered, int nthreads);
 
+/* Building the cache (Sec. 4.1, Stages 1 and 2).  Rows in double unless
+ * stored.  See opd_oracle.c for the definitions.
+ *   oracle_cdf         F[j] = sum_{l<=j} softmax(z)_l, summed in index order
+ *   oracle_sample_row  M draws by inversion of F at uniforms u[M] in [0, 1)
+ *   oracle_topk_row    the k largest of a stored row, ties by lower index
+ *   oracle_score_row   log softmax(z) at ids (NaN for an id outside [0, V)) */
+int oracle_cdf(const double* z, int64_t V, double* F);
+int oracle_sample_row(const double* z, int64_t V, const float* u, int M, int32_t* ids,
+                      double* logp, double* lse);
+int oracle_topk_row(int dtype, const void* row, int64_t V, int k, int32_t* idx, double* logp,
+                    double* lse);
+int oracle_score_row(const double* z, int64_t V, const int32_t* ids, int K, double* logp,
+                     double* lse);
+/* Batch driver: op 0 sample, 1 top-k, 2 score (see opd_oracle.c). */
+int oracle_cache_rows(int op, int dtype, const void* logits, int64_t n_rows, int64_t V, int64_t ld,
+                      int K, const float* uniforms, const uint8_t* mask, int32_t* ids,
+                      double* logp, double* lse, int nthreads);
+
 /* Number of threads oracle_rows uses for nthreads = 0. */
 int oracle_max_threads(void);
 

@@ -27,6 +27,8 @@ _LIB_PATH = os.path.join(_HERE, "libsynth.so")
 
 F32 = 0
 BF16 = 1
+# counter-generator streams of opd_synth.c (one per kind of draw)
+STREAM_STUDENT, STREAM_BOOST, STREAM_TEACHER, STREAM_BEHAVIOUR, STREAM_SAMPLE, STREAM_LENGTH = range(1, 7)
 
 
 def build(force: bool = False) -> str:
