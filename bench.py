@@ -15,6 +15,10 @@ Prints one JSON line on stdout:
               launch stream, against the 8 TB/s MI355X peak
   cpu_baseline  the oracle on a bounded sample of the same workload, on the
               host cores
+
+--op sample|topk|score times one of the cache-building calls instead (Stage
+1 draws with their log-probs, the top-k support, or scoring at cached ids)
+on the same kind of rows; each reads every valid row once.
 """
 from __future__ import annotations
 
@@ -31,7 +35,8 @@ if ROOT not in sys.path:
 
 PEAK_HBM_GBS = 8000.0
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2606_24143_amd", "csrc", f)
-                  for f in ("opd_kernels.hip", "opd_api.cpp", "opd_internal.h", "opd_device.h")]
+                  for f in ("opd_kernels.hip", "opd_cache_kernels.hip", "opd_api.cpp", "opd_internal.h",
+                            "opd_device.h")]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 # estimators that read the top-k cache (renormalised and truncated)
 SUPPORT = ("fkl_topk", "rkl_topk", "fkl_topk_trunc", "rkl_topk_trunc")
@@ -72,6 +77,34 @@ def algorithmic_bytes(w, est: str, n_valid: int, n_masked: int) -> int:
         row_read = V * in_b
         cache = K * (4 + 4 + (0 if est == "rkl_mc_nois" else 4))
     return n_valid * (row_read + cache) + (n_valid + n_masked) * (V * out_b + 4)
+
+
+def cache_op_bytes(w, op: str, n_valid: int, K: int) -> int:
+    """Bytes a cache-building call must move: each valid row read once, plus
+    its per-token inputs and outputs (uniforms in, ids and log-probs out for
+    sampling; ids and log-probs out for top-k; ids in and log-probs out for
+    scoring)."""
+    in_b = 2 if w.dtype == 1 else 4
+    per_tok = {"sample": K * (4 + 4 + 4), "topk": K * (4 + 4), "score": K * (4 + 4)}[op]
+    return n_valid * (w.V * in_b + per_tok)
+
+
+def cpu_cache_baseline(w, op, d, u, rows: int, threads: int):
+    """The oracle's cache-building function over the first `rows` rows."""
+    import oracle
+
+    n = min(rows, w.N) if rows > 0 else w.N
+    dt = oracle.BF16 if w.dtype == 1 else oracle.F32
+    K = w.k if op == "topk" else w.M
+    t0 = time.perf_counter()
+    oracle.cache_rows(op, dt, d["logits"][:n], w.V, K, uniforms=None if u is None else u[:n],
+                      ids=d["mc_ids"][:n] if op == "score" else None, mask=d["mask"][:n],
+                      nthreads=threads)
+    el = time.perf_counter() - t0
+    used = threads if threads > 0 else oracle.max_threads()
+    return {"value": n / el, "unit": "tokens/s", "cores": used, "kind": "oracle",
+            "sample": "first %d of the %d token rows of the timed workload, fp64 oracle %s, "
+                      "%.1f s wall on %d threads" % (n, w.N, op, el, used)}
 
 
 def read_traffic(est_key: str):
@@ -127,6 +160,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="n32768_v151936_bf16_mc16")
     ap.add_argument("--estimator", default=None)
+    ap.add_argument("--op", default="loss", choices=("loss", "sample", "topk", "score"),
+                    help="time the loss (default) or one cache-building call")
     ap.add_argument("--cpu-rows", type=int, default=0, help="0 = every row")
     ap.add_argument("--cpu-threads", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -153,6 +188,11 @@ def main():
     dev = torch.device("cuda:0")
     w = synth.WORKLOADS[args.workload]
     est = args.estimator or w.estimators[0]
+    op = args.op
+    if op == "topk" and w.k == 0 or op in ("sample", "score") and w.M == 0:
+        print("--op %s needs a workload with %s" % (op, "k > 0" if op == "topk" else "M > 0"),
+              file=sys.stderr)
+        sys.exit(2)
 
     log("generating %s ..." % w.name)
     t0 = time.perf_counter()
@@ -183,9 +223,28 @@ def main():
     nbytes = opd.workspace_bytes(N, w.V, w.dtype, est, w.k, w.M)
     ws = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev) if nbytes else None
     stream = torch.cuda.current_stream()
+    u_np = None
+    if op == "loss":
+        def step():
+            opd.loss_fwd_bwd(logits, est, mask=mask, out=out, workspace=ws, stream=stream, **kw)
+    else:
+        del out
+        if op == "sample":
+            u_np = np.stack([synth.uniforms(w.seed + 1, synth.STREAM_SAMPLE, r, w.M)
+                             for r in range(N)])
+            u_np = (np.floor(u_np * 2.0 ** 24) / 2.0 ** 24).astype(np.float32)
+            u_dev = dev_t(u_np)
 
-    def step():
-        opd.loss_fwd_bwd(logits, est, mask=mask, out=out, workspace=ws, stream=stream, **kw)
+            def step():
+                opd.sample_actions(logits, u_dev, mask=mask, stream=stream)
+        elif op == "topk":
+            def step():
+                opd.topk_support(logits, w.k, mask=mask, stream=stream)
+        else:
+            ids_dev = dev_t(d["mc_ids"])
+
+            def step():
+                opd.score_actions(logits, ids_dev, mask=mask, stream=stream)
 
     for _ in range(args.warmup):
         step()
@@ -205,11 +264,19 @@ def main():
     mean_launch_s = sum(launch_ms) / len(launch_ms) / 1e3
     ms_per_step = wall / args.steps * 1e3
 
-    alg = algorithmic_bytes(w, est, n_valid, N - n_valid)
+    if op == "loss":
+        alg = algorithmic_bytes(w, est, n_valid, N - n_valid)
+        key = w.name + "/" + est
+        metric = "OPD loss fwd+bwd tokens/sec at V=151,936 bf16; achieved HBM GB/s vs peak"
+    else:
+        K = w.k if op == "topk" else w.M
+        alg = cache_op_bytes(w, op, n_valid, K)
+        key = w.name + "/" + op
+        metric = "OPD cache build (%s) tokens/sec at V=151,936 bf16; achieved HBM GB/s vs peak" % op
     achieved = alg / mean_launch_s / 1e9
-    traffic = read_traffic(w.name + "/" + est)
+    traffic = read_traffic(key)
     res = {
-        "metric": "OPD loss fwd+bwd tokens/sec at V=151,936 bf16; achieved HBM GB/s vs peak",
+        "metric": metric,
         "value": n_valid / (ms_per_step / 1e3),
         "unit": "tokens/s",
         "n_gpus": 1,
@@ -221,10 +288,11 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": w.name, "estimator": est, "tokens": N, "valid_tokens": n_valid,
+        "config": {"workload": w.name, "op": op, "estimator": est if op == "loss" else None,
+                   "tokens": N, "valid_tokens": n_valid,
                    "vocab": w.V, "logits_dtype": "bf16" if w.dtype == 1 else "f32",
                    "dlogits_dtype": "f32", "k": w.k, "M": w.M,
-                   "path": "split" if nbytes else "rowwise"},
+                   "path": "split" if nbytes and op == "loss" else "rowwise"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": achieved / PEAK_HBM_GBS,
                      "traffic": traffic,
@@ -248,10 +316,14 @@ def main():
         res["copy_calibration"] = {"bytes_per_copy": 2 * n * 4,
                                    "GBps": 2 * n * 4 * 10 / (e0.elapsed_time(e1) / 1e3) / 1e9}
     if not args.no_cpu_baseline:
-        del logits, out
+        del logits
         torch.cuda.empty_cache()
         log("timing the oracle ...")
-        res["cpu_baseline"] = cpu_baseline(w, est, d, args.cpu_rows, args.cpu_threads)
+        if op == "loss":
+            res["cpu_baseline"] = cpu_baseline(w, est, d, args.cpu_rows, args.cpu_threads)
+        else:
+            res["cpu_baseline"] = cpu_cache_baseline(w, op, d, u_np, args.cpu_rows,
+                                                     args.cpu_threads)
     print(json.dumps(res), flush=True)
 
 

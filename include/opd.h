@@ -38,7 +38,7 @@
 extern "C" {
 #endif
 
-#define OPD_VERSION 2
+#define OPD_VERSION 3
 /* Largest cached support size k, and largest sample count M. */
 #define OPD_K_MAX 256
 
@@ -232,6 +232,55 @@ size_t opd_workspace_bytes(int64_t N, int64_t V, int32_t dtype, int32_t estimato
  */
 int opd_validate_cache(const opd_cache* cache, int32_t estimator, int64_t N, int64_t V,
                        int32_t k, int32_t M, int32_t* violations, void* stream);
+
+/*
+ * Building the cache (Sec. 4.1, Stage 1 "Student rollout" and Stage 2
+ * "Teacher scoring").  Each call reads N rows of logits (the rollout policy
+ * p_old for Stage 1, the teacher for Stage 2) with the same dtype, ld and
+ * alignment rules as opd_loss_fwd_bwd, and writes per-row results.  A masked
+ * row (mask[t] == 0) is not read and gets 0 in every output.  lse_out, when
+ * not NULL, receives log sum_j exp(z_j) per row.  No workspace; one
+ * workgroup per row.
+ *
+ * opd_sample_actions: M iid draws per row from softmax(z), as the rollout
+ *   makes them (temperature 1, no top-p or top-k truncation; App. B), by
+ *   inversion: draw i is the first index whose cumulative probability (index
+ *   order) exceeds uniforms[t, i].  The uniforms are supplied by the caller
+ *   ([N, M] fp32 in [0, 1)), so the draws are a deterministic function of
+ *   them.  The CDF is evaluated in fp32 by the device: a uniform within about
+ *   1e-6 of a CDF boundary may land on the neighbouring id, and a drawn id
+ *   always has nonzero probability.
+ *     sampled_ids [N, M] int32 out; logp [N, M] fp32 out (nullable) =
+ *     log softmax(z) at the draw, the rollout-time log-probability the MC
+ *     estimators read as behav_logp.  A uniform outside [0, 1) (or NaN), or a
+ *     row with a NaN or +inf logit or no finite logit, gives id -1, logp NaN.
+ *     1 <= M <= OPD_K_MAX.
+ *
+ * opd_topk_support: the k largest logits of each row, S = TopK(softmax(z), k)
+ *   (Sec. 5: S_old at rollout time, or a teacher-selected support at scoring
+ *   time), in descending order; equal values are ordered by lower index.
+ *   The order is the IEEE-754 total order of the values with -0 equal to +0
+ *   (a +NaN ranks above +inf, a -NaN below -inf).
+ *     idx [N, k] int32 out; logp [N, k] fp32 out (nullable) = log softmax(z)
+ *     at idx.  1 <= k <= min(V, OPD_K_MAX).
+ *
+ * opd_score_actions: log softmax(z) at given ids (teacher scoring of cached
+ *   actions, or rollout log-probs of a given support).
+ *     ids [N, K] int32 in (repeats allowed); logp [N, K] fp32 out, NaN for an
+ *     id outside [0, V).  1 <= K <= OPD_K_MAX.
+ *
+ * Errors as for opd_loss_fwd_bwd: OPD_ERR_DTYPE, OPD_ERR_SHAPE,
+ * OPD_ERR_SUPPORT (M, k or K out of range), OPD_ERR_ALIGN, OPD_ERR_NULL (a
+ * required pointer), OPD_ERR_HIP.  N == 0 is a no-op returning OPD_OK.
+ */
+int opd_sample_actions(const void* logits, int32_t dtype, int64_t N, int64_t V, int64_t ld,
+                       int32_t M, const float* uniforms, const uint8_t* mask, int32_t* sampled_ids,
+                       float* logp, float* lse_out, void* stream);
+int opd_topk_support(const void* logits, int32_t dtype, int64_t N, int64_t V, int64_t ld, int32_t k,
+                     const uint8_t* mask, int32_t* idx, float* logp, float* lse_out, void* stream);
+int opd_score_actions(const void* logits, int32_t dtype, int64_t N, int64_t V, int64_t ld,
+                      const int32_t* ids, int32_t K, const uint8_t* mask, float* logp,
+                      float* lse_out, void* stream);
 
 /* Static description of a status code ("ok", "null pointer", ...). */
 const char* opd_status_string(int status);

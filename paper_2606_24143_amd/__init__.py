@@ -6,8 +6,10 @@ provides device memory and streams only.
 """
 from ._binding import (DENSE, ESTIMATORS, EXPORTS, FLAG_FORCE_ROWWISE, FLAG_FORCE_SPLITV,
                        FLAG_SKIP_MASKED, K_MAX, LIB_PATH, TOPK, OpdCache, OpdError, OpdOpts, lib,
-                       loss_fwd_bwd, status_string, validate_cache, version, workspace_bytes)
+                       loss_fwd_bwd, sample_actions, score_actions, status_string, topk_support,
+                       validate_cache, version, workspace_bytes)
 
 __all__ = ["DENSE", "ESTIMATORS", "EXPORTS", "FLAG_FORCE_ROWWISE", "FLAG_FORCE_SPLITV",
            "FLAG_SKIP_MASKED", "K_MAX", "LIB_PATH", "TOPK", "OpdCache", "OpdError", "OpdOpts", "lib",
-           "loss_fwd_bwd", "status_string", "validate_cache", "version", "workspace_bytes"]
+           "loss_fwd_bwd", "sample_actions", "score_actions", "status_string", "topk_support",
+           "validate_cache", "version", "workspace_bytes"]

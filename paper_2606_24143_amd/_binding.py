@@ -35,8 +35,8 @@ STATUS = {0: "OPD_OK", -1: "OPD_ERR_NULL", -2: "OPD_ERR_SHAPE", -3: "OPD_ERR_SUP
           -7: "OPD_ERR_ESTIMATOR", -8: "OPD_ERR_FLAGS", -9: "OPD_ERR_HIP", -10: "OPD_ERR_PARAM"}
 
 # every symbol include/opd.h declares
-EXPORTS = ("opd_loss_fwd_bwd", "opd_workspace_bytes", "opd_validate_cache", "opd_status_string",
-           "opd_version")
+EXPORTS = ("opd_loss_fwd_bwd", "opd_workspace_bytes", "opd_validate_cache", "opd_sample_actions",
+           "opd_topk_support", "opd_score_actions", "opd_status_string", "opd_version")
 
 
 class OpdError(RuntimeError):
@@ -76,6 +76,12 @@ def lib():
         L.opd_workspace_bytes.restype = ctypes.c_size_t
         L.opd_validate_cache.argtypes = [ctypes.POINTER(OpdCache), i32, i64, i64, i32, i32, P, P]
         L.opd_validate_cache.restype = ctypes.c_int
+        L.opd_sample_actions.argtypes = [P, i32, i64, i64, i64, i32, P, P, P, P, P, P]
+        L.opd_sample_actions.restype = ctypes.c_int
+        L.opd_topk_support.argtypes = [P, i32, i64, i64, i64, i32, P, P, P, P, P]
+        L.opd_topk_support.restype = ctypes.c_int
+        L.opd_score_actions.argtypes = [P, i32, i64, i64, i64, P, i32, P, P, P, P]
+        L.opd_score_actions.restype = ctypes.c_int
         L.opd_status_string.argtypes = [ctypes.c_int]
         L.opd_status_string.restype = ctypes.c_char_p
         L.opd_version.restype = ctypes.c_int
@@ -190,3 +196,78 @@ def validate_cache(estimator: str, V: int, *, idx=None, sampled_ids=None, teache
     if rc != 0:
         raise OpdError(rc, "opd_validate_cache")
     return int(counter.item())
+
+
+# ---------------------------------------------------------------- building the cache
+
+def _row_call(logits: torch.Tensor):
+    _rowmajor(logits, "logits")
+    N, V = logits.shape
+    ld = logits.stride(0) if N > 1 else V
+    return N, V, ld, _dt(logits)
+
+
+def sample_actions(logits: torch.Tensor, uniforms: torch.Tensor, *, mask=None,
+                   want_logp: bool = True, want_lse: bool = False, stream=None) -> dict:
+    """M draws per row from softmax(logits) by inversion at the given uniforms
+    ([N, M] float32 in [0, 1)).  Returns {"ids" [N, M] int32, "logp" [N, M]
+    (log-probs at the draws), "lse" [N] when requested}."""
+    N, V, ld, dt = _row_call(logits)
+    if uniforms.dtype != torch.float32 or uniforms.dim() != 2 or not uniforms.is_contiguous():
+        raise ValueError("uniforms must be a contiguous [N, M] float32 tensor")
+    M = int(uniforms.shape[1])
+    dev = logits.device
+    ids = torch.empty((N, M), dtype=torch.int32, device=dev)
+    logp = torch.empty((N, M), dtype=torch.float32, device=dev) if want_logp else None
+    lse = torch.empty(N, dtype=torch.float32, device=dev) if want_lse else None
+    rc = lib().opd_sample_actions(_ptr(logits), dt, N, V, ld, M, _ptr(uniforms), _ptr(mask),
+                                  _ptr(ids), _ptr(logp), _ptr(lse), _stream(stream))
+    if rc != 0:
+        raise OpdError(rc, "opd_sample_actions")
+    out = {"ids": ids}
+    if logp is not None:
+        out["logp"] = logp
+    if lse is not None:
+        out["lse"] = lse
+    return out
+
+
+def topk_support(logits: torch.Tensor, k: int, *, mask=None, want_logp: bool = True,
+                 want_lse: bool = False, stream=None) -> dict:
+    """The k largest logits per row (descending, ties by lower index).  Returns
+    {"idx" [N, k] int32, "logp" [N, k], "lse" [N] when requested}."""
+    N, V, ld, dt = _row_call(logits)
+    dev = logits.device
+    idx = torch.empty((N, k), dtype=torch.int32, device=dev)
+    logp = torch.empty((N, k), dtype=torch.float32, device=dev) if want_logp else None
+    lse = torch.empty(N, dtype=torch.float32, device=dev) if want_lse else None
+    rc = lib().opd_topk_support(_ptr(logits), dt, N, V, ld, k, _ptr(mask), _ptr(idx), _ptr(logp),
+                                _ptr(lse), _stream(stream))
+    if rc != 0:
+        raise OpdError(rc, "opd_topk_support")
+    out = {"idx": idx}
+    if logp is not None:
+        out["logp"] = logp
+    if lse is not None:
+        out["lse"] = lse
+    return out
+
+
+def score_actions(logits: torch.Tensor, ids: torch.Tensor, *, mask=None, want_lse: bool = False,
+                  stream=None) -> dict:
+    """log softmax(logits) at ids ([N, K] int32).  Returns {"logp" [N, K], "lse"}."""
+    N, V, ld, dt = _row_call(logits)
+    if ids.dtype != torch.int32 or ids.dim() != 2 or not ids.is_contiguous():
+        raise ValueError("ids must be a contiguous [N, K] int32 tensor")
+    K = int(ids.shape[1])
+    dev = logits.device
+    logp = torch.empty((N, K), dtype=torch.float32, device=dev)
+    lse = torch.empty(N, dtype=torch.float32, device=dev) if want_lse else None
+    rc = lib().opd_score_actions(_ptr(logits), dt, N, V, ld, _ptr(ids), K, _ptr(mask), _ptr(logp),
+                                 _ptr(lse), _stream(stream))
+    if rc != 0:
+        raise OpdError(rc, "opd_score_actions")
+    out = {"logp": logp}
+    if lse is not None:
+        out["lse"] = lse
+    return out

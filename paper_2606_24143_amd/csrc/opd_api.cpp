@@ -114,6 +114,39 @@ int64_t nvec_of(int64_t V, int32_t dt) {
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
+// Arguments shared by the cache-building entry points.
+int check_row_call(const void* logits, int32_t dtype, int64_t N, int64_t V, int64_t ld, int32_t K,
+                   int64_t kmax) {
+  if (dtype != OPD_F32 && dtype != OPD_BF16) return OPD_ERR_DTYPE;
+  if (int rc = check_shape(N, V, ld)) return rc;
+  if (K < 1 || K > kmax) return OPD_ERR_SUPPORT;
+  if (N > 0 && (!aligned16(logits) || (ld * elt_bytes(dtype)) % 16 != 0)) return OPD_ERR_ALIGN;
+  return OPD_OK;
+}
+
+opd::CacheArgs row_args(const void* logits, int32_t dtype, int64_t N, int64_t V, int64_t ld,
+                        int32_t K, const uint8_t* mask, float* logp, float* lse_out) {
+  opd::CacheArgs a{};
+  a.logits = logits;
+  a.N = N;
+  a.V = V;
+  a.ld = ld;
+  a.nvec = nvec_of(V, dtype);
+  a.tail = (int)(V - (a.nvec - 1) * elems_per_vec(dtype));
+  a.K = K;
+  a.mask = mask;
+  a.logp = logp;
+  a.lse_out = lse_out;
+  a.G = 1;
+  a.nchunk = a.nvec;
+  return a;
+}
+
+// A row that fits the registers of one workgroup is read once.
+bool row_fits(int64_t nvec, int32_t dtype) {
+  return nvec <= (int64_t)opd::slots_large(dtype) * opd::kRowThreads;
+}
+
 }  // namespace
 
 extern "C" {
@@ -256,6 +289,49 @@ int opd_validate_cache(const opd_cache* cache, int32_t estimator, int64_t N, int
   const hipError_t err =
       opd::launch_validate(ids, cache->teacher_logp, uses_beta ? cache->behav_logp : nullptr, N,
                            V, topk ? k : M, topk ? 1 : 0, violations, (hipStream_t)stream);
+  return err == hipSuccess ? OPD_OK : OPD_ERR_HIP;
+}
+
+int opd_sample_actions(const void* logits, int32_t dtype, int64_t N, int64_t V, int64_t ld,
+                       int32_t M, const float* uniforms, const uint8_t* mask, int32_t* sampled_ids,
+                       float* logp, float* lse_out, void* stream) {
+  if (int rc = check_row_call(logits, dtype, N, V, ld, M, OPD_K_MAX)) return rc;
+  if (N == 0) return OPD_OK;
+  if (!logits || !uniforms || !sampled_ids) return OPD_ERR_NULL;
+  opd::CacheArgs a = row_args(logits, dtype, N, V, ld, M, mask, logp, lse_out);
+  a.u = uniforms;
+  a.ids_out = sampled_ids;
+  // chunks of G vectors, so that a row's chunk sums fit in LDS
+  a.G = (a.nvec + opd::kCdfChunks - 1) / opd::kCdfChunks;
+  a.nchunk = (a.nvec + a.G - 1) / a.G;
+  const hipError_t err = opd::launch_cache(a, opd::CacheOp::Sample, dtype, row_fits(a.nvec, dtype),
+                                           (hipStream_t)stream);
+  return err == hipSuccess ? OPD_OK : OPD_ERR_HIP;
+}
+
+int opd_topk_support(const void* logits, int32_t dtype, int64_t N, int64_t V, int64_t ld, int32_t k,
+                     const uint8_t* mask, int32_t* idx, float* logp, float* lse_out,
+                     void* stream) {
+  if (int rc = check_row_call(logits, dtype, N, V, ld, k, V < OPD_K_MAX ? V : OPD_K_MAX)) return rc;
+  if (N == 0) return OPD_OK;
+  if (!logits || !idx) return OPD_ERR_NULL;
+  opd::CacheArgs a = row_args(logits, dtype, N, V, ld, k, mask, logp, lse_out);
+  a.ids_out = idx;
+  const hipError_t err = opd::launch_cache(a, opd::CacheOp::Topk, dtype, row_fits(a.nvec, dtype),
+                                           (hipStream_t)stream);
+  return err == hipSuccess ? OPD_OK : OPD_ERR_HIP;
+}
+
+int opd_score_actions(const void* logits, int32_t dtype, int64_t N, int64_t V, int64_t ld,
+                      const int32_t* ids, int32_t K, const uint8_t* mask, float* logp,
+                      float* lse_out, void* stream) {
+  if (int rc = check_row_call(logits, dtype, N, V, ld, K, OPD_K_MAX)) return rc;
+  if (N == 0) return OPD_OK;
+  if (!logits || !ids || !logp) return OPD_ERR_NULL;
+  opd::CacheArgs a = row_args(logits, dtype, N, V, ld, K, mask, logp, lse_out);
+  a.ids = ids;
+  const hipError_t err = opd::launch_cache(a, opd::CacheOp::Score, dtype, row_fits(a.nvec, dtype),
+                                           (hipStream_t)stream);
   return err == hipSuccess ? OPD_OK : OPD_ERR_HIP;
 }
 

@@ -1,0 +1,657 @@
+// HIP kernels that build the teacher-score cache for gfx950 (MI355X).
+//
+// Sec. 4.1 splits the pipeline into Stage 1, where rollout draws actions
+// from the stale student p_old and records their rollout-time
+// log-probabilities (or keeps its top-k support), and Stage 2, where the
+// teacher scores the cached actions.  Three row operations cover it:
+//   sample  M draws from softmax(z) by inversion of its index-order CDF at
+//           caller-supplied uniforms (rollout at temperature 1 with no top-p
+//           or top-k truncation, App. B), plus log softmax(z) at the draws;
+//   top-k   the k largest logits (descending, equal values by lower index),
+//           plus log softmax(z) there;
+//   score   log softmax(z) at given ids.
+// One 1024-lane workgroup per token row.  A row that fits the registers
+// (bf16 up to 155,648 entries, fp32 up to 77,824) is loaded once and kept
+// there; wider rows are streamed.
+#include <math.h>
+
+#include "opd_device.h"
+
+namespace opd {
+namespace {
+
+constexpr int NT = kRowThreads;
+constexpr int NW = NT / 64;
+
+// ---------------------------------------------------------------- rows
+
+// Elements [valid, 4) of a vector replaced by -inf, without branches (the
+// masks depend only on the wave-uniform count).
+template <class TI>
+__device__ __forceinline__ typename TI::Vec tail_masked(typename TI::Vec x, int valid) {
+  if constexpr (TI::BYTES == 2) {
+#pragma unroll
+    for (int d = 0; d < 2; ++d) {
+      const uint32_t keep = (2 * d < valid ? 0x0000FFFFu : 0u) | (2 * d + 1 < valid ? 0xFFFF0000u : 0u);
+      x[d] = (x[d] & keep) | (0xFF80FF80u & ~keep);
+    }
+  } else {
+#pragma unroll
+    for (int d = 0; d < 4; ++d) x[d] = d < valid ? x[d] : 0xFF800000u;
+  }
+  return x;
+}
+
+// Resident row in the slot layout of the loss kernels.  Lanes outside the
+// row, and elements of the last vector past V, read as -inf.
+template <class TI, int NSLOT>
+__device__ __forceinline__ void load_row(const void* zrow, uint32_t nvec, int tail, int tid,
+                                         typename TI::Vec (&x)[NSLOT]) {
+#pragma unroll
+  for (int s = 0; s < NSLOT; ++s) {
+    const uint32_t b = slot_base<NT>(s, nvec);
+    x[s] = ld_nt<TI>((const typename TI::Vec*)zrow + b, slot_off<NT>(s, b, tid, nvec));
+  }
+#pragma unroll
+  for (int s = 0; s < NSLOT; ++s)
+    if ((uint32_t)(s * NT + NT) > nvec && !slot_owns<NT>(s, slot_base<NT>(s, nvec), tid, nvec))
+      x[s] = neg_inf_vec<TI>();
+  if (tail != TI::EPV) {
+    // the one slot that owns the last vector (a wave-uniform test), and in
+    // it the one lane that holds it
+    const uint32_t vt = nvec - 1;
+#pragma unroll
+    for (int s = 0; s < NSLOT; ++s) {
+      const uint32_t b = slot_base<NT>(s, nvec);
+      if (vt >= b && vt < b + NT && vt >= (uint32_t)(s * NT) && (uint32_t)tid == vt - b)
+        x[s] = tail_masked<TI>(x[s], tail);
+    }
+  }
+}
+
+// One vector of a streamed row, with the tail past V read as -inf.
+template <class TI>
+__device__ __forceinline__ typename TI::Vec load_vec(const void* zrow, uint32_t v, uint32_t nvec,
+                                                     int tail) {
+  const typename TI::Vec x = ld_cached<TI>(zrow, v);
+  return v == nvec - 1 ? tail_masked<TI>(x, tail) : x;
+}
+
+// exp(z - m) with nm = -m log2(e): the one expression every pass uses, so a
+// value recomputed later is bit-identical to the one summed earlier.
+__device__ __forceinline__ float ez(float f, float nm) { return fast_exp2(fmaf(f, kLog2e, nm)); }
+
+template <class TI, int NSLOT>
+__device__ __forceinline__ float lane_max(const typename TI::Vec (&x)[NSLOT]) {
+  float mx = kNegInf;
+#pragma unroll
+  for (int s = 0; s < NSLOT; ++s) {
+    float f[4];
+    unpack<TI>(x[s], f);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) mx = fmaxf(mx, f[e]);
+  }
+  return mx;
+}
+
+template <class TI, int NSLOT>
+__device__ __forceinline__ float lane_sumexp(const typename TI::Vec (&x)[NSLOT], float nm) {
+  float sm = 0.f;
+#pragma unroll
+  for (int s = 0; s < NSLOT; ++s) {
+    float f[4];
+    unpack<TI>(x[s], f);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) sm += ez(f[e], nm);
+  }
+  return sm;
+}
+
+// Sum of exp(z - m) over one vector, added left to right onto acc.
+template <class TI>
+__device__ __forceinline__ float vec_sumexp(const typename TI::Vec& x, float nm, float acc) {
+  float f[4];
+  unpack<TI>(x, f);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) acc += ez(f[e], nm);
+  return acc;
+}
+
+// Inclusive prefix sum over the 64 lanes of a wavefront (DPP row shifts,
+// then the row broadcasts of lanes 15 and 31).
+template <int CTRL>
+__device__ __forceinline__ float dpp_move(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float wave_incl_scan(float x) {
+  const int lane = threadIdx.x & 63, rl = lane & 15;
+  float t;
+  t = dpp_move<0x111>(x);  // row_shr:1
+  if (rl >= 1) x += t;
+  t = dpp_move<0x112>(x);  // row_shr:2
+  if (rl >= 2) x += t;
+  t = dpp_move<0x114>(x);  // row_shr:4
+  if (rl >= 4) x += t;
+  t = dpp_move<0x118>(x);  // row_shr:8
+  if (rl >= 8) x += t;
+  t = dpp_move<0x142>(x);  // row_bcast:15
+  if ((lane & 31) >= 16) x += t;
+  t = dpp_move<0x143>(x);  // row_bcast:31
+  if (lane >= 32) x += t;
+  return x;
+}
+
+__device__ __forceinline__ uint32_t block_add_u32(uint32_t v, uint32_t* red) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+  __syncthreads();
+  uint32_t r = 0;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) r += red[w];
+  __syncthreads();
+  return r;
+}
+
+// ---------------------------------------------------------------- sampling
+
+// Chunk sums of exp(z - m) in index order (chunk = G consecutive vectors),
+// the inclusive prefix of each thread's run of C consecutive chunks, and
+// the wave totals of the runs.
+struct CdfLds {
+  float ls[kCdfChunks];
+  float p[NT];
+  float wt[NW];
+  float red[NW];
+};
+
+enum Pick : int { kCross = 0, kFirst = 1, kLast = 2 };
+
+__device__ __forceinline__ int64_t last_positive(const CdfLds& c, uint32_t lo, uint32_t hi) {
+  for (uint32_t q = hi; q > lo; --q)
+    if (c.ls[q - 1] > 0.f) return q - 1;
+  return -1;
+}
+__device__ __forceinline__ int64_t first_positive(const CdfLds& c, uint32_t lo, uint32_t hi) {
+  for (uint32_t q = lo; q < hi; ++q)
+    if (c.ls[q] > 0.f) return q;
+  return -1;
+}
+
+// One draw: the first element whose cumulative mass exceeds t, located run
+// -> chunk -> element.  Each level subtracts the mass before the chosen
+// entry; where rounding leaves no crossing at a level, the nearest entry of
+// nonzero mass is taken instead, so a drawn element always has positive
+// probability.
+template <class TI>
+__device__ int64_t draw_one(const CdfLds& c, const void* zrow, uint32_t nvec, int tail, uint32_t G,
+                            uint32_t nchunk, uint32_t C, float t, float S, float nm) {
+  int64_t ch;
+  float r = 0.f;
+  int pick = kLast;
+  if (t < S) {
+    // The run prefixes come from a parallel scan and need not be monotone to
+    // the last bit; this bisection keeps p[hi] > t and p[lo - 1] <= t, so it
+    // ends on a crossing either way.
+    uint32_t lo = 0, hi = NT - 1;
+    while (lo < hi) {
+      const uint32_t mid = (lo + hi) >> 1;
+      if (c.p[mid] > t)
+        hi = mid;
+      else
+        lo = mid + 1;
+    }
+    r = fmaxf(t - (lo ? c.p[lo - 1] : 0.f), 0.f);
+    const uint32_t r0 = min(lo * C, nchunk), r1 = min(r0 + C, nchunk);
+    float cum = 0.f;
+    uint32_t q = r0;
+    for (; q < r1; ++q) {
+      const float nc = cum + c.ls[q];
+      if (nc > r) break;
+      cum = nc;
+    }
+    if (q < r1) {
+      ch = q;
+      r = fmaxf(r - cum, 0.f);
+      pick = kCross;
+    } else {
+      ch = last_positive(c, r0, r1);
+      if (ch < 0) {
+        ch = first_positive(c, r1, nchunk);
+        pick = kFirst;
+        if (ch < 0) {
+          ch = last_positive(c, 0, r0);
+          pick = kLast;
+        }
+      }
+    }
+  } else {
+    ch = last_positive(c, 0, nchunk);
+  }
+  // element level, with the same sums as the chunk level
+  const uint32_t v0 = (uint32_t)ch * G, v1 = min(v0 + G, nvec);
+  float cum = 0.f;
+  int64_t first = -1, last = -1, cross = -1;
+  for (uint32_t v = v0; v < v1; ++v) {
+    float f[4];
+    unpack<TI>(load_vec<TI>(zrow, v, nvec, tail), f);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float w = ez(f[e], nm);
+      const int64_t j = (int64_t)v * 4 + e;
+      if (w > 0.f) {
+        if (first < 0) first = j;
+        last = j;
+      }
+      const float nc = cum + w;
+      if (cross < 0 && nc > r) cross = j;
+      cum = nc;
+    }
+  }
+  if (pick == kFirst) return first;
+  if (pick == kCross && cross >= 0) return cross;
+  return last;
+}
+
+template <class TI, int NSLOT>
+__global__ void __launch_bounds__(NT) k_sample(CacheArgs a) {
+  __shared__ CdfLds c;
+  const int tid = threadIdx.x;
+  const int64_t row = blockIdx.x;
+  const int M = a.K;
+  if (a.mask && a.mask[row] == 0) {
+    for (int i = tid; i < M; i += NT) {
+      a.ids_out[row * M + i] = 0;
+      if (a.logp) a.logp[row * M + i] = 0.f;
+    }
+    if (tid == 0 && a.lse_out) a.lse_out[row] = 0.f;
+    return;
+  }
+  const void* zrow = (const char*)a.logits + row * a.ld * TI::BYTES;
+  const uint32_t nvec = (uint32_t)a.nvec, G = (uint32_t)a.G, nchunk = (uint32_t)a.nchunk;
+  float m, nm;
+  if constexpr (NSLOT > 0) {
+    // G == 1: chunk q is vector q
+    typename TI::Vec x[NSLOT];
+    load_row<TI, NSLOT>(zrow, nvec, a.tail, tid, x);
+    m = block_max<NW>(lane_max<TI, NSLOT>(x), c.red);
+#pragma unroll
+    for (int s = 0; s < NSLOT; ++s) keep_packed(x[s]);
+    nm = -m * kLog2e;
+#pragma unroll
+    for (int s = 0; s < NSLOT; ++s) {
+      const uint32_t b = slot_base<NT>(s, nvec);
+      if ((uint32_t)(s * NT + NT) <= nvec || slot_owns<NT>(s, b, tid, nvec))
+        c.ls[b + tid] = vec_sumexp<TI>(x[s], nm, 0.f);
+    }
+  } else {
+    float mx = kNegInf;
+    for (uint32_t v = tid; v < nvec; v += NT) {
+      float f[4];
+      unpack<TI>(load_vec<TI>(zrow, v, nvec, a.tail), f);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) mx = fmaxf(mx, f[e]);
+    }
+    m = block_max<NW>(mx, c.red);
+    nm = -m * kLog2e;
+    for (uint32_t q = tid; q < nchunk; q += NT) {
+      const uint32_t v1 = min(q * G + G, nvec);
+      float acc = 0.f;
+      for (uint32_t v = q * G; v < v1; ++v) acc = vec_sumexp<TI>(load_vec<TI>(zrow, v, nvec, a.tail), nm, acc);
+      c.ls[q] = acc;
+    }
+  }
+  __syncthreads();
+
+  // runs of C consecutive chunks per thread, and their block-wide prefix
+  const uint32_t C = (nchunk + NT - 1) / NT;
+  {
+    const uint32_t r0 = min((uint32_t)tid * C, nchunk), r1 = min(r0 + C, nchunk);
+    float run = 0.f;
+    for (uint32_t q = r0; q < r1; ++q) run += c.ls[q];
+    const float incl = wave_incl_scan(run);
+    if ((tid & 63) == 63) c.wt[tid >> 6] = incl;
+    __syncthreads();
+    float before = 0.f;
+    for (int w = 0; w < (tid >> 6); ++w) before += c.wt[w];
+    c.p[tid] = before + incl;
+  }
+  float S = 0.f;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) S += c.wt[w];  // equals p[NT - 1] bit for bit
+  __syncthreads();
+
+  const float L = m + logf(S);
+  if (tid == 0 && a.lse_out) a.lse_out[row] = L;
+  // a NaN or +inf logit, or a row of -inf, leaves S NaN: no distribution
+  const bool defined = S > 0.f && S <= 3.4028235e38f;
+  for (int i = tid; i < M; i += NT) {
+    const float u = a.u[row * M + i];
+    int32_t id = -1;
+    float lp = __builtin_nanf("");
+    if (defined && u >= 0.f && u < 1.f) {
+      const int64_t j = draw_one<TI>(c, zrow, nvec, a.tail, G, nchunk, C, u * S, S, nm);
+      id = (int32_t)j;
+      lp = load_elem<TI>(zrow, j) - L;
+    }
+    a.ids_out[row * M + i] = id;
+    if (a.logp) a.logp[row * M + i] = lp;
+  }
+}
+
+// ---------------------------------------------------------------- top-k
+
+// Sort key: the IEEE-754 total order of the fp32 bits (bf16 widened), with
+// -0 taken as +0.  Larger key = larger value.
+__device__ __forceinline__ uint32_t order_key(uint32_t bits) {
+  bits = bits == 0x80000000u ? 0u : bits;
+  return (bits & 0x80000000u) ? ~bits : (bits | 0x80000000u);
+}
+__device__ __forceinline__ float key_value(uint32_t key) {
+  return __uint_as_float((key & 0x80000000u) ? (key & 0x7FFFFFFFu) : ~key);
+}
+
+__device__ __forceinline__ uint32_t shfl_xor_u32(uint32_t v, int m) {
+  return (uint32_t)__shfl_xor((int)v, m, 64);
+}
+__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int m) {
+  const uint32_t lo = shfl_xor_u32((uint32_t)v, m), hi = shfl_xor_u32((uint32_t)(v >> 32), m);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// Bitonic sort of one value per lane over the workgroup, descending: lane i
+// ends with the i-th largest.  Exchanges within a wavefront use lane
+// shuffles; wider ones go through LDS (two buffers, one barrier each).
+template <class T>
+__device__ T block_sort_desc(T v, T (*buf)[NT]) {
+  const int tid = threadIdx.x;
+  int ping = 0;
+#pragma unroll 1
+  for (int size = 2; size <= NT; size <<= 1) {
+#pragma unroll 1
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      T pv;
+      if (stride >= 64) {
+        buf[ping][tid] = v;
+        __syncthreads();
+        pv = buf[ping][tid ^ stride];
+        ping ^= 1;
+      } else if constexpr (sizeof(T) == 8) {
+        pv = shfl_xor_u64(v, stride);
+      } else {
+        pv = shfl_xor_u32(v, stride);
+      }
+      const bool take_max = ((tid & size) == 0) == ((tid & stride) == 0);
+      v = take_max ? (v > pv ? v : pv) : (v < pv ? v : pv);
+    }
+  }
+  return v;
+}
+
+// Bitonic sort, descending, of P entries held in LDS (P a power of two).
+__device__ void lds_sort_desc(uint64_t* s, uint32_t P) {
+  for (uint32_t size = 2; size <= P; size <<= 1) {
+    for (uint32_t stride = size >> 1; stride > 0; stride >>= 1) {
+      for (uint32_t i = threadIdx.x; i < P / 2; i += NT) {
+        const uint32_t lo = 2 * i - (i & (stride - 1)), hi = lo + stride;
+        const uint64_t x = s[lo], y = s[hi];
+        if ((lo & size) == 0 ? x < y : x > y) {
+          s[lo] = y;
+          s[hi] = x;
+        }
+      }
+      __syncthreads();
+    }
+  }
+}
+
+struct TopkLds {
+  uint32_t kbuf[2][NT];
+  uint64_t sbuf[2][NT];
+  uint64_t cand[kTopkCand];
+  uint32_t cnt;
+  uint32_t bound;
+  uint32_t ured[NW];
+  float red[NW];
+};
+
+// Calls f(key, j) for every element j of the row this lane holds (the
+// resident slots, or a streamed pass).  The resident registers pass through
+// an empty barrier first, so keys are recomputed in each pass rather than
+// kept live from an earlier one.
+template <class TI, int NSLOT, class F>
+__device__ __forceinline__ void each_key(typename TI::Vec (&x)[NSLOT > 0 ? NSLOT : 1],
+                                         const void* zrow, uint32_t nvec, int64_t V, int tail,
+                                         int tid, F&& f) {
+  const uint32_t V32 = (uint32_t)V;
+  if constexpr (NSLOT > 0) {
+#pragma unroll
+    for (int s = 0; s < NSLOT; ++s) keep_packed(x[s]);
+#pragma unroll
+    for (int s = 0; s < NSLOT; ++s) {
+      const uint32_t b = slot_base<NT>(s, nvec);
+      if ((uint32_t)(s * NT + NT) <= nvec || slot_owns<NT>(s, b, tid, nvec)) {
+        const uint32_t v = b + (uint32_t)tid;
+        float fv[4];
+        unpack<TI>(x[s], fv);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const uint32_t j = v * 4u + (uint32_t)e;
+          if (tail == TI::EPV || j < V32) f(order_key(__float_as_uint(fv[e])), j);
+        }
+      }
+    }
+  } else {
+    for (uint32_t v = tid; v < nvec; v += NT) {
+      float fv[4];
+      unpack<TI>(ld_cached<TI>(zrow, v), fv);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const uint32_t j = v * 4u + (uint32_t)e;
+        if (j < V32) f(order_key(__float_as_uint(fv[e])), j);
+      }
+    }
+  }
+}
+
+template <class TI, int NSLOT, bool LSE>
+__global__ void __launch_bounds__(NT) k_topk(CacheArgs a) {
+  __shared__ TopkLds sh;
+  const int tid = threadIdx.x;
+  const int64_t row = blockIdx.x;
+  const int k = a.K;
+  if (a.mask && a.mask[row] == 0) {
+    for (int i = tid; i < k; i += NT) {
+      a.ids_out[row * k + i] = 0;
+      if (a.logp) a.logp[row * k + i] = 0.f;
+    }
+    if (tid == 0 && a.lse_out) a.lse_out[row] = 0.f;
+    return;
+  }
+  const void* zrow = (const char*)a.logits + row * a.ld * TI::BYTES;
+  const uint32_t nvec = (uint32_t)a.nvec;
+  const int64_t V = a.V;
+  typename TI::Vec x[NSLOT > 0 ? NSLOT : 1];
+  if constexpr (NSLOT > 0) load_row<TI, NSLOT>(zrow, nvec, a.tail, tid, x);
+
+  float L = 0.f;
+  if constexpr (LSE) {
+    float m, ssum;
+    if constexpr (NSLOT > 0) {
+      m = block_max<NW>(lane_max<TI, NSLOT>(x), sh.red);
+#pragma unroll
+      for (int s = 0; s < NSLOT; ++s) keep_packed(x[s]);
+      ssum = block_sum<NW>(lane_sumexp<TI, NSLOT>(x, -m * kLog2e), sh.red);
+#pragma unroll
+      for (int s = 0; s < NSLOT; ++s) keep_packed(x[s]);
+    } else {
+      float mx = kNegInf;
+      for (uint32_t v = tid; v < nvec; v += NT) {
+        float f[4];
+        unpack<TI>(load_vec<TI>(zrow, v, nvec, a.tail), f);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) mx = fmaxf(mx, f[e]);
+      }
+      m = block_max<NW>(mx, sh.red);
+      const float nm = -m * kLog2e;
+      float sm = 0.f;
+      for (uint32_t v = tid; v < nvec; v += NT) sm = vec_sumexp<TI>(load_vec<TI>(zrow, v, nvec, a.tail), nm, sm);
+      ssum = block_sum<NW>(sm, sh.red);
+    }
+    L = m + logf(ssum);
+  }
+
+  // A lower bound on the k-th largest key: the k-th largest of the lanes'
+  // maxima (k lanes hold an element at least that large).  A lane with no
+  // element contributes key 0, below every element.
+  uint32_t lmax = 0;
+  each_key<TI, NSLOT>(x, zrow, nvec, V, a.tail, tid, [&](uint32_t key, uint32_t) { lmax = max(lmax, key); });
+  const uint32_t sorted = block_sort_desc<uint32_t>(lmax, sh.kbuf);
+  if (tid == k - 1) sh.bound = sorted;
+  if (tid == 0) sh.cnt = 0u;
+  __syncthreads();
+  const uint32_t bound = sh.bound;
+  each_key<TI, NSLOT>(x, zrow, nvec, V, a.tail, tid, [&](uint32_t key, uint32_t j) {
+    if (key >= bound) {
+      const uint32_t pos = atomicAdd(&sh.cnt, 1u);
+      if (pos < (uint32_t)kTopkCand) sh.cand[pos] = ((uint64_t)key << 32) | (0xFFFFFFFFu - j);
+    }
+  });
+  __syncthreads();
+  const uint32_t cnt = sh.cnt;
+
+  uint64_t mine = 0;  // after sorting: this lane's rank in the support
+  if (cnt >= (uint32_t)k && cnt <= (uint32_t)NT) {
+    mine = block_sort_desc<uint64_t>(tid < (int)cnt ? sh.cand[tid] : 0ull, sh.sbuf);
+  } else if (cnt >= (uint32_t)k && cnt <= (uint32_t)kTopkCand) {
+    uint32_t P = NT;
+    while (P < cnt) P <<= 1;
+    for (uint32_t i = cnt + tid; i < P; i += NT) sh.cand[i] = 0ull;
+    __syncthreads();
+    lds_sort_desc(sh.cand, P);
+    mine = sh.cand[tid];
+  } else {
+    // Too many candidates (a row with many equal large values): find the
+    // k-th largest key th by bisection over key bits, then the need-th
+    // lowest index among the elements equal to th, by counting passes.
+    auto count = [&](auto&& pred) {
+      uint32_t n = 0;
+      each_key<TI, NSLOT>(x, zrow, nvec, V, a.tail, tid, [&](uint32_t key, uint32_t j) { n += pred(key, j) ? 1u : 0u; });
+      return block_add_u32(n, sh.ured);
+    };
+    uint32_t th = 0;
+    for (int bit = 31; bit >= 0; --bit) {
+      const uint32_t t = th | (1u << bit);
+      if (count([&](uint32_t key, uint32_t) { return key >= t; }) >= (uint32_t)k) th = t;
+    }
+    const uint32_t gt = th == 0xFFFFFFFFu ? 0u : count([&](uint32_t key, uint32_t) { return key > th; });
+    const uint32_t need = (uint32_t)k - gt;
+    uint32_t y = 0;
+    for (int bit = 30; bit >= 0; --bit) {
+      const uint32_t t = y | (1u << bit);
+      if (count([&](uint32_t key, uint32_t j) { return key == th && j < t; }) < need) y = t;
+    }
+    if (tid == 0) sh.cnt = 0u;
+    __syncthreads();
+    each_key<TI, NSLOT>(x, zrow, nvec, V, a.tail, tid, [&](uint32_t key, uint32_t j) {
+      if (key > th || (key == th && j <= y)) {
+        const uint32_t pos = atomicAdd(&sh.cnt, 1u);
+        if (pos < (uint32_t)kTopkCand) sh.cand[pos] = ((uint64_t)key << 32) | (0xFFFFFFFFu - j);
+      }
+    });
+    __syncthreads();
+    mine = block_sort_desc<uint64_t>(tid < k ? sh.cand[tid] : 0ull, sh.sbuf);
+  }
+
+  if (tid < k) {
+    const uint32_t j = 0xFFFFFFFFu - (uint32_t)mine;
+    a.ids_out[row * k + tid] = (int32_t)j;
+    if (a.logp) a.logp[row * k + tid] = key_value((uint32_t)(mine >> 32)) - L;
+  }
+  if (tid == 0 && a.lse_out) a.lse_out[row] = L;
+}
+
+// ---------------------------------------------------------------- scoring
+
+template <class TI, int NSLOT>
+__global__ void __launch_bounds__(NT) k_score(CacheArgs a) {
+  __shared__ float s_red[NW];
+  __shared__ Stats s_st[NW];
+  const int tid = threadIdx.x;
+  const int64_t row = blockIdx.x;
+  const int K = a.K;
+  if (a.mask && a.mask[row] == 0) {
+    for (int i = tid; i < K; i += NT) a.logp[row * K + i] = 0.f;
+    if (tid == 0 && a.lse_out) a.lse_out[row] = 0.f;
+    return;
+  }
+  const void* zrow = (const char*)a.logits + row * a.ld * TI::BYTES;
+  const uint32_t nvec = (uint32_t)a.nvec;
+  // the ids are requested before the row, so the gather does not wait behind it
+  int32_t id = 0;
+  if (tid < K) id = a.ids[row * K + tid];
+  float L;
+  if constexpr (NSLOT > 0) {
+    typename TI::Vec x[NSLOT];
+    load_row<TI, NSLOT>(zrow, nvec, a.tail, tid, x);
+    const float m = block_max<NW>(lane_max<TI, NSLOT>(x), s_red);
+#pragma unroll
+    for (int s = 0; s < NSLOT; ++s) keep_packed(x[s]);
+    L = m + logf(block_sum<NW>(lane_sumexp<TI, NSLOT>(x, -m * kLog2e), s_red));
+  } else {
+    Stats st = stats_empty();
+    for (uint32_t v = tid; v < nvec; v += NT) {
+      const typename TI::Vec xv = load_vec<TI>(zrow, v, nvec, a.tail);
+      stats_add<TI, false>(st, xv, xv);
+    }
+    st = block_merge<false, NW>(st, s_st);
+    L = st.mz + logf(st.sz);
+  }
+  for (int i = tid; i < K; i += NT) {
+    if (i != tid) id = a.ids[row * K + i];
+    const bool ok = id >= 0 && (int64_t)id < a.V;
+    a.logp[row * K + i] = ok ? load_elem<TI>(zrow, id) - L : __builtin_nanf("");
+  }
+  if (tid == 0 && a.lse_out) a.lse_out[row] = L;
+}
+
+// ---------------------------------------------------------------- dispatch
+
+template <class TI, int NSLOT>
+hipError_t launch_op(const CacheArgs& a, CacheOp op, hipStream_t stream) {
+  const dim3 grid((unsigned)a.N), block(NT);
+  switch (op) {
+    case CacheOp::Sample:
+      hipLaunchKernelGGL((k_sample<TI, NSLOT>), grid, block, 0, stream, a);
+      break;
+    case CacheOp::Topk:
+      if (a.logp || a.lse_out)
+        hipLaunchKernelGGL((k_topk<TI, NSLOT, true>), grid, block, 0, stream, a);
+      else
+        hipLaunchKernelGGL((k_topk<TI, NSLOT, false>), grid, block, 0, stream, a);
+      break;
+    case CacheOp::Score:
+      hipLaunchKernelGGL((k_score<TI, NSLOT>), grid, block, 0, stream, a);
+      break;
+  }
+  return hipGetLastError();
+}
+
+template <class TI>
+hipError_t launch_dt(const CacheArgs& a, CacheOp op, bool resident, hipStream_t stream) {
+  if (!resident) return launch_op<TI, 0>(a, op, stream);
+  constexpr int big = TI::BYTES == 2 ? 38 : 19, small = TI::BYTES == 2 ? 16 : 8;
+  if (a.nvec <= (int64_t)small * NT) return launch_op<TI, small>(a, op, stream);
+  return launch_op<TI, big>(a, op, stream);
+}
+
+}  // namespace
+
+hipError_t launch_cache(const CacheArgs& a, CacheOp op, int in_dt, bool resident,
+                        hipStream_t stream) {
+  if (a.N == 0) return hipSuccess;
+  return in_dt == BF16 ? launch_dt<InBf16>(a, op, resident, stream)
+                       : launch_dt<InF32>(a, op, resident, stream);
+}
+
+}  // namespace opd

@@ -65,6 +65,32 @@ struct Args {
 
 enum class Path { RowResidentSmall, RowResidentLarge, RowStream, Split };
 
+// Building the cache (opd_sample_actions, opd_topk_support, opd_score_actions).
+enum class CacheOp { Sample, Topk, Score };
+// Chunk sums of a row that the sampler keeps in LDS: 38 * 1024 floats (152 KiB).
+constexpr int kCdfChunks = 38 * kRowThreads;
+// Top-k candidates kept in LDS before the exact counting fallback.
+constexpr int kTopkCand = 4096;
+
+struct CacheArgs {
+  const void* logits;
+  int64_t N, V, ld;
+  int64_t nvec;         // 4-element vectors per row covering [0, V)
+  int tail;             // valid elements in the last vector
+  int K;                // draws M, support size k, or scored ids K
+  const float* u;       // [N, K] uniforms (sampling)
+  const int32_t* ids;   // [N, K] ids to score (scoring)
+  const uint8_t* mask;  // nullable
+  int32_t* ids_out;     // [N, K] draws or support (sampling, top-k)
+  float* logp;          // [N, K] log-probs at the ids; nullable except for scoring
+  float* lse_out;       // [N] nullable
+  int64_t G;            // sampler: vectors per CDF chunk
+  int64_t nchunk;       // sampler: chunks per row
+};
+
+hipError_t launch_cache(const CacheArgs& a, CacheOp op, int in_dt, bool resident,
+                        hipStream_t stream);
+
 // Launchers; each returns hipSuccess or the launch error.
 hipError_t launch_rowwise(const Args& a, int est, int in_dt, int out_dt, Path path, bool read_row,
                           hipStream_t stream);

@@ -150,3 +150,54 @@ def test_validate_cache_argument_errors():
     assert L.opd_validate_cache(None, 0, 4, 100, 4, 0, FAKE, None) == NULL
     assert L.opd_validate_cache(ctypes.byref(c), 3, 4, 100, 0, 4, FAKE, None) == NULL
     assert L.opd_validate_cache(ctypes.byref(c), 4, 4, 100, 0, 0, FAKE, None) == OK  # dense: no-op
+
+
+# ---------------------------------------------------------------- cache building
+
+def call_row(op, logits=FAKE, dtype=1, N=4, V=1024, ld=None, K=4, u=FAKE, ids=FAKE, mask=None,
+             out=FAKE, logp=FAKE, lse=None):
+    ld = V if ld is None else ld
+    L = opd.lib()
+    if op == "sample":
+        return L.opd_sample_actions(logits, dtype, N, V, ld, K, u, mask, out, logp, lse, None)
+    if op == "topk":
+        return L.opd_topk_support(logits, dtype, N, V, ld, K, mask, out, logp, lse, None)
+    return L.opd_score_actions(logits, dtype, N, V, ld, ids, K, mask, logp, lse, None)
+
+
+@pytest.mark.parametrize("op", ["sample", "topk", "score"])
+@pytest.mark.parametrize("kw,code", [
+    (dict(dtype=2), DTYPE),
+    (dict(dtype=-1), DTYPE),
+    (dict(N=-1), SHAPE),
+    (dict(N=2 ** 31), SHAPE),
+    (dict(V=1), SHAPE),
+    (dict(V=2 ** 31), SHAPE),
+    (dict(ld=1000), SHAPE),
+    (dict(K=0), SUPPORT),
+    (dict(K=257), SUPPORT),
+    (dict(logits=None), NULL),
+    (dict(logits=FAKE + 2), ALIGN),
+    (dict(V=1020), ALIGN),                  # bf16 rows of 2040 bytes
+    (dict(dtype=0, V=1022), ALIGN),         # fp32 rows of 4088 bytes
+])
+def test_cache_argument_errors_are_reported_before_launch(op, kw, code):
+    assert call_row(op, **kw) == code
+
+
+@pytest.mark.parametrize("op,kw,code", [
+    ("sample", dict(u=None), NULL),
+    ("sample", dict(out=None), NULL),
+    ("sample", dict(K=300, V=100000), SUPPORT),   # M is limited to 256 draws
+    ("topk", dict(out=None), NULL),
+    ("topk", dict(K=9, V=8), SUPPORT),            # k > V
+    ("score", dict(ids=None), NULL),
+    ("score", dict(logp=None), NULL),
+])
+def test_cache_required_pointers_and_sizes(op, kw, code):
+    assert call_row(op, **kw) == code
+
+
+@pytest.mark.parametrize("op", ["sample", "topk", "score"])
+def test_cache_zero_rows_is_a_noop(op):
+    assert call_row(op, N=0, logits=None, u=None, ids=None, out=None, logp=None) == OK
