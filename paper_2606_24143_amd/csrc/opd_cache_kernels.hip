@@ -362,12 +362,14 @@ __device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int m) {
 // Bitonic sort of one value per lane over the workgroup, descending: lane i
 // ends with the i-th largest.  Exchanges within a wavefront use lane
 // shuffles; wider ones go through LDS (two buffers, one barrier each).
+// Only the first P lanes (P a power of two) take part; the others keep their
+// values.
 template <class T>
-__device__ T block_sort_desc(T v, T (*buf)[NT]) {
+__device__ T block_sort_desc(T v, T (*buf)[NT], int P = NT) {
   const int tid = threadIdx.x;
   int ping = 0;
 #pragma unroll 1
-  for (int size = 2; size <= NT; size <<= 1) {
+  for (int size = 2; size <= P; size <<= 1) {
 #pragma unroll 1
     for (int stride = size >> 1; stride > 0; stride >>= 1) {
       T pv;
@@ -383,6 +385,21 @@ __device__ T block_sort_desc(T v, T (*buf)[NT]) {
       }
       const bool take_max = ((tid & size) == 0) == ((tid & stride) == 0);
       v = take_max ? (v > pv ? v : pv) : (v < pv ? v : pv);
+    }
+  }
+  return v;
+}
+
+// Bitonic sort of one value per lane within a wavefront, descending.
+__device__ __forceinline__ uint32_t wave_sort_desc(uint32_t v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int size = 2; size <= 64; size <<= 1) {
+#pragma unroll
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      const uint32_t pv = shfl_xor_u32(v, stride);
+      const bool take_max = ((lane & size) == 0) == ((lane & stride) == 0);
+      v = take_max ? max(v, pv) : min(v, pv);
     }
   }
   return v;
@@ -406,13 +423,13 @@ __device__ void lds_sort_desc(uint64_t* s, uint32_t P) {
 }
 
 struct TopkLds {
-  uint32_t kbuf[2][NT];
   uint64_t sbuf[2][NT];
   uint64_t cand[kTopkCand];
   uint32_t cnt;
-  uint32_t bound;
+  uint32_t wbound[NW];
   uint32_t ured[NW];
   float red[NW];
+  Stats st[NW];
 };
 
 // Calls f(key, j) for every element j of the row this lane holds (the
@@ -474,55 +491,96 @@ __global__ void __launch_bounds__(NT) k_topk(CacheArgs a) {
   typename TI::Vec x[NSLOT > 0 ? NSLOT : 1];
   if constexpr (NSLOT > 0) load_row<TI, NSLOT>(zrow, nvec, a.tail, tid, x);
 
-  float L = 0.f;
-  if constexpr (LSE) {
-    float m, ssum;
-    if constexpr (NSLOT > 0) {
-      m = block_max<NW>(lane_max<TI, NSLOT>(x), sh.red);
+  // Each lane's largest value (NaN ignored), which also starts the
+  // log-partition; a lane with no element reports -inf.
+  float lmx = kNegInf, L = 0.f;
+  if constexpr (NSLOT > 0) {
+    lmx = lane_max<TI, NSLOT>(x);
+#pragma unroll
+    for (int s = 0; s < NSLOT; ++s) keep_packed(x[s]);
+    if constexpr (LSE) {
+      const float m = block_max<NW>(lmx, sh.red);
+      L = m + logf(block_sum<NW>(lane_sumexp<TI, NSLOT>(x, -m * kLog2e), sh.red));
 #pragma unroll
       for (int s = 0; s < NSLOT; ++s) keep_packed(x[s]);
-      ssum = block_sum<NW>(lane_sumexp<TI, NSLOT>(x, -m * kLog2e), sh.red);
-#pragma unroll
-      for (int s = 0; s < NSLOT; ++s) keep_packed(x[s]);
+    }
+  } else {
+    if constexpr (LSE) {
+      Stats st = stats_empty();
+      for (uint32_t v = tid; v < nvec; v += NT) {
+        const typename TI::Vec xv = load_vec<TI>(zrow, v, nvec, a.tail);
+        stats_add<TI, false>(st, xv, xv);
+      }
+      lmx = st.mz;
+      st = block_merge<false, NW>(st, sh.st);
+      L = st.mz + logf(st.sz);
     } else {
-      float mx = kNegInf;
       for (uint32_t v = tid; v < nvec; v += NT) {
         float f[4];
         unpack<TI>(load_vec<TI>(zrow, v, nvec, a.tail), f);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) mx = fmaxf(mx, f[e]);
+        for (int e = 0; e < 4; ++e) lmx = fmaxf(lmx, f[e]);
       }
-      m = block_max<NW>(mx, sh.red);
-      const float nm = -m * kLog2e;
-      float sm = 0.f;
-      for (uint32_t v = tid; v < nvec; v += NT) sm = vec_sumexp<TI>(load_vec<TI>(zrow, v, nvec, a.tail), nm, sm);
-      ssum = block_sum<NW>(sm, sh.red);
     }
-    L = m + logf(ssum);
   }
 
-  // A lower bound on the k-th largest key: the k-th largest of the lanes'
-  // maxima (k lanes hold an element at least that large).  A lane with no
-  // element contributes key 0, below every element.
-  uint32_t lmax = 0;
-  each_key<TI, NSLOT>(x, zrow, nvec, V, a.tail, tid, [&](uint32_t key, uint32_t) { lmax = max(lmax, key); });
-  const uint32_t sorted = block_sort_desc<uint32_t>(lmax, sh.kbuf);
-  if (tid == k - 1) sh.bound = sorted;
-  if (tid == 0) sh.cnt = 0u;
+  // A lower bound on the k-th largest key: in every wave, r = ceil(k / 16)
+  // lanes hold a value at least that wave's r-th largest lane maximum, so
+  // 16 r >= k elements are at least the smallest of those 16 values.  A lane
+  // whose maximum overstates its elements (none, or only NaN) can only
+  // lower the bound to -inf or below, where every element is collected.
+  {
+    const uint32_t lkey = (uint32_t)tid < nvec ? order_key(__float_as_uint(lmx)) : 0u;
+    const uint32_t srt = wave_sort_desc(lkey);
+    const int r = (k + NW - 1) / NW;
+    const uint32_t wb = (uint32_t)__shfl((int)srt, r - 1, 64);
+    if ((tid & 63) == 0) sh.wbound[tid >> 6] = wb;
+    if (tid == 0) sh.cnt = 0u;
+  }
   __syncthreads();
-  const uint32_t bound = sh.bound;
-  each_key<TI, NSLOT>(x, zrow, nvec, V, a.tail, tid, [&](uint32_t key, uint32_t j) {
-    if (key >= bound) {
+  uint32_t bound = sh.wbound[0];
+#pragma unroll
+  for (int w = 1; w < NW; ++w) bound = min(bound, sh.wbound[w]);
+  // Candidates: every element not below the bound's value, and every NaN
+  // (!(v < b) holds for both); their exact keys decide the order.
+  const float bval = key_value(bound);
+  auto take = [&](float v, uint32_t j) {
+    if (!(v < bval)) {
       const uint32_t pos = atomicAdd(&sh.cnt, 1u);
-      if (pos < (uint32_t)kTopkCand) sh.cand[pos] = ((uint64_t)key << 32) | (0xFFFFFFFFu - j);
+      if (pos < (uint32_t)kTopkCand)
+        sh.cand[pos] = ((uint64_t)order_key(__float_as_uint(v)) << 32) | (0xFFFFFFFFu - j);
     }
-  });
+  };
+  if constexpr (NSLOT > 0) {
+#pragma unroll
+    for (int s = 0; s < NSLOT; ++s) {
+      const uint32_t b = slot_base<NT>(s, nvec);
+      if ((uint32_t)(s * NT + NT) <= nvec || slot_owns<NT>(s, b, tid, nvec)) {
+        const uint32_t v = b + (uint32_t)tid;
+        float f[4];
+        unpack<TI>(x[s], f);
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (a.tail == TI::EPV || v * 4u + e < (uint32_t)V) take(f[e], v * 4u + e);
+      }
+    }
+  } else {
+    for (uint32_t v = tid; v < nvec; v += NT) {
+      float f[4];
+      unpack<TI>(ld_cached<TI>(zrow, v), f);
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (v * 4u + e < (uint32_t)V) take(f[e], v * 4u + e);
+    }
+  }
   __syncthreads();
   const uint32_t cnt = sh.cnt;
 
   uint64_t mine = 0;  // after sorting: this lane's rank in the support
   if (cnt >= (uint32_t)k && cnt <= (uint32_t)NT) {
-    mine = block_sort_desc<uint64_t>(tid < (int)cnt ? sh.cand[tid] : 0ull, sh.sbuf);
+    int P = 2;
+    while (P < (int)cnt) P <<= 1;
+    mine = block_sort_desc<uint64_t>(tid < (int)cnt ? sh.cand[tid] : 0ull, sh.sbuf, P);
   } else if (cnt >= (uint32_t)k && cnt <= (uint32_t)kTopkCand) {
     uint32_t P = NT;
     while (P < cnt) P <<= 1;
@@ -534,9 +592,11 @@ __global__ void __launch_bounds__(NT) k_topk(CacheArgs a) {
     // Too many candidates (a row with many equal large values): find the
     // k-th largest key th by bisection over key bits, then the need-th
     // lowest index among the elements equal to th, by counting passes.
+    // These passes re-read the row from memory (a rare path; compact code).
+    typename TI::Vec none[1];
     auto count = [&](auto&& pred) {
       uint32_t n = 0;
-      each_key<TI, NSLOT>(x, zrow, nvec, V, a.tail, tid, [&](uint32_t key, uint32_t j) { n += pred(key, j) ? 1u : 0u; });
+      each_key<TI, 0>(none, zrow, nvec, V, a.tail, tid, [&](uint32_t key, uint32_t j) { n += pred(key, j) ? 1u : 0u; });
       return block_add_u32(n, sh.ured);
     };
     uint32_t th = 0;
@@ -553,7 +613,7 @@ __global__ void __launch_bounds__(NT) k_topk(CacheArgs a) {
     }
     if (tid == 0) sh.cnt = 0u;
     __syncthreads();
-    each_key<TI, NSLOT>(x, zrow, nvec, V, a.tail, tid, [&](uint32_t key, uint32_t j) {
+    each_key<TI, 0>(none, zrow, nvec, V, a.tail, tid, [&](uint32_t key, uint32_t j) {
       if (key > th || (key == th && j <= y)) {
         const uint32_t pos = atomicAdd(&sh.cnt, 1u);
         if (pos < (uint32_t)kTopkCand) sh.cand[pos] = ((uint64_t)key << 32) | (0xFFFFFFFFu - j);
@@ -573,44 +633,72 @@ __global__ void __launch_bounds__(NT) k_topk(CacheArgs a) {
 
 // ---------------------------------------------------------------- scoring
 
-template <class TI, int NSLOT>
-__global__ void __launch_bounds__(NT) k_score(CacheArgs a) {
-  __shared__ float s_red[NW];
-  __shared__ Stats s_st[NW];
+// Scoring reads each row once and writes a handful of values, so it is
+// organised for overlap rather than residency: 256-lane workgroups with a
+// small register footprint (several per CU), each lane loading batches of
+// kScoreBatch vectors and folding them into a running (max, sum-exp) with
+// one rescale per batch.
+constexpr int kScoreThreads = 256;
+constexpr int kScoreBatch = 8;
+
+template <class TI>
+__global__ void __launch_bounds__(kScoreThreads) k_score(CacheArgs a) {
+  constexpr int T = kScoreThreads, W = T / 64, B = kScoreBatch;
+  typedef typename TI::Vec Vec;
+  __shared__ Stats s_st[W];
   const int tid = threadIdx.x;
   const int64_t row = blockIdx.x;
-  const int K = a.K;
+  const int K = a.K;  // <= OPD_K_MAX == T: one id per lane
   if (a.mask && a.mask[row] == 0) {
-    for (int i = tid; i < K; i += NT) a.logp[row * K + i] = 0.f;
+    if (tid < K) a.logp[row * K + tid] = 0.f;
     if (tid == 0 && a.lse_out) a.lse_out[row] = 0.f;
     return;
   }
   const void* zrow = (const char*)a.logits + row * a.ld * TI::BYTES;
   const uint32_t nvec = (uint32_t)a.nvec;
+  const bool ragged = a.tail != TI::EPV;
   // the ids are requested before the row, so the gather does not wait behind it
-  int32_t id = 0;
-  if (tid < K) id = a.ids[row * K + tid];
-  float L;
-  if constexpr (NSLOT > 0) {
-    typename TI::Vec x[NSLOT];
-    load_row<TI, NSLOT>(zrow, nvec, a.tail, tid, x);
-    const float m = block_max<NW>(lane_max<TI, NSLOT>(x), s_red);
+  const int32_t id = tid < K ? a.ids[row * K + tid] : 0;
+  float m = kNegInf, sum = 0.f;
+  for (uint32_t v0 = 0; v0 < nvec; v0 += T * B) {
+    Vec xb[B];
 #pragma unroll
-    for (int s = 0; s < NSLOT; ++s) keep_packed(x[s]);
-    L = m + logf(block_sum<NW>(lane_sumexp<TI, NSLOT>(x, -m * kLog2e), s_red));
-  } else {
-    Stats st = stats_empty();
-    for (uint32_t v = tid; v < nvec; v += NT) {
-      const typename TI::Vec xv = load_vec<TI>(zrow, v, nvec, a.tail);
-      stats_add<TI, false>(st, xv, xv);
+    for (int b = 0; b < B; ++b) {
+      const uint32_t v = v0 + (uint32_t)(b * T + tid);
+      xb[b] = ld_nt<TI>(zrow, min(v, nvec - 1));  // clamped: every lane loads
     }
-    st = block_merge<false, NW>(st, s_st);
-    L = st.mz + logf(st.sz);
+    float f[B][4];
+    float bm = kNegInf;
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+      const uint32_t v = v0 + (uint32_t)(b * T + tid);
+      Vec xv = xb[b];
+      if (v >= nvec) xv = neg_inf_vec<TI>();
+      else if (ragged && v == nvec - 1) xv = tail_masked<TI>(xv, a.tail);
+      unpack<TI>(xv, f[b]);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) bm = fmaxf(bm, f[b][e]);
+    }
+    const float mn = fmaxf(m, bm);
+    if (mn != kNegInf) {
+      float acc = sum * rescale(m, mn);
+      const float nm = -mn * kLog2e;
+#pragma unroll
+      for (int b = 0; b < B; ++b)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc += ez(f[b][e], nm);
+      sum = acc;
+      m = mn;
+    }
   }
-  for (int i = tid; i < K; i += NT) {
-    if (i != tid) id = a.ids[row * K + i];
+  Stats st = stats_empty();
+  st.mz = m;
+  st.sz = sum;
+  st = block_merge<false, W>(st, s_st);
+  const float L = st.mz + logf(st.sz);
+  if (tid < K) {
     const bool ok = id >= 0 && (int64_t)id < a.V;
-    a.logp[row * K + i] = ok ? load_elem<TI>(zrow, id) - L : __builtin_nanf("");
+    a.logp[row * K + tid] = ok ? load_elem<TI>(zrow, id) - L : __builtin_nanf("");
   }
   if (tid == 0 && a.lse_out) a.lse_out[row] = L;
 }
@@ -631,7 +719,6 @@ hipError_t launch_op(const CacheArgs& a, CacheOp op, hipStream_t stream) {
         hipLaunchKernelGGL((k_topk<TI, NSLOT, false>), grid, block, 0, stream, a);
       break;
     case CacheOp::Score:
-      hipLaunchKernelGGL((k_score<TI, NSLOT>), grid, block, 0, stream, a);
       break;
   }
   return hipGetLastError();
@@ -639,6 +726,10 @@ hipError_t launch_op(const CacheArgs& a, CacheOp op, hipStream_t stream) {
 
 template <class TI>
 hipError_t launch_dt(const CacheArgs& a, CacheOp op, bool resident, hipStream_t stream) {
+  if (op == CacheOp::Score) {
+    hipLaunchKernelGGL((k_score<TI>), dim3((unsigned)a.N), dim3(kScoreThreads), 0, stream, a);
+    return hipGetLastError();
+  }
   if (!resident) return launch_op<TI, 0>(a, op, stream);
   constexpr int big = TI::BYTES == 2 ? 38 : 19, small = TI::BYTES == 2 ? 16 : 8;
   if (a.nvec <= (int64_t)small * NT) return launch_op<TI, small>(a, op, stream);
