@@ -70,6 +70,10 @@ def lib():
         L.oracle_cache_rows.argtypes = [ctypes.c_int, ctypes.c_int, P, i64, i64, i64, ctypes.c_int,
                                         P, P, P, P, P, ctypes.c_int]
         L.oracle_cache_rows.restype = ctypes.c_int
+        L.oracle_mc_diagnostics.argtypes = [P, P, P, P, i64, ctypes.c_int, P, ctypes.c_double,
+                                            ctypes.c_double, P, ctypes.c_int, i64, P, P, P, P, P,
+                                            P, P]
+        L.oracle_mc_diagnostics.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -203,3 +207,35 @@ def cache_rows(op: str, dtype: int, logits: np.ndarray, V: int, K: int, *, unifo
     if rc != 0:
         raise ValueError("oracle_cache_rows rejected its arguments (%d)" % rc)
     return {"ids": out_ids, "logp": logp, "lse": lse}
+
+
+# ---------------------------------------------------------------- MC diagnostics
+
+def mc_diagnostics(lse, gathered, tau, beta, *, mask=None, q: float = 0.99, eps: float = CLIP_EPS,
+                   group_sizes=(), seq_len: int = 0) -> dict:
+    """Diagnostics of the MC estimator in double from per-token lse [N],
+    gathered student logits, tau and beta [N, M].  Returns per-token
+    "mean", "var", "rho_max" and batch "rho_quantile", "clip_frac",
+    "ratio_local", "ratio_seq" (one entry per group size)."""
+    lse = np.ascontiguousarray(lse, np.float64)
+    gathered = np.ascontiguousarray(gathered, np.float64)
+    tau = np.ascontiguousarray(tau, np.float32)
+    beta = np.ascontiguousarray(beta, np.float32)
+    N, M = gathered.shape
+    mask = None if mask is None else np.ascontiguousarray(mask, np.uint8)
+    gs = np.ascontiguousarray(group_sizes, np.int32)
+    out = {"mean": np.zeros(N), "var": np.zeros(N), "rho_max": np.zeros(N),
+           "rho_quantile": np.zeros(1), "clip_frac": np.zeros(1),
+           "ratio_local": np.zeros(max(len(gs), 1)), "ratio_seq": np.zeros(max(len(gs), 1))}
+    rc = lib().oracle_mc_diagnostics(_p(lse), _p(gathered), _p(tau), _p(beta), N, M, _p(mask), q,
+                                     eps, _p(gs) if len(gs) else None, len(gs), seq_len,
+                                     _p(out["mean"]), _p(out["var"]), _p(out["rho_max"]),
+                                     _p(out["rho_quantile"]), _p(out["clip_frac"]),
+                                     _p(out["ratio_local"]), _p(out["ratio_seq"]))
+    if rc != 0:
+        raise ValueError("oracle_mc_diagnostics rejected its arguments (%d)" % rc)
+    out["rho_quantile"] = float(out["rho_quantile"][0])
+    out["clip_frac"] = float(out["clip_frac"][0])
+    out["ratio_local"] = out["ratio_local"][:len(gs)]
+    out["ratio_seq"] = out["ratio_seq"][:len(gs)]
+    return out

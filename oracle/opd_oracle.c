@@ -565,3 +565,143 @@ int oracle_cache_rows(int op, int dtype, const void* logits, int64_t n_rows, int
   }
   return err;
 }
+
+/* ------------------------------------------------------------------------
+ * Diagnostics of the Monte-Carlo estimator (Sec. 5.2, Fig. 5: the p99 tail
+ * of the importance ratio rho_theta; App. E: variance of the m-sample
+ * estimator at a fixed prefix and after averaging over the tokens of a
+ * sequence).  Inputs are what the loss call returns or reads per token t:
+ * L_t = log sum_j exp(z_j), the student logits z_{t,i} at the M cached
+ * samples, and the cached tau_{t,i} = log q, beta_{t,i} = log p_old.
+ *   log p_theta = z - L,  A = tau - log p_theta,  rho = exp(log p_theta - beta),
+ *   X_{t,i} = -rho_{t,i} A_{t,i}   (one-sample estimate; the loss is their mean)
+ * Per valid token: mean_t = (1/M) sum_i X, var_t = unbiased sample variance of
+ * X over i (M >= 2, else NaN), rhomax_t = max_i rho.
+ * Over all valid entries: the q-quantile of rho by nearest rank (the r-th
+ * smallest, r = ceil(q n), at least 1), and the fraction with |rho - 1| > eps.
+ * Variance ratios for group sizes m (M a multiple of m, G = M / m >= 2):
+ * group g holds samples [g m, g m + m); Y_{t,g} its mean.
+ *   local:  R_m = sum_t var_g(Y_{t,g}) / sum_t var_t
+ *   seq:    tokens [s T, s T + T) form sequence s; S_{s,g} = mean over its
+ *           valid tokens of Y_{t,g}; R_m = sum_s var_g(S_{s,g}) / sum_s
+ *           var_i(S1_{s,i}), S1 the same with single samples (m = 1).
+ * var_g is the unbiased variance over the G groups.  Replicate groups of the
+ * iid draws stand in for repeated sampling at the fixed prefix (or path).
+ * ------------------------------------------------------------------------ */
+
+static double unbiased_var(const double* x, int n) {
+  double mean = 0.0;
+  for (int i = 0; i < n; ++i) mean += x[i];
+  mean /= n;
+  double ss = 0.0;
+  for (int i = 0; i < n; ++i) ss += (x[i] - mean) * (x[i] - mean);
+  return ss / (n - 1);
+}
+
+static int cmp_double(const void* pa, const void* pb) {
+  const double a = *(const double*)pa, b = *(const double*)pb;
+  /* NaN after every number */
+  if (isnan(a) || isnan(b)) return isnan(a) - isnan(b);
+  return a < b ? -1 : (a > b ? 1 : 0);
+}
+
+int oracle_mc_diagnostics(const double* lse, const double* gathered, const float* tau,
+                          const float* beta, int64_t N, int M, const uint8_t* mask, double q,
+                          double eps, const int* group_sizes, int n_groups, int64_t seq_len,
+                          double* row_mean, double* row_var, double* row_rhomax,
+                          double* rho_quantile, double* clip_frac, double* ratio_local,
+                          double* ratio_seq) {
+  if (!lse || !gathered || !tau || !beta || N < 0 || M < 1 || !(q > 0.0 && q <= 1.0)) return -1;
+  if (n_groups < 0 || (n_groups > 0 && !group_sizes) || seq_len < 0) return -1;
+  for (int k = 0; k < n_groups; ++k)
+    if (group_sizes[k] < 1 || M % group_sizes[k] != 0 || M / group_sizes[k] < 2) return -1;
+  double* X = (double*)malloc(sizeof(double) * (size_t)(N * M + 1));
+  double* rho = (double*)malloc(sizeof(double) * (size_t)(N * M + 1));
+  double* Y = (double*)malloc(sizeof(double) * (size_t)(M + 1));
+  if (!X || !rho || !Y) {
+    free(X);
+    free(rho);
+    free(Y);
+    return -2;
+  }
+  int64_t n = 0, clipped = 0;
+  double sum_var = 0.0;
+  for (int64_t t = 0; t < N; ++t) {
+    const int valid = mask ? mask[t] != 0 : 1;
+    double mean = 0.0, mx = NAN; /* the largest ratio, NaN ratios ignored */
+    for (int i = 0; i < M && valid; ++i) {
+      const double lp = gathered[t * M + i] - lse[t];
+      const double r = exp(lp - (double)beta[t * M + i]);
+      const double A = (double)tau[t * M + i] - lp;
+      X[t * M + i] = -r * A;
+      rho[n++] = r;
+      if (fabs(r - 1.0) > eps) ++clipped;
+      mean += X[t * M + i];
+      if (!isnan(r) && (isnan(mx) || r > mx)) mx = r;
+    }
+    const double var = (valid && M >= 2) ? unbiased_var(X + t * M, M) : NAN;
+    if (valid && M >= 2) sum_var += var;
+    if (row_mean) row_mean[t] = valid ? mean / M : 0.0;
+    if (row_var) row_var[t] = valid ? var : 0.0;
+    if (row_rhomax) row_rhomax[t] = valid ? mx : 0.0;
+  }
+  if (rho_quantile) {
+    if (n == 0) {
+      *rho_quantile = NAN;
+    } else {
+      qsort(rho, (size_t)n, sizeof(double), cmp_double);
+      int64_t r = (int64_t)ceil(q * (double)n);
+      if (r < 1) r = 1;
+      *rho_quantile = rho[r - 1];
+    }
+  }
+  if (clip_frac) *clip_frac = n ? (double)clipped / (double)n : NAN;
+  for (int k = 0; k < n_groups; ++k) {
+    const int m = group_sizes[k], G = M / m;
+    if (ratio_local) {
+      double sum_g = 0.0;
+      for (int64_t t = 0; t < N; ++t) {
+        if (mask && mask[t] == 0) continue;
+        for (int g = 0; g < G; ++g) {
+          double y = 0.0;
+          for (int i = g * m; i < g * m + m; ++i) y += X[t * M + i];
+          Y[g] = y / m;
+        }
+        sum_g += unbiased_var(Y, G);
+      }
+      ratio_local[k] = sum_g / sum_var;
+    }
+    if (ratio_seq && seq_len > 0) {
+      double num = 0.0, den = 0.0;
+      double* S = (double*)calloc((size_t)M, sizeof(double));
+      double* S1 = (double*)calloc((size_t)M, sizeof(double));
+      for (int64_t s0 = 0; s0 < N; s0 += seq_len) {
+        const int64_t s1 = s0 + seq_len < N ? s0 + seq_len : N;
+        int64_t nv = 0;
+        for (int i = 0; i < M; ++i) S[i] = S1[i] = 0.0;
+        for (int64_t t = s0; t < s1; ++t) {
+          if (mask && mask[t] == 0) continue;
+          ++nv;
+          for (int i = 0; i < M; ++i) S1[i] += X[t * M + i];
+          for (int g = 0; g < G; ++g) {
+            double y = 0.0;
+            for (int i = g * m; i < g * m + m; ++i) y += X[t * M + i];
+            S[g] += y / m;
+          }
+        }
+        if (nv == 0) continue;
+        for (int i = 0; i < M; ++i) S1[i] /= (double)nv;
+        for (int g = 0; g < G; ++g) S[g] /= (double)nv;
+        num += unbiased_var(S, G);
+        den += unbiased_var(S1, M);
+      }
+      ratio_seq[k] = num / den;
+      free(S);
+      free(S1);
+    }
+  }
+  free(X);
+  free(rho);
+  free(Y);
+  return 0;
+}

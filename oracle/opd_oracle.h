@@ -71,6 +71,18 @@ int oracle_cache_rows(int op, int dtype, const void* logits, int64_t n_rows, int
                       int K, const float* uniforms, const uint8_t* mask, int32_t* ids,
                       double* logp, double* lse, int nthreads);
 
+/* Diagnostics of the MC estimator (Sec. 5.2, Fig. 5; App. E): per-token mean,
+ * unbiased variance and maximum importance ratio of the one-sample terms,
+ * the q-quantile (nearest rank) of the ratio over the batch, the fraction of
+ * ratios outside [1 - eps, 1 + eps], and fixed-prefix and sequence-level
+ * variance ratios for group sizes m.  See opd_oracle.c. */
+int oracle_mc_diagnostics(const double* lse, const double* gathered, const float* tau,
+                          const float* beta, int64_t N, int M, const uint8_t* mask, double q,
+                          double eps, const int* group_sizes, int n_groups, int64_t seq_len,
+                          double* row_mean, double* row_var, double* row_rhomax,
+                          double* rho_quantile, double* clip_frac, double* ratio_local,
+                          double* ratio_seq);
+
 /* Number of threads oracle_rows uses for nthreads = 0. */
 int oracle_max_threads(void);
 
