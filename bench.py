@@ -35,8 +35,8 @@ if ROOT not in sys.path:
 
 PEAK_HBM_GBS = 8000.0
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2606_24143_amd", "csrc", f)
-                  for f in ("opd_kernels.hip", "opd_cache_kernels.hip", "opd_api.cpp", "opd_internal.h",
-                            "opd_device.h")]
+                  for f in ("opd_kernels.hip", "opd_cache_kernels.hip", "opd_diag_kernels.hip",
+                            "opd_api.cpp", "opd_internal.h", "opd_device.h")]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 # estimators that read the top-k cache (renormalised and truncated)
 SUPPORT = ("fkl_topk", "rkl_topk", "fkl_topk_trunc", "rkl_topk_trunc")
@@ -85,6 +85,9 @@ def cache_op_bytes(w, op: str, n_valid: int, K: int) -> int:
     sampling; ids and log-probs out for top-k; ids in and log-probs out for
     scoring)."""
     in_b = 2 if w.dtype == 1 else 4
+    if op == "diag":
+        # reads lse, gathered logits, tau and beta; writes three per-token values
+        return n_valid * (4 + K * 12 + 12)
     per_tok = {"sample": K * (4 + 4 + 4), "topk": K * (4 + 4), "score": K * (4 + 4)}[op]
     return n_valid * (w.V * in_b + per_tok)
 
@@ -105,6 +108,19 @@ def cpu_cache_baseline(w, op, d, u, rows: int, threads: int):
     return {"value": n / el, "unit": "tokens/s", "cores": used, "kind": "oracle",
             "sample": "first %d of the %d token rows of the timed workload, fp64 oracle %s, "
                       "%.1f s wall on %d threads" % (n, w.N, op, el, used)}
+
+
+def cpu_diag_baseline(w, d, lse, gathered, seq):
+    """The oracle's MC diagnostics over the whole batch (single-threaded)."""
+    import oracle
+
+    t0 = time.perf_counter()
+    oracle.mc_diagnostics(lse, gathered, d["mc_tau"], d["mc_beta"], mask=d["mask"],
+                          group_sizes=(2, 4, 8), seq_len=seq)
+    el = time.perf_counter() - t0
+    return {"value": w.N / el, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "sample": "all %d token rows of the timed workload, fp64 oracle diagnostics, "
+                      "%.2f s wall on 1 thread" % (w.N, el)}
 
 
 def read_traffic(est_key: str):
@@ -160,8 +176,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="n32768_v151936_bf16_mc16")
     ap.add_argument("--estimator", default=None)
-    ap.add_argument("--op", default="loss", choices=("loss", "sample", "topk", "score"),
-                    help="time the loss (default) or one cache-building call")
+    ap.add_argument("--op", default="loss", choices=("loss", "sample", "topk", "score", "diag"),
+                    help="time the loss (default), one cache-building call, or the MC "
+                         "diagnostics")
     ap.add_argument("--cpu-rows", type=int, default=0, help="0 = every row")
     ap.add_argument("--cpu-threads", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -189,7 +206,7 @@ def main():
     w = synth.WORKLOADS[args.workload]
     est = args.estimator or w.estimators[0]
     op = args.op
-    if op == "topk" and w.k == 0 or op in ("sample", "score") and w.M == 0:
+    if op == "topk" and w.k == 0 or op in ("sample", "score", "diag") and w.M == 0:
         print("--op %s needs a workload with %s" % (op, "k > 0" if op == "topk" else "M > 0"),
               file=sys.stderr)
         sys.exit(2)
@@ -240,6 +257,17 @@ def main():
         elif op == "topk":
             def step():
                 opd.topk_support(logits, w.k, mask=mask, stream=stream)
+        elif op == "diag":
+            # the inputs are what an MC loss call returns (lse_out, gathered_out)
+            aux = opd.loss_fwd_bwd(logits, est, mask=mask, want_lse=True, want_gathered=True, **kw)
+            lse_dev, gat_dev = aux["lse"], aux["gathered"].contiguous()
+            del aux
+            tau_dev, beta_dev = kw["teacher_logp"], kw["behav_logp"]
+            seq = w.rollout_len if w.ragged else 2048
+
+            def step():
+                opd.mc_diagnostics(lse_dev, gat_dev, tau_dev, beta_dev, mask=mask,
+                                   group_sizes=(2, 4, 8), seq_len=seq, stream=stream)
         else:
             ids_dev = dev_t(d["mc_ids"])
 
@@ -272,7 +300,8 @@ def main():
         K = w.k if op == "topk" else w.M
         alg = cache_op_bytes(w, op, n_valid, K)
         key = w.name + "/" + op
-        metric = "OPD cache build (%s) tokens/sec at V=151,936 bf16; achieved HBM GB/s vs peak" % op
+        metric = ("OPD MC diagnostics tokens/sec; achieved HBM GB/s vs peak" if op == "diag" else
+                  "OPD cache build (%s) tokens/sec at V=151,936 bf16; achieved HBM GB/s vs peak" % op)
     achieved = alg / mean_launch_s / 1e9
     traffic = read_traffic(key)
     res = {
@@ -321,6 +350,9 @@ def main():
         log("timing the oracle ...")
         if op == "loss":
             res["cpu_baseline"] = cpu_baseline(w, est, d, args.cpu_rows, args.cpu_threads)
+        elif op == "diag":
+            res["cpu_baseline"] = cpu_diag_baseline(w, d, lse_dev.cpu().numpy(),
+                                                    gat_dev.cpu().numpy(), seq)
         else:
             res["cpu_baseline"] = cpu_cache_baseline(w, op, d, u_np, args.cpu_rows,
                                                      args.cpu_threads)

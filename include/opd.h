@@ -38,7 +38,7 @@
 extern "C" {
 #endif
 
-#define OPD_VERSION 3
+#define OPD_VERSION 4
 /* Largest cached support size k, and largest sample count M. */
 #define OPD_K_MAX 256
 
@@ -281,6 +281,64 @@ int opd_topk_support(const void* logits, int32_t dtype, int64_t N, int64_t V, in
 int opd_score_actions(const void* logits, int32_t dtype, int64_t N, int64_t V, int64_t ld,
                       const int32_t* ids, int32_t K, const uint8_t* mask, float* logp,
                       float* lse_out, void* stream);
+
+/*
+ * Diagnostics of the Monte-Carlo estimator: the importance-ratio tail that
+ * Sec. 5.2 tracks (the p99 of rho_theta, Fig. 5) and the variance of the
+ * m-sample estimator at a fixed prefix and over a sequence (App. E, Table 6).
+ * Inputs are per token t what an MC loss call returns or reads: lse [N]
+ * (lse_out, log sum_j exp z_j), gathered [N, M] (gathered_out, the student
+ * logits at the M draws), teacher_logp and behav_logp [N, M] (the cache).
+ * With log p = gathered - lse, A = teacher_logp - log p, rho = exp(log p -
+ * behav_logp), the one-sample terms are X = -rho A (the loss is their mean).
+ * Outputs (device fp32, each nullable):
+ *   row_mean [N]     (1/M) sum_i X_i
+ *   row_var [N]      unbiased variance of X_i over i (NaN when M = 1)
+ *   row_rho_max [N]  max_i rho_i (NaN ratios ignored)
+ *   rho_quantile [1] nearest-rank quantile of rho over all valid entries:
+ *                    the r-th smallest, r = max(1, ceil(quantile * n)) (in
+ *                    double, from the fp32 quantile); NaN ratios rank above
+ *                    +inf
+ *   clip_frac [1]    fraction of valid entries with |rho - 1| > clip_eps
+ *   ratio_local [n_groups], ratio_seq [n_groups]
+ *                    variance ratios for group sizes m = group_sizes[k]
+ *                    (host array; M a multiple of m, M / m >= 2): the draws
+ *                    of a token split into M / m groups of m consecutive
+ *                    draws with means Y_g;
+ *                      ratio_local = sum_t var_g(Y_g) / sum_t row_var_t,
+ *                    and, with tokens [s seq_len, (s + 1) seq_len) forming
+ *                    sequence s and S_g its valid-token average of Y_g,
+ *                      ratio_seq = sum_s var_g(S_g) / sum_s var_i(S1_i)
+ *                    (S1: the same with single draws).  var is unbiased.
+ *                    ratio_seq needs seq_len > 0.
+ * Masked tokens (mask[t] == 0) are excluded and get 0 in the per-token
+ * outputs.  The workspace (size from opd_mc_diag_workspace_bytes, 16-byte
+ * aligned) holds intermediates; the quantile is exact (radix selection with
+ * integer histograms); sums run in a fixed order.
+ * Errors: OPD_ERR_SHAPE (N), OPD_ERR_SUPPORT (M outside [1, OPD_K_MAX]),
+ * OPD_ERR_PARAM (quantile outside (0, 1], clip_eps negative or not finite,
+ * more than 8 or invalid group sizes, seq_len < 0, ratio_seq without
+ * seq_len), OPD_ERR_NULL, OPD_ERR_WORKSPACE, OPD_ERR_HIP.
+ */
+typedef struct opd_mc_diag {
+  float* row_mean;
+  float* row_var;
+  float* row_rho_max;
+  float* rho_quantile;
+  float* clip_frac;
+  float* ratio_local;
+  float* ratio_seq;
+} opd_mc_diag;
+
+/* Workspace bytes of opd_mc_diagnostics (0 for invalid arguments). */
+size_t opd_mc_diag_workspace_bytes(int64_t N, int32_t M, const int32_t* group_sizes,
+                                   int32_t n_groups, int64_t seq_len);
+
+int opd_mc_diagnostics(const float* lse, const float* gathered, const float* teacher_logp,
+                       const float* behav_logp, int64_t N, int32_t M, const uint8_t* mask,
+                       float quantile, float clip_eps, const int32_t* group_sizes,
+                       int32_t n_groups, int64_t seq_len, const opd_mc_diag* out, void* workspace,
+                       size_t workspace_bytes, void* stream);
 
 /* Static description of a status code ("ok", "null pointer", ...). */
 const char* opd_status_string(int status);

@@ -36,7 +36,8 @@ STATUS = {0: "OPD_OK", -1: "OPD_ERR_NULL", -2: "OPD_ERR_SHAPE", -3: "OPD_ERR_SUP
 
 # every symbol include/opd.h declares
 EXPORTS = ("opd_loss_fwd_bwd", "opd_workspace_bytes", "opd_validate_cache", "opd_sample_actions",
-           "opd_topk_support", "opd_score_actions", "opd_status_string", "opd_version")
+           "opd_topk_support", "opd_score_actions", "opd_mc_diag_workspace_bytes",
+           "opd_mc_diagnostics", "opd_status_string", "opd_version")
 
 
 class OpdError(RuntimeError):
@@ -55,6 +56,13 @@ class OpdCache(ctypes.Structure):
 class OpdOpts(ctypes.Structure):
     _fields_ = [("grad_scale", ctypes.c_float), ("dlogits_dtype", ctypes.c_int32),
                 ("flags", ctypes.c_uint32), ("clip_eps", ctypes.c_float)]
+
+
+class OpdMcDiag(ctypes.Structure):
+    _fields_ = [("row_mean", ctypes.c_void_p), ("row_var", ctypes.c_void_p),
+                ("row_rho_max", ctypes.c_void_p), ("rho_quantile", ctypes.c_void_p),
+                ("clip_frac", ctypes.c_void_p), ("ratio_local", ctypes.c_void_p),
+                ("ratio_seq", ctypes.c_void_p)]
 
 
 _lib = None
@@ -82,6 +90,12 @@ def lib():
         L.opd_topk_support.restype = ctypes.c_int
         L.opd_score_actions.argtypes = [P, i32, i64, i64, i64, P, i32, P, P, P, P]
         L.opd_score_actions.restype = ctypes.c_int
+        L.opd_mc_diag_workspace_bytes.argtypes = [i64, i32, P, i32, i64]
+        L.opd_mc_diag_workspace_bytes.restype = ctypes.c_size_t
+        L.opd_mc_diagnostics.argtypes = [P, P, P, P, i64, i32, P, ctypes.c_float, ctypes.c_float,
+                                         P, i32, i64, ctypes.POINTER(OpdMcDiag), P,
+                                         ctypes.c_size_t, P]
+        L.opd_mc_diagnostics.restype = ctypes.c_int
         L.opd_status_string.argtypes = [ctypes.c_int]
         L.opd_status_string.restype = ctypes.c_char_p
         L.opd_version.restype = ctypes.c_int
@@ -270,4 +284,43 @@ def score_actions(logits: torch.Tensor, ids: torch.Tensor, *, mask=None, want_ls
     out = {"logp": logp}
     if lse is not None:
         out["lse"] = lse
+    return out
+
+
+# ---------------------------------------------------------------- MC diagnostics
+
+DIAG_OUTPUTS = ("row_mean", "row_var", "row_rho_max", "rho_quantile", "clip_frac", "ratio_local",
+                "ratio_seq")
+
+
+def mc_diagnostics(lse: torch.Tensor, gathered: torch.Tensor, teacher_logp: torch.Tensor,
+                   behav_logp: torch.Tensor, *, mask=None, quantile: float = 0.99,
+                   clip_eps: float = 0.2, group_sizes=(), seq_len: int = 0, want=None,
+                   stream=None) -> dict:
+    """Diagnostics of the MC estimator from an MC loss call's lse_out and
+    gathered_out and the cache's teacher and behaviour log-probs (see
+    opd_mc_diagnostics).  Returns the requested outputs as device tensors."""
+    N, M = gathered.shape
+    for t, name in ((gathered, "gathered"), (teacher_logp, "teacher_logp"),
+                    (behav_logp, "behav_logp")):
+        if t.dtype != torch.float32 or not t.is_contiguous() or tuple(t.shape) != (N, M):
+            raise ValueError("%s must be a contiguous [N, M] float32 tensor" % name)
+    if want is None:
+        want = DIAG_OUTPUTS if seq_len and len(group_sizes) else DIAG_OUTPUTS[:-1]
+    gs = (ctypes.c_int32 * max(len(group_sizes), 1))(*group_sizes)
+    dev = gathered.device
+    sizes = {"row_mean": N, "row_var": N, "row_rho_max": N, "rho_quantile": 1, "clip_frac": 1,
+             "ratio_local": max(len(group_sizes), 1), "ratio_seq": max(len(group_sizes), 1)}
+    out = {k: torch.empty(sizes[k], dtype=torch.float32, device=dev) for k in want}
+    st = OpdMcDiag(*[_ptr(out.get(k)) for k in DIAG_OUTPUTS])
+    nbytes = int(lib().opd_mc_diag_workspace_bytes(N, M, gs, len(group_sizes), seq_len))
+    ws = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
+    rc = lib().opd_mc_diagnostics(_ptr(lse), _ptr(gathered), _ptr(teacher_logp), _ptr(behav_logp),
+                                  N, M, _ptr(mask), quantile, clip_eps, gs, len(group_sizes),
+                                  seq_len, ctypes.byref(st), _ptr(ws), nbytes, _stream(stream))
+    if rc != 0:
+        raise OpdError(rc, "opd_mc_diagnostics")
+    for k in ("ratio_local", "ratio_seq"):
+        if k in out:
+            out[k] = out[k][:len(group_sizes)]
     return out

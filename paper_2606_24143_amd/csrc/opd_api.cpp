@@ -147,6 +147,47 @@ bool row_fits(int64_t nvec, int32_t dtype) {
   return nvec <= (int64_t)opd::slots_large(dtype) * opd::kRowThreads;
 }
 
+// Workspace of opd_mc_diagnostics: regions in order, each 256-byte aligned.
+struct DiagLayout {
+  size_t rho, var, clip, vloc, ycol, wseq, hist, total;
+  int ncol;
+  int64_t nseq;
+};
+
+DiagLayout diag_layout(int64_t N, int32_t M, const int32_t* groups, int32_t n_groups,
+                       int64_t seq_len) {
+  DiagLayout l{};
+  auto take = [&](size_t bytes) {
+    const size_t at = l.total;
+    l.total += (bytes + 255) & ~(size_t)255;
+    return at;
+  };
+  l.ncol = M;
+  for (int k = 0; k < n_groups; ++k) l.ncol += M / groups[k];
+  const bool seq = seq_len > 0 && n_groups > 0;
+  l.nseq = seq ? (N + seq_len - 1) / seq_len : 0;
+  l.rho = take((size_t)N * M * 4);
+  l.var = take((size_t)N * 4);
+  l.clip = take((size_t)N * 4);
+  l.vloc = take((size_t)N * (n_groups > 0 ? n_groups : 1) * 4);
+  l.ycol = seq ? take((size_t)N * l.ncol * 4) : 0;
+  l.wseq = seq ? take((size_t)l.nseq * (n_groups + 1) * 4) : 0;
+  l.hist = take((4 * 256 + 4) * 4);
+  return l;
+}
+
+int check_diag(int64_t N, int32_t M, float q, float clip_eps, const int32_t* groups,
+               int32_t n_groups, int64_t seq_len) {
+  if (N < 0 || N > INT32_MAX) return OPD_ERR_SHAPE;
+  if (M < 1 || M > OPD_K_MAX) return OPD_ERR_SUPPORT;
+  if (!(q > 0.0f && q <= 1.0f) || !(clip_eps >= 0.0f && clip_eps <= 3.0e38f)) return OPD_ERR_PARAM;
+  if (n_groups < 0 || n_groups > opd::kDiagMaxGroups || seq_len < 0) return OPD_ERR_PARAM;
+  if (n_groups > 0 && !groups) return OPD_ERR_NULL;
+  for (int k = 0; k < n_groups; ++k)
+    if (groups[k] < 1 || M % groups[k] != 0 || M / groups[k] < 2) return OPD_ERR_PARAM;
+  return OPD_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -332,6 +373,58 @@ int opd_score_actions(const void* logits, int32_t dtype, int64_t N, int64_t V, i
   a.ids = ids;
   const hipError_t err = opd::launch_cache(a, opd::CacheOp::Score, dtype, row_fits(a.nvec, dtype),
                                            (hipStream_t)stream);
+  return err == hipSuccess ? OPD_OK : OPD_ERR_HIP;
+}
+
+size_t opd_mc_diag_workspace_bytes(int64_t N, int32_t M, const int32_t* group_sizes,
+                                   int32_t n_groups, int64_t seq_len) {
+  if (check_diag(N, M, 0.5f, 0.2f, group_sizes, n_groups, seq_len) != OPD_OK) return 0;
+  return diag_layout(N, M, group_sizes, n_groups, seq_len).total;
+}
+
+int opd_mc_diagnostics(const float* lse, const float* gathered, const float* teacher_logp,
+                       const float* behav_logp, int64_t N, int32_t M, const uint8_t* mask,
+                       float quantile, float clip_eps, const int32_t* group_sizes,
+                       int32_t n_groups, int64_t seq_len, const opd_mc_diag* out, void* workspace,
+                       size_t workspace_bytes, void* stream) {
+  if (int rc = check_diag(N, M, quantile, clip_eps, group_sizes, n_groups, seq_len)) return rc;
+  if (!out) return OPD_ERR_NULL;
+  if (out->ratio_seq && (seq_len == 0 || n_groups == 0)) return OPD_ERR_PARAM;
+  if (N == 0) return OPD_OK;
+  if (!lse || !gathered || !teacher_logp || !behav_logp) return OPD_ERR_NULL;
+  const DiagLayout l = diag_layout(N, M, group_sizes, n_groups, seq_len);
+  if (!workspace || workspace_bytes < l.total || !aligned16(workspace)) return OPD_ERR_WORKSPACE;
+  opd::DiagArgs a{};
+  a.lse = lse;
+  a.gathered = gathered;
+  a.tau = teacher_logp;
+  a.beta = behav_logp;
+  a.N = N;
+  a.M = M;
+  a.mask = mask;
+  a.q = quantile;
+  a.clip_eps = clip_eps;
+  a.n_groups = n_groups;
+  for (int k = 0; k < n_groups; ++k) a.group[k] = group_sizes[k];
+  a.seq_len = seq_len;
+  a.nseq = l.nseq;
+  a.ncol = l.ncol;
+  a.row_mean = out->row_mean;
+  a.row_var = out->row_var;
+  a.row_rho_max = out->row_rho_max;
+  a.rho_quantile = out->rho_quantile;
+  a.clip_frac = out->clip_frac;
+  a.ratio_local = out->ratio_local;
+  a.ratio_seq = out->ratio_seq;
+  char* ws = (char*)workspace;
+  a.ws_rho = (float*)(ws + l.rho);
+  a.ws_var = (float*)(ws + l.var);
+  a.ws_clip = (uint32_t*)(ws + l.clip);
+  a.ws_vloc = (float*)(ws + l.vloc);
+  a.ws_ycol = l.nseq ? (float*)(ws + l.ycol) : nullptr;
+  a.ws_wseq = l.nseq ? (float*)(ws + l.wseq) : nullptr;
+  a.ws_hist = (uint32_t*)(ws + l.hist);
+  const hipError_t err = opd::launch_diag(a, (hipStream_t)stream);
   return err == hipSuccess ? OPD_OK : OPD_ERR_HIP;
 }
 

@@ -91,6 +91,38 @@ struct CacheArgs {
 hipError_t launch_cache(const CacheArgs& a, CacheOp op, int in_dt, bool resident,
                         hipStream_t stream);
 
+// Monte-Carlo diagnostics (opd_mc_diagnostics).
+constexpr int kDiagMaxGroups = 8;
+// replicate columns per token: M single draws plus the groups of each size
+constexpr int kDiagMaxCols = kKMax * (1 + kDiagMaxGroups);
+
+struct DiagArgs {
+  const float* lse;       // [N]
+  const float* gathered;  // [N, M]
+  const float* tau;       // [N, M]
+  const float* beta;      // [N, M]
+  int64_t N;
+  int M;
+  const uint8_t* mask;    // nullable
+  float q, clip_eps;
+  int n_groups;
+  int group[kDiagMaxGroups];
+  int64_t seq_len, nseq;
+  int ncol;               // replicate columns per token
+  // outputs (nullable)
+  float *row_mean, *row_var, *row_rho_max, *rho_quantile, *clip_frac, *ratio_local, *ratio_seq;
+  // workspace
+  float* ws_rho;          // [N, M]
+  float* ws_var;          // [N]
+  uint32_t* ws_clip;      // [N]
+  float* ws_vloc;         // [N, n_groups]
+  float* ws_ycol;         // [N, ncol] (sequence ratios only, else NULL)
+  float* ws_wseq;         // [nseq, n_groups + 1] (sequence ratios only, else NULL)
+  uint32_t* ws_hist;      // [4 * 256 + 4] radix-select histograms and state
+};
+
+hipError_t launch_diag(const DiagArgs& a, hipStream_t stream);
+
 // Launchers; each returns hipSuccess or the launch error.
 hipError_t launch_rowwise(const Args& a, int est, int in_dt, int out_dt, Path path, bool read_row,
                           hipStream_t stream);

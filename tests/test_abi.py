@@ -201,3 +201,58 @@ def test_cache_required_pointers_and_sizes(op, kw, code):
 @pytest.mark.parametrize("op", ["sample", "topk", "score"])
 def test_cache_zero_rows_is_a_noop(op):
     assert call_row(op, N=0, logits=None, u=None, ids=None, out=None, logp=None) == OK
+
+
+# ---------------------------------------------------------------- MC diagnostics
+
+def call_diag(N=4, M=8, q=0.99, eps=0.2, groups=(2, 4), seq=0, out=True, ws=FAKE,
+              ws_bytes=1 << 30, ptrs=(FAKE, FAKE, FAKE, FAKE)):
+    gs = (ctypes.c_int32 * max(len(groups), 1))(*groups)
+    st = opd.OpdMcDiag(FAKE, None, None, None, None, None, None) if out else None
+    L = opd.lib()
+    return L.opd_mc_diagnostics(*ptrs, N, M, None, q, eps, gs, len(groups), seq,
+                                ctypes.byref(st) if st else None, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(N=-1), SHAPE),
+    (dict(M=0), SUPPORT),
+    (dict(M=257), SUPPORT),
+    (dict(q=0.0), PARAM),
+    (dict(q=1.5), PARAM),
+    (dict(q=float("nan")), PARAM),
+    (dict(eps=-0.1), PARAM),
+    (dict(eps=float("inf")), PARAM),
+    (dict(groups=(3,)), PARAM),           # 3 does not divide 8
+    (dict(groups=(8,)), PARAM),           # a single group has no variance
+    (dict(groups=(0,)), PARAM),
+    (dict(groups=(1,) * 9), PARAM),       # at most 8 group sizes
+    (dict(seq=-1), PARAM),
+    (dict(out=False), NULL),
+    (dict(ptrs=(None, FAKE, FAKE, FAKE)), NULL),
+    (dict(ptrs=(FAKE, FAKE, FAKE, None)), NULL),
+    (dict(ws=None), WORKSPACE),
+    (dict(ws_bytes=16), WORKSPACE),
+    (dict(ws=FAKE + 4), WORKSPACE),
+])
+def test_diag_argument_errors_are_reported_before_launch(kw, code):
+    assert call_diag(**kw) == code
+
+
+def test_diag_ratio_seq_needs_seq_len():
+    gs = (ctypes.c_int32 * 1)(2)
+    st = opd.OpdMcDiag(None, None, None, None, None, None, FAKE)
+    L = opd.lib()
+    assert L.opd_mc_diagnostics(FAKE, FAKE, FAKE, FAKE, 4, 8, None, 0.99, 0.2, gs, 1, 0,
+                                ctypes.byref(st), FAKE, 1 << 30, None) == PARAM
+
+
+def test_diag_workspace_sizing():
+    L = opd.lib()
+    gs = (ctypes.c_int32 * 3)(2, 4, 8)
+    a = L.opd_mc_diag_workspace_bytes(32768, 16, gs, 3, 0)
+    b = L.opd_mc_diag_workspace_bytes(32768, 16, gs, 3, 2048)
+    assert 32768 * 16 * 4 < a < b          # the sequence ratios add replicate columns
+    assert L.opd_mc_diag_workspace_bytes(32768, 16, gs, 3, -1) == 0
+    assert L.opd_mc_diag_workspace_bytes(4, 0, gs, 0, 0) == 0
+    assert call_diag(N=0, ptrs=(None, None, None, None), ws=None) == OK
