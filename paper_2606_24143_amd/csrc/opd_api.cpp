@@ -149,7 +149,7 @@ bool row_fits(int64_t nvec, int32_t dtype) {
 
 // Workspace of opd_mc_diagnostics: regions in order, each 256-byte aligned.
 struct DiagLayout {
-  size_t rho, var, clip, vloc, ycol, wseq, hist, total;
+  size_t rho, var, clip, vloc, ycol, savg, parts, hist, total;
   int ncol;
   int64_t nseq;
 };
@@ -171,7 +171,8 @@ DiagLayout diag_layout(int64_t N, int32_t M, const int32_t* groups, int32_t n_gr
   l.clip = take((size_t)N * 4);
   l.vloc = take((size_t)N * (n_groups > 0 ? n_groups : 1) * 4);
   l.ycol = seq ? take((size_t)N * l.ncol * 4) : 0;
-  l.wseq = seq ? take((size_t)l.nseq * (n_groups + 1) * 4) : 0;
+  l.savg = seq ? take((size_t)l.nseq * l.ncol * 4) : 0;
+  l.parts = take((size_t)opd::kDiagParts * (3 + opd::kDiagMaxGroups) * 8);
   l.hist = take((4 * 256 + 4) * 4);
   return l;
 }
@@ -422,7 +423,8 @@ int opd_mc_diagnostics(const float* lse, const float* gathered, const float* tea
   a.ws_clip = (uint32_t*)(ws + l.clip);
   a.ws_vloc = (float*)(ws + l.vloc);
   a.ws_ycol = l.nseq ? (float*)(ws + l.ycol) : nullptr;
-  a.ws_wseq = l.nseq ? (float*)(ws + l.wseq) : nullptr;
+  a.ws_savg = l.nseq ? (float*)(ws + l.savg) : nullptr;
+  a.ws_parts = (double*)(ws + l.parts);
   a.ws_hist = (uint32_t*)(ws + l.hist);
   const hipError_t err = opd::launch_diag(a, (hipStream_t)stream);
   return err == hipSuccess ? OPD_OK : OPD_ERR_HIP;

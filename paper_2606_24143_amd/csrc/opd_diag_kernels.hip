@@ -10,12 +10,13 @@
 //   rows     one wavefront per token: mean, unbiased variance and largest
 //            rho of its M terms; count of rho outside [1 - eps, 1 + eps];
 //            means of replicate groups of m draws and their variance
-//   seq      one workgroup per sequence: token averages of each replicate
-//            column, and their variance per group size
+//   seq      one wavefront per (sequence, replicate column): the column's
+//            average over the sequence's valid tokens
 //   select   the nearest-rank quantile of rho by radix selection over its
 //            bits (rho >= 0, so bits order like values): four 8-bit passes,
 //            each an integer histogram then a one-workgroup pick
-//   final    one workgroup: fixed-order sums in double, the batch outputs
+//   final    fixed-order sums in double (per-range parts, then one
+//            workgroup), the per-sequence set variances, the batch outputs
 // Integer histograms make the selection exact and order-independent; every
 // floating-point sum has a fixed order.
 #include <math.h>
@@ -119,50 +120,27 @@ __global__ void __launch_bounds__(kDiagThreads) k_diag_rows(DiagArgs a) {
   }
 }
 
-// One workgroup per sequence of seq_len tokens: the token average of every
-// replicate column (valid tokens only), then the unbiased variance over the
-// columns of each set (single draws, then each group size).
+// One wavefront per (sequence, replicate column): the average of that column
+// over the sequence's valid tokens (lanes stride the tokens; fixed-order
+// butterfly sum).  The variances over the columns of each set are taken in
+// the final pass.
 __global__ void __launch_bounds__(kDiagThreads) k_diag_seq(DiagArgs a) {
-  __shared__ float s_avg[kDiagMaxCols];
-  __shared__ int s_nv;
+  const int lane = threadIdx.x & 63;
+  const int c = blockIdx.y * kDiagWaves + (threadIdx.x >> 6);
+  if (c >= a.ncol) return;
   const int64_t s = blockIdx.x;
   const int64_t t0 = s * a.seq_len, t1 = min(t0 + a.seq_len, a.N);
-  if (threadIdx.x == 0) {
-    int nv = 0;
-    for (int64_t t = t0; t < t1; ++t) nv += (!a.mask || a.mask[t] != 0) ? 1 : 0;
-    s_nv = nv;
+  float acc = 0.f;
+  uint32_t nv = 0;
+  for (int64_t t = t0 + lane; t < t1; t += 64) {
+    if (a.mask && a.mask[t] == 0) continue;
+    acc += a.ws_ycol[t * a.ncol + c];
+    ++nv;
   }
-  __syncthreads();
-  const int nv = s_nv;
-  float* out = a.ws_wseq + s * (a.n_groups + 1);
-  if (nv == 0) {
-    if (threadIdx.x <= a.n_groups) out[threadIdx.x] = __builtin_nanf("");
-    return;
-  }
-  for (int c = threadIdx.x; c < a.ncol; c += kDiagThreads) {
-    float acc = 0.f;
-    for (int64_t t = t0; t < t1; ++t)
-      if (!a.mask || a.mask[t] != 0) acc += a.ws_ycol[t * a.ncol + c];
-    s_avg[c] = acc / (float)nv;
-  }
-  __syncthreads();
-  // set k = 0: the M single-draw columns; set k >= 1: the groups of size
-  // group[k - 1]
-  if (threadIdx.x <= a.n_groups) {
-    const int k = threadIdx.x;
-    int c0 = 0, n = a.M;
-    if (k > 0) {
-      c0 = a.M;
-      for (int j = 0; j < k - 1; ++j) c0 += a.M / a.group[j];
-      n = a.M / a.group[k - 1];
-    }
-    float mean = 0.f;
-    for (int c = c0; c < c0 + n; ++c) mean += s_avg[c];
-    mean /= (float)n;
-    float ss = 0.f;
-    for (int c = c0; c < c0 + n; ++c) ss += (s_avg[c] - mean) * (s_avg[c] - mean);
-    out[k] = ss / (float)(n - 1);
-  }
+  acc = wave_sum(acc);
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) nv += __shfl_xor(nv, o, 64);
+  if (lane == 0) a.ws_savg[s * a.ncol + c] = nv ? acc / (float)nv : __builtin_nanf("");
 }
 
 // The radix-select state lives in the workspace: sel[0] = key prefix chosen
@@ -189,91 +167,134 @@ __global__ void __launch_bounds__(kDiagThreads) k_diag_hist(DiagArgs a, int pass
   if (h[threadIdx.x]) atomicAdd(&a.ws_hist[pass * 256 + threadIdx.x], h[threadIdx.x]);
 }
 
-// One workgroup: the bucket holding the wanted rank (a sequential scan of 256
-// counts by one lane; negligible).
-__global__ void __launch_bounds__(64) k_diag_pick(DiagArgs a, int pass) {
-  if (threadIdx.x != 0) return;
+// One workgroup of 256 lanes, one bucket each: an inclusive scan of the
+// counts finds the bucket holding the wanted rank.
+__global__ void __launch_bounds__(256) k_diag_pick(DiagArgs a, int pass) {
+  __shared__ uint32_t s_w[4];
+  __shared__ uint32_t s_rank;
   uint32_t* sel = a.ws_hist + 4 * 256;
   const uint32_t* hist = a.ws_hist + pass * 256;
-  uint32_t rank;
-  if (pass == 0) {
-    uint32_t n = 0;
-    for (int b = 0; b < 256; ++b) n += hist[b];
-    sel[2] = n;
-    // nearest rank: the ceil(q n)-th smallest, at least the first
-    const double want = ceil((double)a.q * (double)n);
-    rank = n == 0 ? 0u : (uint32_t)(want < 1.0 ? 1.0 : (want > n ? (double)n : want));
-    sel[0] = 0u;
-  } else {
-    rank = sel[1];
+  const int b = threadIdx.x, lane = b & 63, w = b >> 6;
+  const uint32_t h = hist[b];
+  // inclusive scan of the counts (integers: any order gives the same sums)
+  uint32_t incl = h;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint32_t t = (uint32_t)__shfl_up((int)incl, o, 64);
+    if (lane >= o) incl += t;
   }
-  uint32_t before = 0, b = 0;
-  for (; b < 255; ++b) {
-    if (before + hist[b] >= rank) break;
-    before += hist[b];
-  }
-  sel[0] = (sel[0] << 8) | b;
-  sel[1] = rank - before;
-  if (pass == 3 && a.rho_quantile)
-    a.rho_quantile[0] = sel[2] == 0 ? __builtin_nanf("") : __uint_as_float(sel[0]);
-}
-
-// Fixed-order sums in double by one workgroup: lane j takes rows j, j + 256,
-// ..., then a sequential pass over the 256 partials.
-__global__ void __launch_bounds__(kDiagThreads) k_diag_final(DiagArgs a) {
-  __shared__ double s_p[kDiagThreads];
-  __shared__ double s_tot[4 + 2 * (kDiagMaxGroups + 1)];
-  const int tid = threadIdx.x;
-  auto reduce = [&](double v) {
-    s_p[tid] = v;
-    __syncthreads();
-    double r = 0.0;
-    if (tid == 0)
-      for (int j = 0; j < kDiagThreads; ++j) r += s_p[j];
-    __syncthreads();
-    return r;  // lane 0 only
-  };
-  double var = 0.0, clip = 0.0, rows = 0.0;
-  for (int64_t t = tid; t < a.N; t += kDiagThreads) {
-    if (a.mask && a.mask[t] == 0) continue;
-    rows += 1.0;
-    clip += (double)a.ws_clip[t];
-    if (a.M >= 2) var += (double)a.ws_var[t];
-  }
-  var = reduce(var);
-  clip = reduce(clip);
-  rows = reduce(rows);
-  if (tid == 0) {
-    s_tot[0] = var;
-    s_tot[1] = clip;
-    s_tot[2] = rows;
-  }
-  for (int k = 0; k < a.n_groups; ++k) {
-    double v = 0.0;
-    for (int64_t t = tid; t < a.N; t += kDiagThreads)
-      if (!a.mask || a.mask[t] != 0) v += (double)a.ws_vloc[t * a.n_groups + k];
-    v = reduce(v);
-    if (tid == 0) s_tot[4 + k] = v;
-  }
-  if (a.ws_wseq) {
-    for (int k = 0; k <= a.n_groups; ++k) {
-      double v = 0.0;
-      for (int64_t s = tid; s < a.nseq; s += kDiagThreads) {
-        const float x = a.ws_wseq[s * (a.n_groups + 1) + k];
-        if (x == x) v += (double)x;  // sequences with no valid token are NaN
-      }
-      v = reduce(v);
-      if (tid == 0) s_tot[4 + kDiagMaxGroups + k] = v;
+  if (lane == 63) s_w[w] = incl;
+  __syncthreads();
+  for (int j = 0; j < w; ++j) incl += s_w[j];
+  const uint32_t n = s_w[0] + s_w[1] + s_w[2] + s_w[3];
+  if (b == 0) {
+    if (pass == 0) {
+      sel[2] = n;
+      // nearest rank: the ceil(q n)-th smallest, at least the first
+      const double want = ceil((double)a.q * (double)n);
+      s_rank = n == 0 ? 1u : (uint32_t)(want < 1.0 ? 1.0 : (want > n ? (double)n : want));
+    } else {
+      s_rank = sel[1];
     }
   }
+  __syncthreads();
+  const uint32_t rank = s_rank, excl = incl - h;
+  // the one bucket with excl < rank <= incl (the last one if rounding ever
+  // left rank beyond the total)
+  if ((excl < rank && rank <= incl) || (b == 255 && incl < rank)) {
+    const uint32_t prefix = pass == 0 ? 0u : sel[0];
+    sel[0] = (prefix << 8) | (uint32_t)b;
+    sel[1] = rank - excl;
+    if (pass == 3 && a.rho_quantile)
+      a.rho_quantile[0] = sel[2] == 0 ? __builtin_nanf("") : __uint_as_float((prefix << 8) | (uint32_t)b);
+  }
+}
+
+// Batch sums in two fixed-order stages: kDiagParts workgroups each sum a
+// contiguous range of tokens (lane-strided, then the lanes' partials in lane
+// order), in double; one workgroup then adds the parts in order and forms
+// the outputs.  Quantities: [0] sum of row_var, [1] clipped entries, [2]
+// valid tokens, [3 + k] sum of the group-k variances.
+__device__ __forceinline__ double block_sum_ordered(double v, double* red) {
+  red[threadIdx.x] = v;
+  __syncthreads();
+  double r = 0.0;
+  if (threadIdx.x == 0)
+    for (int j = 0; j < kDiagThreads; ++j) r += red[j];
+  __syncthreads();
+  return r;  // lane 0 only
+}
+
+__global__ void __launch_bounds__(kDiagThreads) k_diag_parts(DiagArgs a) {
+  __shared__ double red[kDiagThreads];
+  const int nq = 3 + a.n_groups;
+  const int64_t per = (a.N + kDiagParts - 1) / kDiagParts;
+  const int64_t t0 = blockIdx.x * per, t1 = min(t0 + per, a.N);
+  double* out = a.ws_parts + (int64_t)blockIdx.x * (3 + kDiagMaxGroups);
+  for (int q = 0; q < nq; ++q) {
+    double v = 0.0;
+    for (int64_t t = t0 + threadIdx.x; t < t1; t += kDiagThreads) {
+      if (a.mask && a.mask[t] == 0) continue;
+      if (q == 0)
+        v += a.M >= 2 ? (double)a.ws_var[t] : 0.0;
+      else if (q == 1)
+        v += (double)a.ws_clip[t];
+      else if (q == 2)
+        v += 1.0;
+      else
+        v += (double)a.ws_vloc[t * a.n_groups + (q - 3)];
+    }
+    v = block_sum_ordered(v, red);
+    if (threadIdx.x == 0) out[q] = v;
+  }
+}
+
+// Unbiased variance over the columns [c0, c0 + n) of one sequence.
+__device__ double seq_set_var(const float* avg, int c0, int n) {
+  double mean = 0.0;
+  for (int c = c0; c < c0 + n; ++c) mean += avg[c];
+  mean /= n;
+  double ss = 0.0;
+  for (int c = c0; c < c0 + n; ++c) ss += (avg[c] - mean) * (avg[c] - mean);
+  return ss / (n - 1);
+}
+
+__global__ void __launch_bounds__(kDiagThreads) k_diag_final(DiagArgs a) {
+  __shared__ double red[kDiagThreads];
+  __shared__ double tot[3 + kDiagMaxGroups];
+  __shared__ double seq[kDiagMaxGroups + 1];
+  const int tid = threadIdx.x;
+  if (tid < 3 + a.n_groups) {
+    double v = 0.0;
+    for (int p = 0; p < kDiagParts; ++p) v += a.ws_parts[p * (3 + kDiagMaxGroups) + tid];
+    tot[tid] = v;
+  }
+  // sequence level: set 0 = the M single-draw columns, set k >= 1 = the
+  // groups of size group[k - 1]; sequences without a valid token are skipped
+  if (a.ws_savg) {
+    for (int k = 0; k <= a.n_groups; ++k) {
+      int c0 = 0, n = a.M;
+      if (k > 0) {
+        c0 = a.M;
+        for (int j = 0; j < k - 1; ++j) c0 += a.M / a.group[j];
+        n = a.M / a.group[k - 1];
+      }
+      double v = 0.0;
+      for (int64_t s = tid; s < a.nseq; s += kDiagThreads) {
+        const float* avg = a.ws_savg + s * a.ncol;
+        if (avg[0] == avg[0]) v += seq_set_var(avg, c0, n);
+      }
+      v = block_sum_ordered(v, red);
+      if (tid == 0) seq[k] = v;
+    }
+  }
+  __syncthreads();
   if (tid == 0) {
-    const double n = s_tot[2] * (double)a.M;
-    if (a.clip_frac) a.clip_frac[0] = n > 0 ? (float)(s_tot[1] / n) : __builtin_nanf("");
+    const double n = tot[2] * (double)a.M;
+    if (a.clip_frac) a.clip_frac[0] = n > 0 ? (float)(tot[1] / n) : __builtin_nanf("");
     for (int k = 0; k < a.n_groups; ++k) {
-      if (a.ratio_local) a.ratio_local[k] = (float)(s_tot[4 + k] / s_tot[0]);
-      if (a.ratio_seq && a.ws_wseq)
-        a.ratio_seq[k] =
-            (float)(s_tot[4 + kDiagMaxGroups + 1 + k] / s_tot[4 + kDiagMaxGroups]);
+      if (a.ratio_local) a.ratio_local[k] = (float)(tot[3 + k] / tot[0]);
+      if (a.ratio_seq && a.ws_savg) a.ratio_seq[k] = (float)(seq[1 + k] / seq[0]);
     }
   }
 }
@@ -286,16 +307,19 @@ hipError_t launch_diag(const DiagArgs& a, hipStream_t stream) {
   hipLaunchKernelGGL(k_diag_zero, dim3(1), blk, 0, stream, a);
   hipLaunchKernelGGL(k_diag_rows, dim3((unsigned)((a.N + kDiagWaves - 1) / kDiagWaves)), blk, 0,
                      stream, a);
-  if (a.ws_wseq) hipLaunchKernelGGL(k_diag_seq, dim3((unsigned)a.nseq), blk, 0, stream, a);
+  if (a.ws_savg)
+    hipLaunchKernelGGL(k_diag_seq, dim3((unsigned)a.nseq, (unsigned)((a.ncol + kDiagWaves - 1) / kDiagWaves)),
+                       blk, 0, stream, a);
   if (a.rho_quantile) {
     const int64_t total = a.N * a.M;
     const int64_t blocks = (total + kDiagThreads - 1) / kDiagThreads;
     const unsigned grid = (unsigned)(blocks < 2048 ? blocks : 2048);
     for (int pass = 0; pass < 4; ++pass) {
       hipLaunchKernelGGL(k_diag_hist, dim3(grid), blk, 0, stream, a, pass);
-      hipLaunchKernelGGL(k_diag_pick, dim3(1), dim3(64), 0, stream, a, pass);
+      hipLaunchKernelGGL(k_diag_pick, dim3(1), dim3(256), 0, stream, a, pass);
     }
   }
+  hipLaunchKernelGGL(k_diag_parts, dim3(kDiagParts), blk, 0, stream, a);
   hipLaunchKernelGGL(k_diag_final, dim3(1), blk, 0, stream, a);
   return hipGetLastError();
 }

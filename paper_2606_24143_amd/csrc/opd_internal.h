@@ -93,8 +93,8 @@ hipError_t launch_cache(const CacheArgs& a, CacheOp op, int in_dt, bool resident
 
 // Monte-Carlo diagnostics (opd_mc_diagnostics).
 constexpr int kDiagMaxGroups = 8;
-// replicate columns per token: M single draws plus the groups of each size
-constexpr int kDiagMaxCols = kKMax * (1 + kDiagMaxGroups);
+// workgroups of the first stage of the batch sums
+constexpr int kDiagParts = 64;
 
 struct DiagArgs {
   const float* lse;       // [N]
@@ -117,7 +117,8 @@ struct DiagArgs {
   uint32_t* ws_clip;      // [N]
   float* ws_vloc;         // [N, n_groups]
   float* ws_ycol;         // [N, ncol] (sequence ratios only, else NULL)
-  float* ws_wseq;         // [nseq, n_groups + 1] (sequence ratios only, else NULL)
+  float* ws_savg;         // [nseq, ncol] (sequence ratios only, else NULL)
+  double* ws_parts;       // [kDiagParts, 3 + kDiagMaxGroups] first-stage sums
   uint32_t* ws_hist;      // [4 * 256 + 4] radix-select histograms and state
 };
 
