@@ -257,7 +257,7 @@ template <class TI, int NSLOT>
 __global__ void __launch_bounds__(NT) k_sample(CacheArgs a) {
   __shared__ CdfLds c;
   const int tid = threadIdx.x;
-  const int64_t row = blockIdx.x;
+  const int64_t row = xcd_remap(blockIdx.x, gridDim.x);
   const int M = a.K;
   if (a.mask && a.mask[row] == 0) {
     for (int i = tid; i < M; i += NT) {
@@ -475,7 +475,7 @@ template <class TI, int NSLOT, bool LSE>
 __global__ void __launch_bounds__(NT) k_topk(CacheArgs a) {
   __shared__ TopkLds sh;
   const int tid = threadIdx.x;
-  const int64_t row = blockIdx.x;
+  const int64_t row = xcd_remap(blockIdx.x, gridDim.x);
   const int k = a.K;
   if (a.mask && a.mask[row] == 0) {
     for (int i = tid; i < k; i += NT) {
@@ -647,7 +647,7 @@ __global__ void __launch_bounds__(kScoreThreads) k_score(CacheArgs a) {
   typedef typename TI::Vec Vec;
   __shared__ Stats s_st[W];
   const int tid = threadIdx.x;
-  const int64_t row = blockIdx.x;
+  const int64_t row = xcd_remap(blockIdx.x, gridDim.x);
   const int K = a.K;  // <= OPD_K_MAX == T: one id per lane
   if (a.mask && a.mask[row] == 0) {
     if (tid < K) a.logp[row * K + tid] = 0.f;

@@ -333,7 +333,7 @@ __global__ void __launch_bounds__(kRowThreads) k_row_resident(Args a) {
   __shared__ uint32_t s_spk[2][NT];
   static_assert(NSLOT <= 64, "spike map holds 64 slots");
   const int tid = threadIdx.x;
-  const int64_t row = blockIdx.x;
+  const int64_t row = xcd_remap(blockIdx.x, gridDim.x);
   const void* zrow = (const char*)a.logits + row * a.ld * TI::BYTES;
   void* grow = (char*)a.dlogits + row * a.ld * TO::BYTES;
   if (a.mask && a.mask[row] == 0) {
@@ -498,7 +498,7 @@ __global__ void __launch_bounds__(kRowThreads) k_row_dense_resident(Args a) {
   __shared__ Stats s_st[NW];
   __shared__ Vec s_y[YL][NT];
   const int tid = threadIdx.x;
-  const int64_t row = blockIdx.x;
+  const int64_t row = xcd_remap(blockIdx.x, gridDim.x);
   const void* zrow = (const char*)a.logits + row * a.ld * TI::BYTES;
   const void* yrow = (const char*)a.teacher + row * a.ld * TI::BYTES;
   void* grow = (char*)a.dlogits + row * a.ld * TO::BYTES;
@@ -674,7 +674,7 @@ __global__ void __launch_bounds__(kRowThreads) k_row_stream(Args a) {
   __shared__ Stats s_red[NW];
   __shared__ CacheLds c;
   const int tid = threadIdx.x;
-  const int64_t row = blockIdx.x;
+  const int64_t row = xcd_remap(blockIdx.x, gridDim.x);
   const void* zrow = (const char*)a.logits + row * a.ld * TI::BYTES;
   const void* yrow = DENSE ? (const char*)a.teacher + row * a.ld * TI::BYTES : nullptr;
   void* grow = (char*)a.dlogits + row * a.ld * TO::BYTES;
@@ -738,8 +738,9 @@ template <class TI, bool DENSE>
 __global__ void __launch_bounds__(kSplitThreads) k_split_stats(Args a) {
   constexpr int NT = kSplitThreads, NW = NT / 64;
   __shared__ Stats s_red[NW];
-  const int64_t row = blockIdx.x / a.P;
-  const int chunk = (int)(blockIdx.x % a.P);
+  const int64_t bi = xcd_remap(blockIdx.x, gridDim.x);
+  const int64_t row = bi / a.P;
+  const int chunk = (int)(bi % a.P);
   if (a.mask && a.mask[row] == 0) return;
   const int64_t v0 = (int64_t)chunk * a.chunk_vec;
   const int64_t v1 = v0 + a.chunk_vec < a.nvec ? v0 + a.chunk_vec : a.nvec;
@@ -761,8 +762,9 @@ __global__ void __launch_bounds__(kSplitThreads) k_split_write(Args a) {
   __shared__ CacheLds c;
   __shared__ Stats s_row;
   const int tid = threadIdx.x;
-  const int64_t row = blockIdx.x / a.P;
-  const int chunk = (int)(blockIdx.x % a.P);
+  const int64_t bi = xcd_remap(blockIdx.x, gridDim.x);
+  const int64_t row = bi / a.P;
+  const int chunk = (int)(bi % a.P);
   const int64_t v0 = (int64_t)chunk * a.chunk_vec;
   const int64_t v1 = v0 + a.chunk_vec < a.nvec ? v0 + a.chunk_vec : a.nvec;
   const void* zrow = (const char*)a.logits + row * a.ld * TI::BYTES;
@@ -840,8 +842,9 @@ constexpr int kSparseRowsPerBlock = 4;
 template <class TO>
 __global__ void __launch_bounds__(kFillThreads) k_fill_zero(Args a, int64_t row0,
                                                             int64_t blocks_per_row) {
-  const int64_t row = row0 + blockIdx.x / blocks_per_row;
-  const int64_t v = (int64_t)(blockIdx.x % blocks_per_row) * kFillThreads + threadIdx.x;
+  const int64_t bi = xcd_remap(blockIdx.x, gridDim.x);
+  const int64_t row = row0 + bi / blocks_per_row;
+  const int64_t v = (int64_t)(bi % blocks_per_row) * kFillThreads + threadIdx.x;
   if (row >= a.N || v >= a.nvec) return;
   if (a.skip_masked && a.mask && a.mask[row] == 0) return;
   const float g[4] = {0.f, 0.f, 0.f, 0.f};
