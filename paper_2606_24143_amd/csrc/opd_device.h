@@ -42,16 +42,27 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 
 // ---------------------------------------------------------------- XCD-aware placement
 // The MI355X dispatcher hands workgroup b of a grid to XCD b % 8.  Remapping
-// b so that each XCD covers one contiguous eighth of the grid's work (in its
-// own dispatch order) keeps every XCD's concurrent rows adjacent in memory;
-// measured on the row-per-workgroup read+write pattern at V = 151,936 this
-// cut the time by about 6% against the identity mapping.  The last G % 8
-// workgroups keep their place, so the map is a permutation of [0, G).
+// b so that each XCD works through blocks of kXcdBlock consecutive rows (in
+// its own dispatch order) keeps every XCD's concurrent rows adjacent in
+// memory; measured on the row-per-workgroup read+write pattern at
+// V = 151,936 this cuts the time by about 6% against the identity mapping.
+// Blocks, rather than one contiguous eighth per XCD, keep the XCDs balanced
+// when the valid rows of a masked batch cluster.  Workgroups past the last
+// whole round of 8 blocks keep their place, so the map is a permutation of
+// [0, G).
 constexpr int kXcds = 8;
+#ifndef OPD_XCD_BLOCK
+#define OPD_XCD_BLOCK 64
+#endif
+constexpr int64_t kXcdBlock = OPD_XCD_BLOCK;
 
 __device__ __forceinline__ int64_t xcd_remap(int64_t b, int64_t G) {
-  const int64_t g8 = G - G % kXcds;
-  return b < g8 ? (b % kXcds) * (g8 / kXcds) + b / kXcds : b;
+  const int64_t B = G / kXcds < kXcdBlock ? G / kXcds : kXcdBlock;
+  if (B == 0) return b;
+  const int64_t span = B * kXcds;
+  if (b >= G - G % span) return b;
+  const int64_t q = b / kXcds;  // b's place in its XCD's dispatch order
+  return (q / B) * span + (b % kXcds) * B + q % B;
 }
 
 // ---------------------------------------------------------------- dtype helpers
