@@ -65,6 +65,15 @@ __device__ __forceinline__ int64_t xcd_remap(int64_t b, int64_t G) {
   return (q / B) * span + (b % kXcds) * B + q % B;
 }
 
+// One contiguous eighth of a one-shot grid per XCD (32-bit indices).  For
+// grids of short workgroups that each write one 16 KiB piece; measured on a
+// zero fill of an [8192, 151936] fp32 gradient this beat both the identity
+// and the 64-row blocks above.
+__device__ __forceinline__ uint32_t xcd_eighths(uint32_t b, uint32_t G) {
+  const uint32_t g8 = G - G % kXcds;
+  return b < g8 ? (b % kXcds) * (g8 / kXcds) + b / kXcds : b;
+}
+
 // ---------------------------------------------------------------- dtype helpers
 
 template <class TI>

@@ -29,6 +29,12 @@ SHAPES = {  # name: (N, V, ld)
     "v151936": (6, 151936, 151936),
     "v7_tail": (5, 7, 8),
     "v200000_wide": (3, 200000, 200000),
+    # an odd number of 4-element vectors (a trailing 8-byte bf16 vector), padded
+    "v1004_odd": (9, 1004, 1008),
+    # fp32 rows on the large register-resident dense variant
+    "v50000": (4, 50000, 50000),
+    # the shortest bf16 row the large dense variant takes (one slot past its LDS part)
+    "v81920": (3, 81920, 81920),
 }
 PATHS = {"rowwise": opd.FLAG_FORCE_ROWWISE, "split": opd.FLAG_FORCE_SPLITV}
 
