@@ -34,9 +34,14 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0
-KERNEL_SOURCES = [os.path.join(ROOT, "paper_2606_24143_amd", "csrc", f)
-                  for f in ("opd_kernels.hip", "opd_cache_kernels.hip", "opd_diag_kernels.hip",
-                            "opd_api.cpp", "opd_internal.h", "opd_device.h")]
+_CSRC = os.path.join(ROOT, "paper_2606_24143_amd", "csrc")
+_COMMON_SOURCES = ("opd_api.cpp", "opd_internal.h", "opd_device.h")
+# the sources each op's kernels are built from
+KERNEL_SOURCES = {"loss": ("opd_kernels.hip",) + _COMMON_SOURCES,
+                  "sample": ("opd_cache_kernels.hip",) + _COMMON_SOURCES,
+                  "topk": ("opd_cache_kernels.hip",) + _COMMON_SOURCES,
+                  "score": ("opd_cache_kernels.hip",) + _COMMON_SOURCES,
+                  "diag": ("opd_diag_kernels.hip",) + _COMMON_SOURCES}
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 # estimators that read the top-k cache (renormalised and truncated)
 SUPPORT = ("fkl_topk", "rkl_topk", "fkl_topk_trunc", "rkl_topk_trunc")
@@ -46,11 +51,12 @@ def log(msg: str):
     print(msg, file=sys.stderr, flush=True)
 
 
-def kernel_hash() -> str:
+def kernel_hash(op: str = "loss") -> str:
+    """Hash of the sources the op's kernels are built from."""
     h = hashlib.sha256()
-    for p in KERNEL_SOURCES:
-        with open(p, "rb") as f:
-            h.update(f.read())
+    for f in KERNEL_SOURCES[op]:
+        with open(os.path.join(_CSRC, f), "rb") as fh:
+            h.update(fh.read())
     return h.hexdigest()[:16]
 
 
@@ -123,18 +129,18 @@ def cpu_diag_baseline(w, d, lse, gathered, seq):
                       "%.2f s wall on 1 thread" % (w.N, el)}
 
 
-def read_traffic(est_key: str):
+def read_traffic(est_key: str, op: str):
     """Measured HBM bytes per launch from the committed counter summary, if it
-    was taken on the current kernel sources."""
+    was taken on the current sources of the op's kernels."""
     try:
         with open(TRAFFIC_FILE) as f:
             t = json.load(f)
     except (OSError, ValueError):
         return None
-    if t.get("kernel_hash") != kernel_hash():
-        return None
     e = t.get("workloads", {}).get(est_key)
-    return None if e is None else e.get("bytes_per_launch")
+    if e is None or e.get("kernel_hash") != kernel_hash(op):
+        return None
+    return e.get("bytes_per_launch")
 
 
 def cpu_baseline(w, est, d, rows: int, threads: int, chunk: int = 512):
@@ -303,7 +309,7 @@ def main():
         metric = ("OPD MC diagnostics tokens/sec; achieved HBM GB/s vs peak" if op == "diag" else
                   "OPD cache build (%s) tokens/sec at V=151,936 bf16; achieved HBM GB/s vs peak" % op)
     achieved = alg / mean_launch_s / 1e9
-    traffic = read_traffic(key)
+    traffic = read_traffic(key, op)
     res = {
         "metric": metric,
         "value": n_valid / (ms_per_step / 1e3),
