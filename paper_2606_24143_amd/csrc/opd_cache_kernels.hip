@@ -339,6 +339,289 @@ __global__ void __launch_bounds__(NT) k_sample(CacheArgs a) {
   }
 }
 
+// ---------------------------------------------------------------- sampling, streamed
+
+// Draws read each row once, so the common case is organised for overlap
+// rather than residency: 256-lane workgroups with about 17 KiB of LDS,
+// several per CU, so one row's prefix and draws overlap other rows' reads.
+// The index-order CDF is kept as chunk records.  A chunk is 128 consecutive
+// vectors (512 elements); the 16 lanes of one DPP row load it with eight
+// instructions, each covering 16 consecutive vectors (128 bytes of bf16), so
+// every load is coalesced.  Its record is the chunk max m_q (a DPP row max)
+// and s_q = sum exp(z - m_q) (per-lane sums in load order, then a DPP row
+// scan).  After the row, each record is scaled to the row max M
+// (s'_q = s_q f_q, f_q = exp(m_q - M)), each thread sums its run of C
+// consecutive chunks in order, and a block scan gives the run prefixes.  One
+// wavefront per draw then finds the run (ballot over the prefixes), the
+// chunk (a wave scan of the run's records and a ballot), and the element (a
+// wave scan over the chunk in index order, two vectors per lane, at the same
+// weights exp(z - m_q) f_q).  Where rounding leaves no crossing at a level,
+// the nearest entry of nonzero mass is taken, as in the resident kernel.
+constexpr int kSmpThreads = 256;
+constexpr int kSmpWaves = kSmpThreads / 64;
+constexpr int kSmpLoads = 8;                          // loads per lane per chunk
+constexpr int kSmpChunkVecs = 16 * kSmpLoads;         // vectors per chunk (128)
+constexpr int kSmpMaxChunks = 2048;                   // records per row: V <= 1,048,576
+
+struct SmpLds {
+  float m[kSmpMaxChunks];  // chunk max
+  float s[kSmpMaxChunks];  // chunk sum at its max; then at the row max
+  float p[kSmpThreads];    // inclusive prefix of the runs
+  float wt[kSmpWaves];
+  float red[kSmpWaves];
+};
+
+// max over the 16 lanes of a DPP row, in every lane of the row
+__device__ __forceinline__ float row16_max(float x) {
+  x = fmaxf(x, dpp_move<0x140>(x));  // row_mirror
+  x = fmaxf(x, dpp_move<0x141>(x));  // row_half_mirror
+  x = fmaxf(x, dpp_move<0xB1>(x));   // quad_perm [1,0,3,2]
+  x = fmaxf(x, dpp_move<0x4E>(x));   // quad_perm [2,3,0,1]
+  return x;
+}
+// inclusive prefix sum within each DPP row of 16 lanes
+__device__ __forceinline__ float row16_scan(float x) {
+  const int rl = threadIdx.x & 15;
+  float t;
+  t = dpp_move<0x111>(x);  // row_shr:1
+  if (rl >= 1) x += t;
+  t = dpp_move<0x112>(x);  // row_shr:2
+  if (rl >= 2) x += t;
+  t = dpp_move<0x114>(x);  // row_shr:4
+  if (rl >= 4) x += t;
+  t = dpp_move<0x118>(x);  // row_shr:8
+  if (rl >= 8) x += t;
+  return x;
+}
+
+__device__ __forceinline__ int first_lane(uint64_t b) { return b ? __ffsll((long long)b) - 1 : -1; }
+__device__ __forceinline__ int last_lane(uint64_t b) { return b ? 63 - __clzll((long long)b) : -1; }
+
+// First (or last) chunk in [lo, hi) with positive mass, by wave ballots; -1 if none.
+__device__ __forceinline__ int64_t chunk_positive(const SmpLds& c, int64_t lo, int64_t hi,
+                                                  bool last) {
+  const int lane = threadIdx.x & 63;
+  if (!last) {
+    for (int64_t b = lo; b < hi; b += 64) {
+      const int64_t q = b + lane;
+      const int f = first_lane(__ballot(q < hi && c.s[q] > 0.f));
+      if (f >= 0) return b + f;
+    }
+  } else {
+    for (int64_t b = hi; b > lo; b -= 64) {
+      const int64_t q = b - 64 + lane;
+      const int l = last_lane(__ballot(q >= lo && q < b && c.s[q] > 0.f));
+      if (l >= 0) return b - 64 + l;
+    }
+  }
+  return -1;
+}
+
+// One draw by one wavefront (the result is wave-uniform): the first element
+// whose cumulative mass exceeds t = u * S.
+template <class TI>
+__device__ int64_t smp_draw(const SmpLds& c, const void* zrow, uint32_t nvec, int tail,
+                            uint32_t nchunk, uint32_t C, float t, float S, float nM) {
+  const int lane = threadIdx.x & 63;
+  int64_t q = -1;
+  float r = 0.f;
+  int pick = kLast;
+  if (t < S) {
+    // run: the first i with p[i] > t (each lane looks at 4 entries)
+    int li = -1;
+#pragma unroll
+    for (int k = 3; k >= 0; --k)
+      if (c.p[4 * lane + k] > t) li = 4 * lane + k;
+    const int fl = first_lane(__ballot(li >= 0));
+    const int i = __shfl(li, fl < 0 ? 0 : fl, 64);  // fl >= 0: p[255] = S > t
+    r = fmaxf(t - (i ? c.p[i - 1] : 0.f), 0.f);
+    // chunk within the run (C <= 8 chunks, one per lane)
+    const uint32_t r0 = min((uint32_t)i * C, nchunk), r1 = min(r0 + C, nchunk);
+    const uint32_t qq = r0 + (uint32_t)lane;
+    const float sq = qq < r1 ? c.s[qq] : 0.f;
+    const float incl = wave_incl_scan(sq);
+    const int cl = first_lane(__ballot(qq < r1 && incl > r));
+    if (cl >= 0) {
+      const float before = cl > 0 ? __shfl(incl, cl - 1, 64) : 0.f;
+      q = r0 + cl;
+      r = fmaxf(r - before, 0.f);
+      pick = kCross;
+    } else {
+      const int ll = last_lane(__ballot(qq < r1 && sq > 0.f));
+      if (ll >= 0) {
+        q = r0 + ll;
+      } else {
+        q = chunk_positive(c, r1, nchunk, false);
+        pick = kFirst;
+        if (q < 0) {
+          q = chunk_positive(c, 0, r0, true);
+          pick = kLast;
+        }
+      }
+    }
+  } else {
+    q = chunk_positive(c, 0, nchunk, true);
+  }
+  if (q < 0) return -1;  // no chunk of positive mass (excluded by S > 0)
+  // element within chunk q: lane l holds vectors 2l and 2l + 1 of the chunk
+  // (elements 8l .. 8l + 7, in index order)
+  const float mq = c.m[q];
+  const float nmq = -mq * kLog2e, fq = fast_exp2(fmaf(mq, kLog2e, nM));
+  const uint32_t v = (uint32_t)q * kSmpChunkVecs + 2u * (uint32_t)lane;
+  float wl[8];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const bool in = v + h < nvec;
+    float f[4];
+    unpack<TI>(in ? load_vec<TI>(zrow, v + h, nvec, tail) : neg_inf_vec<TI>(), f);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) wl[4 * h + e] = in ? ez(f[e], nmq) : 0.f;
+  }
+  float lsum = 0.f;
+  int e_first = -1, e_last = -1;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    lsum += wl[e];
+    if (wl[e] > 0.f) {
+      if (e_first < 0) e_first = e;
+      e_last = e;
+    }
+  }
+  int vl = -1, el = -1;  // chosen lane and element in it
+  if (pick == kCross) {
+    const float incl = wave_incl_scan(lsum);
+    vl = first_lane(__ballot(incl * fq > r));
+    if (vl >= 0) {
+      float cum = vl > 0 ? __shfl(incl, vl - 1, 64) : 0.f;
+      int ec = -1;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        cum += wl[e];
+        if (ec < 0 && cum * fq > r) ec = e;
+      }
+      el = __shfl(ec, vl, 64);
+      if (el < 0) vl = -1;  // rounding: no element crossing in that lane
+    }
+    if (vl < 0) pick = kLast;
+  }
+  if (pick == kFirst) {
+    vl = first_lane(__ballot(e_first >= 0));
+    el = __shfl(e_first, vl < 0 ? 0 : vl, 64);
+  } else if (pick == kLast) {
+    vl = last_lane(__ballot(e_last >= 0));
+    el = __shfl(e_last, vl < 0 ? 0 : vl, 64);
+  }
+  if (vl < 0 || el < 0) return -1;
+  return ((int64_t)q * kSmpChunkVecs + 2 * vl) * 4 + el;
+}
+
+template <class TI>
+__global__ void __launch_bounds__(kSmpThreads) k_sample_stream(CacheArgs a) {
+  constexpr int T = kSmpThreads, W = kSmpWaves, R = kSmpLoads, CV = kSmpChunkVecs;
+  typedef typename TI::Vec Vec;
+  __shared__ SmpLds c;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int64_t row = xcd_remap(blockIdx.x, gridDim.x);
+  const int M = a.K;
+  if (a.mask && a.mask[row] == 0) {
+    for (int i = tid; i < M; i += T) {
+      a.ids_out[row * M + i] = 0;
+      if (a.logp) a.logp[row * M + i] = 0.f;
+    }
+    if (tid == 0 && a.lse_out) a.lse_out[row] = 0.f;
+    return;
+  }
+  const void* zrow = (const char*)a.logits + row * a.ld * TI::BYTES;
+  const uint32_t nvec = (uint32_t)a.nvec;
+  const uint32_t nchunk = (nvec + CV - 1) / CV;  // <= kSmpMaxChunks
+  const bool ragged = a.tail != TI::EPV;
+
+  // one pass over the row: DPP row k of wave w takes chunks 4 w + k,
+  // 4 w + k + 4 W, ...; its lane l loads vectors 16 b + l of the chunk
+  const uint32_t rowk = (uint32_t)lane >> 4, rl = (uint32_t)lane & 15;
+  float lmax = kNegInf;
+  for (uint32_t q0 = 4u * w; q0 < nchunk; q0 += 4u * W) {  // wave-uniform
+    const uint32_t q = q0 + rowk;
+    const uint32_t v0 = q * CV + rl;
+    Vec x[R];
+#pragma unroll
+    for (int b = 0; b < R; ++b) x[b] = ld_nt<TI>(zrow, min(v0 + 16u * b, nvec - 1));
+    float lm = kNegInf;
+#pragma unroll
+    for (int b = 0; b < R; ++b) {
+      const uint32_t v = v0 + 16u * b;
+      if (v >= nvec) x[b] = neg_inf_vec<TI>();
+      else if (ragged && v == nvec - 1) x[b] = tail_masked<TI>(x[b], a.tail);
+      float f[4];
+      unpack<TI>(x[b], f);
+      lm = fmaxf(lm, fmaxf(fmaxf(f[0], f[1]), fmaxf(f[2], f[3])));
+    }
+    const float mq = row16_max(lm);
+    float ls = 0.f;
+    if (mq != kNegInf) {  // an all -inf chunk has no mass (and no NaN)
+      const float nm = -mq * kLog2e;
+#pragma unroll
+      for (int b = 0; b < R; ++b) {
+        float f[4];
+        unpack<TI>(x[b], f);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) ls += ez(f[e], nm);
+      }
+    }
+    const float sq = row16_scan(ls);
+    if (rl == 15 && q < nchunk) {
+      c.m[q] = mq;
+      c.s[q] = sq;
+    }
+    lmax = fmaxf(lmax, lm);
+  }
+  const float Mx = block_max<W>(lmax, c.red);  // ends with a barrier: records visible
+  const float nM = -Mx * kLog2e;
+  // records at the row max; runs of C consecutive chunks per thread
+  const uint32_t C = (nchunk + T - 1) / T;
+  {
+    const uint32_t r0 = min((uint32_t)tid * C, nchunk), r1 = min(r0 + C, nchunk);
+    float run = 0.f;
+    for (uint32_t q = r0; q < r1; ++q) {
+      const float mq = c.m[q];
+      const float sq = mq == kNegInf ? 0.f : c.s[q] * fast_exp2(fmaf(mq, kLog2e, nM));
+      c.s[q] = sq;
+      run += sq;
+    }
+    const float incl = wave_incl_scan(run);
+    if (lane == 63) c.wt[w] = incl;
+    __syncthreads();
+    float before = 0.f;
+    for (int k = 0; k < w; ++k) before += c.wt[k];
+    c.p[tid] = before + incl;
+  }
+  float S = 0.f;
+#pragma unroll
+  for (int k = 0; k < W; ++k) S += c.wt[k];  // equals p[T - 1] bit for bit
+  __syncthreads();
+
+  const float L = Mx + logf(S);
+  if (tid == 0 && a.lse_out) a.lse_out[row] = L;
+  // a NaN or +inf logit, or a row of -inf, leaves S NaN or 0: no distribution
+  const bool defined = S > 0.f && S <= 3.4028235e38f;
+  for (int i = w; i < M; i += W) {  // one draw per wavefront
+    const float u = a.u[row * M + i];
+    int32_t id = -1;
+    float lp = __builtin_nanf("");
+    if (defined && u >= 0.f && u < 1.f) {
+      const int64_t j = smp_draw<TI>(c, zrow, nvec, a.tail, nchunk, C, u * S, S, nM);
+      if (j >= 0) {
+        id = (int32_t)j;
+        lp = load_elem<TI>(zrow, j) - L;
+      }
+    }
+    if (lane == 0) {
+      a.ids_out[row * M + i] = id;
+      if (a.logp) a.logp[row * M + i] = lp;
+    }
+  }
+}
+
 // ---------------------------------------------------------------- top-k
 
 // Sort key: the IEEE-754 total order of the fp32 bits (bf16 widened), with
@@ -726,6 +1009,12 @@ hipError_t launch_op(const CacheArgs& a, CacheOp op, hipStream_t stream) {
 
 template <class TI>
 hipError_t launch_dt(const CacheArgs& a, CacheOp op, bool resident, hipStream_t stream) {
+  if (op == CacheOp::Sample &&
+      (a.nvec + kSmpChunkVecs - 1) / kSmpChunkVecs <= (int64_t)kSmpMaxChunks) {
+    hipLaunchKernelGGL((k_sample_stream<TI>), dim3((unsigned)a.N), dim3(kSmpThreads), 0, stream,
+                       a);
+    return hipGetLastError();
+  }
   if (op == CacheOp::Score) {
     hipLaunchKernelGGL((k_score<TI>), dim3((unsigned)a.N), dim3(kScoreThreads), 0, stream, a);
     return hipGetLastError();

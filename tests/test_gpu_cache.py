@@ -6,7 +6,8 @@ oracle in double, so a uniform within rounding of a CDF boundary may land on
 the neighbouring id.  A draw passes if it equals the oracle's, or if the
 oracle's exact CDF puts u within DELTA of the drawn id's interval
 [F(j-1), F(j)] and the id has positive probability; at least 99% of the
-draws must be identical.  DELTA = 1e-5 (as a fraction of the total mass):
+draws (and all but one of a small sample) must be identical.  DELTA = 1e-5
+(as a fraction of the total mass):
 the device's partial sums are fp32 sums of at most ~50 levels of
 positive terms (run, scan, chunk), each term within 2 ulp, so their error
 is below 50 * 2^-24 * 1.2 ~ 4e-6 of the total.
@@ -28,7 +29,9 @@ pytestmark = pytest.mark.gpu
 DELTA = 1e-5
 LP_TOL = 1e-5
 
-# (V, ld, dtype, path the row takes)
+# (V, ld, dtype); the paths noted are those of the top-k kernel (scoring always
+# streams; draws stream in 64-element chunks up to V = 262,144, and take the
+# resident or chunked kernel beyond)
 SHAPES = [
     (1000, 1000, synth.BF16),      # narrow resident row
     (3001, 3008, synth.BF16),      # V not a multiple of 4, padded stride
@@ -36,7 +39,8 @@ SHAPES = [
     (32000, 32000, synth.F32),     # fp32 resident
     (151936, 151936, synth.BF16),  # bf16 resident, 38 slots
     (151936, 151936, synth.F32),   # fp32 streamed (wider than the registers)
-    (200000, 200000, synth.BF16),  # streamed, two vectors per CDF chunk
+    (200000, 200000, synth.BF16),  # streamed
+    (300000, 300000, synth.BF16),  # streamed; draws in two-vector CDF chunks
 ]
 SHAPE_IDS = ["v%d_ld%d_%s" % (v, ld, "bf16" if dt == synth.BF16 else "f32") for v, ld, dt in SHAPES]
 
@@ -78,7 +82,10 @@ def check_draws(name, ids, logp, stored, V, dtype, u, ref, min_exact=0.99):
         assert lo - DELTA <= u[r, i] <= F[j] + DELTA, (
             "%s: row %d draw %d: u=%r outside [%r, %r] of id %d (oracle %d)" %
             (name, r, i, u[r, i], lo, F[j], j, ref["ids"][r, i]))
-    assert same.mean() >= min_exact, "%s: only %.4f of draws identical" % (name, same.mean())
+    # fp32 boundary draws occur at a rate of a few per thousand at V ~ 1.5e5..3e5
+    # (measured on both sampler kernels); a small sample may hold one
+    allowed = max(1, int((1.0 - min_exact) * same.size))
+    assert (~same).sum() <= allowed, "%s: only %.4f of draws identical" % (name, same.mean())
     # log-probabilities at the GPU's ids
     z_at = np.take_along_axis(widen(stored[:, :V], dtype), ids.clip(0, V - 1).astype(np.int64), 1)
     want = z_at - ref["lse"][:, None]
@@ -102,6 +109,23 @@ def test_sample_parity(shape, M):
                 u, ref)
     lse = out["lse"].cpu().numpy().astype(np.float64)
     assert np.all(np.abs(lse - ref["lse"]) <= LP_TOL * (1 + np.abs(ref["lse"])))
+
+
+def test_sample_wide_rows():
+    # wider than the streamed sampler's chunk records (V > 1,048,576): the
+    # chunked kernel
+    V, N, M = 1_200_000, 3, 64
+    say("sample wide V=%d" % V)
+    stored = make_logits(V, V, synth.BF16, N, seed=4)
+    u = f32_uniforms(21, N, M)
+    out = opd.sample_actions(as_device(stored, V), to_dev(u), want_lse=True)
+    torch.cuda.synchronize()
+    ref = oracle.cache_rows("sample", synth.BF16, stored, V, M, uniforms=u)
+    # CDF boundaries are eight times denser than at V = 151,936, and so are
+    # the fp32 boundary draws (about 1.6% here; each is still checked
+    # against DELTA)
+    check_draws("wide", out["ids"].cpu().numpy(), out["logp"].cpu().numpy(), stored, V,
+                synth.BF16, u, ref, min_exact=0.95)
 
 
 def test_sample_masked_rows_and_determinism():
