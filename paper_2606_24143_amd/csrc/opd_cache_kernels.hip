@@ -22,6 +22,8 @@ namespace {
 
 constexpr int NT = kRowThreads;
 constexpr int NW = NT / 64;
+// ids_out[row * k] of a row the streamed top-k kernel leaves to the resident one
+constexpr int32_t kTopkRedo = -2;
 
 // ---------------------------------------------------------------- rows
 
@@ -647,8 +649,8 @@ __device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int m) {
 // shuffles; wider ones go through LDS (two buffers, one barrier each).
 // Only the first P lanes (P a power of two) take part; the others keep their
 // values.
-template <class T>
-__device__ T block_sort_desc(T v, T (*buf)[NT], int P = NT) {
+template <class T, int NTH = NT>
+__device__ T block_sort_desc(T v, T (*buf)[NTH], int P = NTH) {
   const int tid = threadIdx.x;
   int ping = 0;
 #pragma unroll 1
@@ -760,6 +762,8 @@ __global__ void __launch_bounds__(NT) k_topk(CacheArgs a) {
   const int tid = threadIdx.x;
   const int64_t row = xcd_remap(blockIdx.x, gridDim.x);
   const int k = a.K;
+  // after the streamed kernel: only the rows it left to this one
+  if (a.redo && a.ids_out[row * k] != kTopkRedo) return;
   if (a.mask && a.mask[row] == 0) {
     for (int i = tid; i < k; i += NT) {
       a.ids_out[row * k + i] = 0;
@@ -914,6 +918,213 @@ __global__ void __launch_bounds__(NT) k_topk(CacheArgs a) {
   if (tid == 0 && a.lse_out) a.lse_out[row] = L;
 }
 
+// ---------------------------------------------------------------- top-k, streamed
+
+// The top-k support of rows of at least 16,384 entries, for k <= 64, reads
+// each row once: 256-lane workgroups with about 38 KiB of LDS, four per CU.
+// Each lane keeps the running maximum of the values it has seen.  After each
+// tile of 8 coalesced loads per lane, the k-th largest of the wave's 64
+// running maxima (a radix select over their order keys by ballots) is a
+// lower bound on the row's k-th largest (k lanes have each seen an element
+// at least that large), updated every fourth tile; the bound only rises.
+// Elements not below the wave's current bound, and NaNs, are appended to
+// its LDS buffer by ballot compaction, skipping every vector whose maximum
+// is below the bound in all lanes.  At the end the largest of the four wave
+// bounds is still a lower bound, every element at or above it is in some
+// buffer, and a block sort of those (at most 256) gives the support.  A row
+// whose buffers overflow (many equal large values) or that leaves more than
+// 256 candidates is marked, and a second launch runs the resident kernel on
+// the marked rows only.
+constexpr int kTkThreads = 256;
+constexpr int kTkWaves = kTkThreads / 64;
+constexpr int kTkLoads = 8;    // vector loads per lane per tile
+constexpr int kTkCap = 1024;   // candidates per wave
+constexpr int kTkMaxK = 64;    // one running maximum per lane bounds k
+constexpr int64_t kTkMinVec = 4096;
+
+struct TkLds {
+  uint64_t buf[kTkWaves][kTkCap];
+  uint64_t sbuf[2][kTkThreads];
+  uint64_t sel[kTkThreads];
+  uint32_t cnt[kTkWaves];
+  uint32_t theta[kTkWaves];
+  uint32_t nsel;
+  Stats st[kTkWaves];
+};
+
+template <class TI, bool LSE>
+__global__ void __launch_bounds__(kTkThreads) k_topk_stream(CacheArgs a) {
+  constexpr int T = kTkThreads, W = kTkWaves, B = kTkLoads;
+  typedef typename TI::Vec Vec;
+  __shared__ TkLds sh;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int64_t row = xcd_remap(blockIdx.x, gridDim.x);
+  const int k = a.K;  // <= kTkMaxK
+  if (a.mask && a.mask[row] == 0) {
+    for (int i = tid; i < k; i += T) {
+      a.ids_out[row * k + i] = 0;
+      if (a.logp) a.logp[row * k + i] = 0.f;
+    }
+    if (tid == 0 && a.lse_out) a.lse_out[row] = 0.f;
+    return;
+  }
+  const void* zrow = (const char*)a.logits + row * a.ld * TI::BYTES;
+  const uint32_t nvec = (uint32_t)a.nvec;  // >= kTkMinVec: every wave's first tile is full
+  const uint32_t V32 = (uint32_t)a.V;
+  float run = kNegInf;  // this lane's running maximum (NaN ignored)
+  uint32_t theta = 0;   // the wave's bound as an order key (wave-uniform)
+  float thf = kNegInf;  // the same bound as a value
+  uint32_t nb = 0;      // the wave's candidates so far (wave-uniform)
+  float m = kNegInf, sum = 0.f;
+  uint32_t tile = 0;
+  for (uint32_t t0 = (uint32_t)w * 64 * B; t0 < nvec; t0 += W * 64 * B) {  // wave-uniform
+    Vec xb[B];
+#pragma unroll
+    for (int b = 0; b < B; ++b) xb[b] = ld_nt<TI>(zrow, min(t0 + 64u * b + lane, nvec - 1));
+    // a whole tile inside the row needs no per-element checks (wave-uniform)
+    const bool full = t0 + 64u * B <= nvec && a.tail == TI::EPV;
+    auto vals = [&](int b, float (&f)[4]) {
+      unpack<TI>(xb[b], f);
+      if (!full) {
+        const uint32_t v = t0 + 64u * b + lane;
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (!(v < nvec && v * 4u + e < V32)) f[e] = kNegInf;
+      }
+    };
+    // pass 1: vector maxima (NaN ignored) and the tile's
+    float vm[B];
+    float tmx = kNegInf;
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+      float f[4];
+      vals(b, f);
+      vm[b] = fmaxf(fmaxf(f[0], f[1]), fmaxf(f[2], f[3]));
+      tmx = fmaxf(tmx, vm[b]);
+    }
+    // NaN (or +inf) in this lane's part of the tile: the tile's sum of
+    // exponentials is NaN; without the sums, tested element by element
+    bool nan = false;
+    if constexpr (LSE) {
+      const float mn = fmaxf(m, tmx);
+      if (mn != kNegInf) {
+        float acc = 0.f;
+        const float nm = -mn * kLog2e;
+#pragma unroll
+        for (int b = 0; b < B; ++b) {
+          float f[4];
+          vals(b, f);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) acc += fast_exp2(fmaf(f[e], kLog2e, nm));
+        }
+        nan = acc != acc;
+        sum = fmaf(sum, rescale(m, mn), acc);
+        m = mn;
+      }
+    } else {
+#pragma unroll
+      for (int b = 0; b < B; ++b) {
+        float f[4];
+        vals(b, f);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) nan = nan || f[e] != f[e];
+      }
+    }
+    run = fmaxf(run, tmx);
+    // every fourth tile: k lanes of this wave have each seen a value at
+    // least the k-th largest running maximum, found bit by bit with ballots
+    // (the bound only rises)
+    if ((tile++ & 3) == 0) {
+      const uint32_t rk = order_key(__float_as_uint(run));
+      if ((uint32_t)__popcll(__ballot(rk > theta)) >= (uint32_t)k) {
+        uint32_t t = 0;
+        for (int bit = 31; bit >= 0; --bit) {
+          const uint32_t c = t | (1u << bit);
+          if ((uint32_t)__popcll(__ballot(rk >= c)) >= (uint32_t)k) t = c;
+        }
+        theta = t;
+        thf = key_value(t);
+      }
+    }
+    // candidates: every element not below the bound, and every NaN
+    // (!(x < bound) holds for both); vectors whose maximum is below the
+    // bound and that hold no NaN are skipped by the whole wave
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+      if (__ballot(!(vm[b] < thf) || nan)) {  // wave-uniform
+        const uint32_t v = t0 + 64u * b + lane;
+        float f[4];
+        vals(b, f);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const bool take = !(f[e] < thf) && (full || (v < nvec && v * 4u + e < V32));
+          const uint64_t mask = __ballot(take);
+          if (mask) {  // wave-uniform
+            const uint32_t pos = nb + (uint32_t)__popcll(mask & ((1ull << lane) - 1ull));
+            if (take && pos < (uint32_t)kTkCap)
+              sh.buf[w][pos] = ((uint64_t)order_key(__float_as_uint(f[e])) << 32) |
+                               (0xFFFFFFFFu - (v * 4u + e));
+            nb += (uint32_t)__popcll(mask);
+          }
+        }
+      }
+    }
+  }
+  if (lane == 0) {
+    sh.cnt[w] = nb;
+    sh.theta[w] = theta;
+  }
+  if (tid == 0) sh.nsel = 0u;
+  float L = 0.f;
+  if constexpr (LSE) {
+    Stats st = stats_empty();
+    st.mz = m;
+    st.sz = sum;
+    st = block_merge<false, W>(st, sh.st);  // barriers: counts and bounds visible
+    L = st.mz + logf(st.sz);
+  } else {
+    __syncthreads();
+  }
+  uint32_t tstar = 0;
+  bool overflow = false;
+#pragma unroll
+  for (int q = 0; q < W; ++q) {
+    tstar = max(tstar, sh.theta[q]);
+    overflow = overflow || sh.cnt[q] > (uint32_t)kTkCap;
+  }
+  if (!overflow) {
+    // every element with key >= tstar is in some buffer: each wave's bound
+    // never exceeded tstar while it appended
+#pragma unroll
+    for (int q = 0; q < W; ++q) {
+      const uint32_t n = sh.cnt[q];
+      for (uint32_t i = tid; i < n; i += T) {
+        const uint64_t e = sh.buf[q][i];
+        if ((uint32_t)(e >> 32) >= tstar) {
+          const uint32_t pos = atomicAdd(&sh.nsel, 1u);
+          if (pos < (uint32_t)T) sh.sel[pos] = e;
+        }
+      }
+    }
+  }
+  __syncthreads();
+  const uint32_t nsel = sh.nsel;
+  if (overflow || nsel > (uint32_t)T || nsel < (uint32_t)k) {  // workgroup-uniform
+    if (tid == 0) a.ids_out[row * k] = kTopkRedo;
+    return;
+  }
+  int P = 2;
+  while (P < (int)nsel) P <<= 1;
+  const uint64_t mine =
+      block_sort_desc<uint64_t, T>(tid < (int)nsel ? sh.sel[tid] : 0ull, sh.sbuf, P);
+  if (tid < k) {
+    const uint32_t j = 0xFFFFFFFFu - (uint32_t)mine;
+    a.ids_out[row * k + tid] = (int32_t)j;
+    if (a.logp) a.logp[row * k + tid] = key_value((uint32_t)(mine >> 32)) - L;
+  }
+  if (tid == 0 && a.lse_out) a.lse_out[row] = L;
+}
+
 // ---------------------------------------------------------------- scoring
 
 // Scoring reads each row once and writes a handful of values, so it is
@@ -1018,6 +1229,22 @@ hipError_t launch_dt(const CacheArgs& a, CacheOp op, bool resident, hipStream_t 
   if (op == CacheOp::Score) {
     hipLaunchKernelGGL((k_score<TI>), dim3((unsigned)a.N), dim3(kScoreThreads), 0, stream, a);
     return hipGetLastError();
+  }
+  if (op == CacheOp::Topk && a.K <= kTkMaxK && a.nvec >= kTkMinVec) {
+    if (a.logp || a.lse_out)
+      hipLaunchKernelGGL((k_topk_stream<TI, true>), dim3((unsigned)a.N), dim3(kTkThreads), 0,
+                         stream, a);
+    else
+      hipLaunchKernelGGL((k_topk_stream<TI, false>), dim3((unsigned)a.N), dim3(kTkThreads), 0,
+                         stream, a);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    CacheArgs b = a;
+    b.redo = 1;  // the rows the streamed kernel left
+    if (!resident) return launch_op<TI, 0>(b, op, stream);
+    constexpr int big = TI::BYTES == 2 ? 38 : 19, small = TI::BYTES == 2 ? 16 : 8;
+    if (b.nvec <= (int64_t)small * NT) return launch_op<TI, small>(b, op, stream);
+    return launch_op<TI, big>(b, op, stream);
   }
   if (!resident) return launch_op<TI, 0>(a, op, stream);
   constexpr int big = TI::BYTES == 2 ? 38 : 19, small = TI::BYTES == 2 ? 16 : 8;

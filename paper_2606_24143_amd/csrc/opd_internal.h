@@ -86,6 +86,7 @@ struct CacheArgs {
   float* lse_out;       // [N] nullable
   int64_t G;            // sampler: vectors per CDF chunk
   int64_t nchunk;       // sampler: chunks per row
+  int redo;             // top-k: only the rows the streamed kernel marked
 };
 
 hipError_t launch_cache(const CacheArgs& a, CacheOp op, int in_dt, bool resident,

@@ -280,6 +280,65 @@ def test_topk_ties_and_special_values(dtype, case):
     check_topk(case, out, stored, V, k, dtype, ref)
 
 
+def to_stored(x, dtype):
+    """float32 rows as stored logits (bf16 by round-to-nearest-even, NaN kept)."""
+    if dtype != synth.BF16:
+        return np.ascontiguousarray(x)
+    b = x.view(np.uint32).astype(np.uint64)
+    stored = ((b + 0x7FFF + ((b >> 16) & 1)) >> 16).astype(np.uint16)
+    stored[np.isnan(x)] = 0x7FC0
+    return np.ascontiguousarray(stored)
+
+
+@pytest.mark.parametrize("dtype", [synth.F32, synth.BF16])
+@pytest.mark.parametrize("k", [16, 64])
+@pytest.mark.parametrize("case", ["constant", "ties_100", "ties_300", "special", "ascending",
+                                  "descending"])
+def test_topk_streamed_ties_and_special_values(dtype, k, case):
+    # rows wide enough for the streamed kernel (k <= 64): constant rows and
+    # 300 equal maxima leave it too many candidates (the resident kernel
+    # redoes those rows); 100 equal maxima are sorted in the streamed kernel
+    rng = np.random.default_rng(23)
+    V, N = 40000, 3
+    x = rng.normal(0, 1, (N, V)).astype(np.float32)
+    if case == "constant":
+        x[:] = -1.25
+    elif case.startswith("ties_"):
+        n = int(case[5:])
+        for r in range(N):
+            x[r, rng.choice(V, n, replace=False)] = 9.5
+    elif case == "special":
+        x[:, 10] = np.inf
+        x[:, 20] = np.nan
+        x[:, 30] = -0.0
+        x[:, 31] = 0.0
+        x[:, 40:100] = -np.inf
+        x[1, :] = np.where(x[1] > 0, -0.0, 0.0)  # only signed zeros
+        x[2, 5000:6000] = np.nan
+    elif case == "ascending":
+        x = np.sort(x, axis=1)
+    elif case == "descending":
+        x = np.sort(x, axis=1)[:, ::-1].copy()
+    stored = to_stored(x, dtype)
+    say("topk streamed %s k=%d dtype=%d" % (case, k, dtype))
+    out = opd.topk_support(as_device(stored, V), k, want_lse=True)
+    torch.cuda.synchronize()
+    ref = oracle.cache_rows("topk", dtype, stored, V, k)
+    check_topk(case, out, stored, V, k, dtype, ref)
+
+
+def test_topk_streamed_masked_rows_and_no_logp():
+    V, N, k = 20000, 6, 16
+    stored = make_logits(V, V, synth.BF16, N, seed=9)
+    mask = np.array([0, 1, 1, 0, 1, 1], np.uint8)
+    out = opd.topk_support(as_device(stored, V), k, mask=to_dev(mask), want_logp=False)
+    torch.cuda.synchronize()
+    idx = out["idx"].cpu().numpy()
+    assert np.all(idx[mask == 0] == 0)
+    ref = oracle.cache_rows("topk", synth.BF16, stored, V, k, mask=mask)
+    assert np.array_equal(idx, ref["ids"])
+
+
 def test_topk_masked_rows_and_no_logp():
     V, N, k = 5000, 6, 16
     stored = make_logits(V, V, synth.BF16, N, seed=9)
