@@ -40,6 +40,14 @@ struct OutBf16 {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// a * b with 0 * x = 0 for every x (NaN and infinities included): the
+// legacy multiply, for weights of zero times differences that may be NaN.
+// Bound to the compiler intrinsic rather than written as inline asm, so that
+// the wait state a VALU read of a fresh v_exp_f32 result needs on gfx950 is
+// inserted by the compiler (it does not inspect inline asm for that hazard).
+extern "C" __device__ float opd_fmul_legacy(float, float) __asm("llvm.amdgcn.fmul.legacy");
+__device__ __forceinline__ float mul_zero_safe(float a, float b) { return opd_fmul_legacy(a, b); }
+
 // ---------------------------------------------------------------- XCD-aware placement
 // The MI355X dispatcher hands workgroup b of a grid to XCD b % 8.  Remapping
 // b so that each XCD works through blocks of kXcdBlock consecutive rows (in

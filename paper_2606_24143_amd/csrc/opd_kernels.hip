@@ -543,19 +543,20 @@ __global__ void __launch_bounds__(kRowThreads) k_row_dense_resident(Args a) {
   Vec yq[kYAhead];
   const uint32_t nvec1 = fresh_s(nvec);
   const int tid1 = fresh_v(tid);
+  // teacher vector of slot s for this lane (whole slots take the plain
+  // address; a wave-uniform test)
+  auto y_load = [&](int s, uint32_t nv, int t) -> Vec {
+    if ((uint32_t)(s * NT + NT) <= nv) return ld_cached<TI>((const Vec*)yrow + s * NT, (uint32_t)t);
+    const uint32_t b = slot_base<NT>(s, nv);
+    return ld_cached<TI>((const Vec*)yrow + b, slot_off<NT>(s, b, t, nv));
+  };
 #pragma unroll
-  for (int j = 0; j < kYAhead && j < NSLOT; ++j) {
-    const uint32_t b = slot_base<NT>(j, nvec1);
-    yq[j] = ld_cached<TI>((const Vec*)yrow + b, slot_off<NT>(j, b, tid1, nvec1));
-  }
+  for (int j = 0; j < kYAhead && j < NSLOT; ++j) yq[j] = y_load(j, nvec1, tid1);
 #pragma unroll
   for (int s = 0; s < NSLOT; ++s) {
     const uint32_t b = slot_base<NT>(s, nvec1);
     Vec yv = yq[s % kYAhead];
-    if (s + kYAhead < NSLOT) {
-      const uint32_t bn = slot_base<NT>(s + kYAhead, nvec1);
-      yq[s % kYAhead] = ld_cached<TI>((const Vec*)yrow + bn, slot_off<NT>(s + kYAhead, bn, tid1, nvec1));
-    }
+    if (s + kYAhead < NSLOT) yq[s % kYAhead] = y_load(s + kYAhead, nvec1, tid1);
     if (s < YL) s_y[s][tid1] = yv;  // kept for sweep 2 (each lane reads back its own entry)
     if (!slot_owns<NT>(s, b, tid1, nvec1)) yv = neg_inf_vec<TI>();
     after(x[s], yv);
@@ -566,21 +567,21 @@ __global__ void __launch_bounds__(kRowThreads) k_row_dense_resident(Args a) {
 #pragma unroll
     for (int e = 1; e < EPV; ++e) vmy = fmaxf(vmy, fy[e]);
     const float mny = fmaxf(st.my, vmy);
-    const bool live = mny != kNegInf;  // some teacher entry seen so far is finite
     const float cy = rescale(st.my, mny);
-    const float nmy = live ? -mny * kLog2e : 0.f;
+    // while every teacher entry so far is -inf, exp(y - 0) = 0 for this slot
+    const float nmy = mny != kNegInf ? -mny * kLog2e : 0.f;
     float sy = st.sy * cy, tf = st.tf * cy;
-    // branch-free: entries with zero weight (the -inf tail, or an underflow)
-    // are excluded by selects, since their difference d can be NaN
+    // entries of zero weight (-inf, or an underflow) may have a NaN
+    // difference d: the legacy multiply gives 0 * d = 0 for any d
 #pragma unroll
     for (int e = 0; e < EPV; ++e) {
       const float pz = fast_exp2(fmaf(fz[e], kLog2e, nmz));
-      const float py = live ? fast_exp2(fmaf(fy[e], kLog2e, nmy)) : 0.f;
+      const float py = fast_exp2(fmaf(fy[e], kLog2e, nmy));
       const float d = fz[e] - fy[e];
       st.sz += pz;
-      st.tr += pz != 0.f ? pz * d : 0.f;
+      st.tr += mul_zero_safe(pz, d);
       sy += py;
-      tf -= py != 0.f ? py * d : 0.f;
+      tf -= mul_zero_safe(py, d);
     }
     st.my = mny;
     st.sy = sy;
@@ -601,10 +602,7 @@ __global__ void __launch_bounds__(kRowThreads) k_row_dense_resident(Args a) {
   const uint32_t nvec2 = fresh_s(nvec);
   const int tid2 = fresh_v(tid);
 #pragma unroll
-  for (int j = 0; j < kYAhead && YL + j < NSLOT; ++j) {
-    const uint32_t b = slot_base<NT>(YL + j, nvec2);
-    yq[j] = ld_cached<TI>((const Vec*)yrow + b, slot_off<NT>(YL + j, b, tid2, nvec2));
-  }
+  for (int j = 0; j < kYAhead && YL + j < NSLOT; ++j) yq[j] = y_load(YL + j, nvec2, tid2);
 #pragma unroll
   for (int s = 0; s < NSLOT; ++s) {
     const uint32_t b = slot_base<NT>(s, nvec2);
@@ -613,11 +611,7 @@ __global__ void __launch_bounds__(kRowThreads) k_row_dense_resident(Args a) {
       yv = s_y[s][tid2];
     } else {
       yv = yq[(s - YL) % kYAhead];
-      if (s + kYAhead < NSLOT) {
-        const uint32_t bn = slot_base<NT>(s + kYAhead, nvec2);
-        yq[(s - YL) % kYAhead] =
-            ld_cached<TI>((const Vec*)yrow + bn, slot_off<NT>(s + kYAhead, bn, tid2, nvec2));
-      }
+      if (s + kYAhead < NSLOT) yq[(s - YL) % kYAhead] = y_load(s + kYAhead, nvec2, tid2);
     }
     after(x[s], yv);
     if (slot_owns<NT>(s, b, tid2, nvec2)) {
