@@ -16,6 +16,7 @@
 // of each logit where the row fits in registers, non-temporal hints so the
 // stream does not evict anything useful from L2.
 #include <math.h>
+#include <type_traits>
 
 #include "opd_device.h"
 
@@ -51,23 +52,42 @@ __device__ __forceinline__ DenseRow dense_row(const Stats& s) {
 
 // Gradient values of one vector for the dense estimators:
 //   forward  g = gamma (p - q);   reverse  g = gamma p ((z - y) - E_p[z - y]),
-// the softmax-Jacobian form of eq. reverse-kl-gradient.
-template <class TI, int EST>
+// the softmax-Jacobian form of eq. reverse-kl-gradient.  |gamma| enters the
+// exponents as log2|gamma| (DenseGrad) and its sign the operand order (NEG),
+// so no element is multiplied by gamma.
+struct DenseGrad {
+  float nLz, nLy;  // log2|gamma| - L * log2(e), student and teacher
+  float ez;
+  bool neg;        // gamma < 0
+};
+__device__ __forceinline__ DenseGrad dense_grad_consts(const DenseRow& d, float gamma) {
+  const float lg = log2f(fabsf(gamma));  // -inf for gamma = 0: every g is 0
+  return DenseGrad{fmaf(-d.Lz, kLog2e, lg), fmaf(-d.Ly, kLog2e, lg), d.ez, gamma < 0.f};
+}
+template <class TI, int EST, bool NEG>
 __device__ __forceinline__ void dense_grad(const typename TI::Vec& xz, const typename TI::Vec& xy,
-                                           const DenseRow& d,
-                                           float gamma, float (&g)[TI::EPV]) {
+                                           const DenseGrad& k, float (&g)[TI::EPV]) {
   float fz[TI::EPV], fy[TI::EPV];
   unpack<TI>(xz, fz);
   unpack<TI>(xy, fy);
-  const float nLz = -d.Lz * kLog2e, nLy = -d.Ly * kLog2e;
 #pragma unroll
   for (int e = 0; e < TI::EPV; ++e) {
-    const float p = fast_exp2(fmaf(fz[e], kLog2e, nLz));
-    if constexpr (EST == FKL_DENSE)
-      g[e] = gamma * (p - fast_exp2(fmaf(fy[e], kLog2e, nLy)));
-    else
-      g[e] = gamma * p * ((fz[e] - fy[e]) - d.ez);
+    const float p = fast_exp2(fmaf(fz[e], kLog2e, k.nLz));  // |gamma| p
+    if constexpr (EST == FKL_DENSE) {
+      const float q = fast_exp2(fmaf(fy[e], kLog2e, k.nLy));
+      g[e] = NEG ? q - p : p - q;
+    } else {
+      g[e] = NEG ? p * ((fy[e] - fz[e]) + k.ez) : p * ((fz[e] - fy[e]) - k.ez);
+    }
   }
+}
+template <class TI, int EST>
+__device__ __forceinline__ void dense_grad(const typename TI::Vec& xz, const typename TI::Vec& xy,
+                                           const DenseGrad& k, float (&g)[TI::EPV]) {
+  if (k.neg)
+    dense_grad<TI, EST, true>(xz, xy, k, g);
+  else
+    dense_grad<TI, EST, false>(xz, xy, k, g);
 }
 
 // ---------------------------------------------------------------- cache, estimator, spikes
@@ -579,9 +599,12 @@ __global__ void __launch_bounds__(kRowThreads) k_row_dense_resident(Args a) {
       const float py = fast_exp2(fmaf(fy[e], kLog2e, nmy));
       const float d = fz[e] - fy[e];
       st.sz += pz;
-      st.tr += mul_zero_safe(pz, d);
       sy += py;
-      tf -= mul_zero_safe(py, d);
+      // the reverse estimator needs E_p[z - y], the forward one E_q[y - z]
+      if constexpr (EST == RKL_DENSE)
+        st.tr += mul_zero_safe(pz, d);
+      else
+        tf -= mul_zero_safe(py, d);
     }
     st.my = mny;
     st.sy = sy;
@@ -598,29 +621,38 @@ __global__ void __launch_bounds__(kRowThreads) k_row_dense_resident(Args a) {
   }
 
   // sweep 2: gradient from the resident z; y from LDS for the first YL slots,
-  // a second read for the rest
-  const uint32_t nvec2 = fresh_s(nvec);
-  const int tid2 = fresh_v(tid);
+  // a second read for the rest.  One copy per sign of gamma (a row-uniform
+  // branch), so the sign costs no instruction per element.
+  const DenseGrad k = dense_grad_consts(d, a.gamma);
+  auto sweep2 = [&](auto neg) {
+    constexpr bool NEG = decltype(neg)::value;
+    const uint32_t nvec2 = fresh_s(nvec);
+    const int tid2 = fresh_v(tid);
 #pragma unroll
-  for (int j = 0; j < kYAhead && YL + j < NSLOT; ++j) yq[j] = y_load(YL + j, nvec2, tid2);
+    for (int j = 0; j < kYAhead && YL + j < NSLOT; ++j) yq[j] = y_load(YL + j, nvec2, tid2);
 #pragma unroll
-  for (int s = 0; s < NSLOT; ++s) {
-    const uint32_t b = slot_base<NT>(s, nvec2);
-    Vec yv;
-    if (s < YL) {
-      yv = s_y[s][tid2];
-    } else {
-      yv = yq[(s - YL) % kYAhead];
-      if (s + kYAhead < NSLOT) yq[(s - YL) % kYAhead] = y_load(s + kYAhead, nvec2, tid2);
+    for (int s = 0; s < NSLOT; ++s) {
+      const uint32_t b = slot_base<NT>(s, nvec2);
+      Vec yv;
+      if (s < YL) {
+        yv = s_y[s][tid2];
+      } else {
+        yv = yq[(s - YL) % kYAhead];
+        if (s + kYAhead < NSLOT) yq[(s - YL) % kYAhead] = y_load(s + kYAhead, nvec2, tid2);
+      }
+      after(x[s], yv);
+      if (slot_owns<NT>(s, b, tid2, nvec2)) {
+        float g[EPV];
+        dense_grad<TI, EST, NEG>(x[s], yv, k, g);
+        store_vec<TI, TO>((char*)grow + (size_t)b * EPV * TO::BYTES, (uint32_t)tid2, g, EPV);
+      }
+      __builtin_amdgcn_sched_barrier(0);
     }
-    after(x[s], yv);
-    if (slot_owns<NT>(s, b, tid2, nvec2)) {
-      float g[EPV];
-      dense_grad<TI, EST>(x[s], yv, d, a.gamma, g);
-      store_vec<TI, TO>((char*)grow + (size_t)b * EPV * TO::BYTES, (uint32_t)tid2, g, EPV);
-    }
-    __builtin_amdgcn_sched_barrier(0);
-  }
+  };
+  if (k.neg)
+    sweep2(std::true_type{});
+  else
+    sweep2(std::false_type{});
 }
 
 // Sweep-1 statistics of vectors [v0, v1) of a row, one lane's share
@@ -690,9 +722,10 @@ __global__ void __launch_bounds__(kRowThreads) k_row_stream(Args a) {
       a.loss[row] = d.loss;
       if (a.lse_out) a.lse_out[row] = d.Lz;
     }
+    const DenseGrad dk = dense_grad_consts(d, a.gamma);
     for (int64_t v = tid; v < a.nvec; v += NT) {
       float g[EPV];
-      dense_grad<TI, EST>(ld_cached<TI>(zrow, v), ld_cached<TI>(yrow, v), d, a.gamma, g);
+      dense_grad<TI, EST>(ld_cached<TI>(zrow, v), ld_cached<TI>(yrow, v), dk, g);
       store_vec<TI, TO>(grow, v, g, v == a.nvec - 1 ? a.tail : EPV);
     }
   } else {
@@ -790,9 +823,10 @@ __global__ void __launch_bounds__(kSplitThreads) k_split_write(Args a) {
       a.loss[row] = d.loss;
       if (a.lse_out) a.lse_out[row] = d.Lz;
     }
+    const DenseGrad dk = dense_grad_consts(d, a.gamma);
     for (int64_t v = v0 + tid; v < v1; v += NT) {
       float g[EPV];
-      dense_grad<TI, EST>(ld_cached<TI>(zrow, v), ld_cached<TI>(yrow, v), d, a.gamma, g);
+      dense_grad<TI, EST>(ld_cached<TI>(zrow, v), ld_cached<TI>(yrow, v), dk, g);
       store_vec<TI, TO>(grow, v, g, v == a.nvec - 1 ? a.tail : EPV);
     }
   } else {

@@ -90,6 +90,28 @@ def test_parity_small(shape, dtype, est, path):
     compare("%s/%s/%s" % (shape, est, path), w, d, est, out, ref, mask)
 
 
+@pytest.mark.parametrize("gamma", [-0.5, 0.0, 3.0])
+@pytest.mark.parametrize("est", ALL)
+@pytest.mark.parametrize("shape", ["v3001_tail", "v151936"])
+def test_grad_scale_sign_and_zero(shape, est, gamma):
+    """The gradient scale enters some kernels through the exponent (log2|gamma|)
+    and its sign through the operand order: negative and zero scales, on every
+    path, against the oracle's gamma * dloss/dz."""
+    w, d, mask = small_inputs(shape, synth.BF16)
+    N, V, ld = SHAPES[shape]
+    say("grad-scale %s %s gamma=%g" % (shape, est, gamma))
+    logits = to_dev(d["logits"])[:, :V]
+    teacher = to_dev(d["teacher_logits"])[:, :V] if est in DENSE else None
+    ids, tau, beta = cache_arrays(d, est)
+    ref = oracle_for(w, d, est, mask, gamma=gamma)
+    for path, flags in PATHS.items():
+        out = run_gpu(logits, est, ids, tau, beta, teacher, mask=mask, grad_scale=gamma,
+                      flags=flags)
+        compare("%s/%s/%s/gamma=%g" % (shape, est, path, gamma), w, d, est, out, ref, mask)
+        if gamma == 0.0:
+            assert not out["dlogits"].any(), "a zero gradient scale leaves dlogits zero"
+
+
 @pytest.mark.parametrize("est", ALL)
 @pytest.mark.parametrize("shape", ["v1000", "v3001_tail", "v151936"])
 def test_parity_bf16_gradient_output(shape, est):
