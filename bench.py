@@ -13,6 +13,9 @@ Prints one JSON line on stdout:
               (one read of the logits, one write of the gradient, the cache)
               over the mean launch time measured with HIP events on the
               launch stream, against the 8 TB/s MI355X peak
+  two_read_model  the same launch priced with a second read of each row for
+              the estimators whose gradient is dense (MC, truncated top-k,
+              dense): the bytes a kernel that re-reads the row would move
   cpu_baseline  the oracle on a bounded sample of the same workload, on the
               host cores
 
@@ -83,6 +86,19 @@ def algorithmic_bytes(w, est: str, n_valid: int, n_masked: int) -> int:
         row_read = V * in_b
         cache = K * (4 + 4 + (0 if est == "rkl_mc_nois" else 4))
     return n_valid * (row_read + cache) + (n_valid + n_masked) * (V * out_b + 4)
+
+
+def second_read_bytes(w, est: str, n_valid: int) -> int:
+    """Extra bytes of the two-read accounting model: estimators whose dense
+    gradient depends on every logit (MC, truncated top-k, dense) are charged
+    a second read of each valid row (both rows for the dense estimators), as
+    a kernel that does not hold the row on chip would move.  The renormalised
+    top-k estimators read only the cached entries and are charged nothing."""
+    in_b = 2 if w.dtype == 1 else 4
+    if est in ("fkl_topk", "rkl_topk"):
+        return 0
+    rows = 2 if est in ("fkl_dense", "rkl_dense") else 1
+    return n_valid * rows * w.V * in_b
 
 
 def cache_op_bytes(w, op: str, n_valid: int, K: int) -> int:
@@ -335,6 +351,12 @@ def main():
                      "mean_launch_ms": mean_launch_s * 1e3,
                      "min_launch_ms": min(launch_ms)},
     }
+    res["roofline"]["median_launch_ms"] = sorted(launch_ms)[len(launch_ms) // 2]
+    if op == "loss":
+        model = alg + second_read_bytes(w, est, n_valid)
+        res["two_read_model"] = {"bytes_per_launch": model,
+                                 "GBps": model / mean_launch_s / 1e9,
+                                 "frac": model / mean_launch_s / 1e9 / PEAK_HBM_GBS}
     if args.calib_copy:
         n = args.calib_copy * (1 << 20) // 4
         a = torch.ones(n, dtype=torch.float32, device=dev)
@@ -348,8 +370,9 @@ def main():
             b.copy_(a)
         e1.record(stream)
         torch.cuda.synchronize()
-        res["copy_calibration"] = {"bytes_per_copy": 2 * n * 4,
-                                   "GBps": 2 * n * 4 * 10 / (e0.elapsed_time(e1) / 1e3) / 1e9}
+        copy_gbs = 2 * n * 4 * 10 / (e0.elapsed_time(e1) / 1e3) / 1e9
+        res["copy_calibration"] = {"bytes_per_copy": 2 * n * 4, "GBps": copy_gbs,
+                                   "frac_of_copy": achieved / copy_gbs}
     if not args.no_cpu_baseline:
         del logits
         torch.cuda.empty_cache()
