@@ -149,6 +149,35 @@ __device__ __forceinline__ typename TI::Vec ld_cached(const void* row, IdxT v) {
   return ((const typename TI::Vec*)row)[v];
 }
 
+// ---------------------------------------------------------------- buffer access
+// A buffer resource for one slot of a row: its base is the slot's first
+// vector and its byte count what remains of the row from there (0 for a slot
+// wholly past the end).  The hardware checks each lane's offset against that
+// count: loads past the end return zeros, stores past the end are dropped.
+// The check covers the lane offset only, not the scalar offset operand, so
+// the slot's position goes into the base (scalar arithmetic) and the scalar
+// offset stays 0.  A lane then addresses every slot with one fixed offset and
+// no arithmetic or bounds test of its own.
+typedef __amdgpu_buffer_rsrc_t Rsrc;
+constexpr int kRsrcWord3 = 0x00020000;  // raw access, 32-bit data format
+constexpr int kAuxNt = 2;              // cache policy: non-temporal
+// (row bytes < 2^31; the count is clamped with a signed max, which has a
+// scalar instruction, and read back as a scalar so the resource stays in
+// scalar registers)
+__device__ __forceinline__ Rsrc slot_rsrc(const void* row, uint32_t row_bytes, uint32_t off) {
+  const int left = (int)row_bytes - (int)off;
+  const int count = __builtin_amdgcn_readfirstlane(left > 0 ? left : 0);
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>((const char*)row + off), 0, count,
+                                           kRsrcWord3);
+}
+template <class TI, int AUX>
+__device__ __forceinline__ typename TI::Vec buf_ld(Rsrc r, uint32_t voff) {
+  if constexpr (TI::BYTES == 2)
+    return __builtin_amdgcn_raw_buffer_load_b64(r, (int)voff, 0, AUX);
+  else
+    return __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, 0, AUX);
+}
+
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   const uint32_t a = __builtin_bit_cast(uint16_t, (__bf16)lo);
   const uint32_t b = __builtin_bit_cast(uint16_t, (__bf16)hi);
@@ -174,6 +203,20 @@ __device__ __forceinline__ void store_vec(void* grow, IdxT v, const float (&g)[4
     else
       for (int e = 0; e < valid; ++e) p[e] = __builtin_bit_cast(uint16_t, (__bf16)g[e]);
   }
+}
+
+// Store the four gradient values of a vector through a slot's buffer resource
+// (non-temporal; a store past the row's end is dropped).
+template <class TO>
+__device__ __forceinline__ void buf_store(Rsrc r, uint32_t voff, const float (&g)[4]) {
+  if constexpr (TO::BYTES == 4)
+    __builtin_amdgcn_raw_buffer_store_b128(
+        u32x4{__float_as_uint(g[0]), __float_as_uint(g[1]), __float_as_uint(g[2]),
+              __float_as_uint(g[3])},
+        r, (int)voff, 0, kAuxNt);
+  else
+    __builtin_amdgcn_raw_buffer_store_b64(u32x2{pack_bf16x2(g[0], g[1]), pack_bf16x2(g[2], g[3])},
+                                          r, (int)voff, 0, kAuxNt);
 }
 
 // ---------------------------------------------------------------- reductions
@@ -276,6 +319,31 @@ __device__ __forceinline__ Stats block_merge(Stats s, Stats* red) {
   Stats r = red[0];
 #pragma unroll
   for (int w = 1; w < NW; ++w) r = stats_merge<DENSE>(r, red[w]);
+  __syncthreads();
+  return r;
+}
+
+// The same merge with the NW wave results combined by a butterfly over NW
+// lanes of every wave (log2(NW) steps instead of NW - 1 in sequence).  The
+// pairing, and so the rounding, is fixed.  NW is a power of two up to 64.
+template <bool DENSE, int NW>
+__device__ __forceinline__ Stats block_merge_tree(Stats s, Stats* red) {
+  static_assert((NW & (NW - 1)) == 0 && NW <= 64, "NW: a power of two up to 64");
+  s = wave_merge<DENSE>(s);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
+  __syncthreads();
+  Stats r = red[threadIdx.x & (NW - 1)];
+#pragma unroll
+  for (int o = NW / 2; o >= 1; o >>= 1) {
+    Stats t;
+    t.mz = __shfl_xor(r.mz, o, 64);
+    t.sz = __shfl_xor(r.sz, o, 64);
+    t.tr = __shfl_xor(r.tr, o, 64);
+    t.my = __shfl_xor(r.my, o, 64);
+    t.sy = __shfl_xor(r.sy, o, 64);
+    t.tf = __shfl_xor(r.tf, o, 64);
+    r = stats_merge<DENSE>(r, t);
+  }
   __syncthreads();
   return r;
 }

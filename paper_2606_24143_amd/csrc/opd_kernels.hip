@@ -60,9 +60,14 @@ struct DenseGrad {
   float ez;
   bool neg;        // gamma < 0
 };
+// (row-uniform values: read back as scalars, so they occupy no lane registers)
+__device__ __forceinline__ float uniform(float v) {
+  return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(v)));
+}
 __device__ __forceinline__ DenseGrad dense_grad_consts(const DenseRow& d, float gamma) {
   const float lg = log2f(fabsf(gamma));  // -inf for gamma = 0: every g is 0
-  return DenseGrad{fmaf(-d.Lz, kLog2e, lg), fmaf(-d.Ly, kLog2e, lg), d.ez, gamma < 0.f};
+  return DenseGrad{uniform(fmaf(-d.Lz, kLog2e, lg)), uniform(fmaf(-d.Ly, kLog2e, lg)),
+                   uniform(d.ez), gamma < 0.f};
 }
 template <class TI, int EST, bool NEG>
 __device__ __forceinline__ void dense_grad(const typename TI::Vec& xz, const typename TI::Vec& xy,
@@ -504,6 +509,14 @@ __global__ void __launch_bounds__(kRowThreads) k_row_resident(Args a) {
 // teacher rows live, which fits the 256 MB Infinity Cache, so the second
 // read of y can be served from there instead of HBM.
 constexpr int kYAhead = 4;
+constexpr int kXAhead = 8;
+// offsets of the running sums are raised when an exponent (log2 units)
+// exceeds this: terms stay below 2^24, sums of a row below 2^42
+constexpr float kLazyRaise = 24.f;
+// -offset * log2(e) before any value is seen: an offset of about -2.08e38,
+// so a lane's first value above that raises it (a row whose every logit is
+// below it reads as a row of -inf)
+constexpr float kOffsetFloor = 3e38f;
 // LDS that holds the first teacher slots between the sweeps: only the rest
 // of the teacher row is read a second time.
 constexpr int kYLdsBytes = 144 * 1024;
@@ -514,7 +527,6 @@ __global__ void __launch_bounds__(kRowThreads) k_row_dense_resident(Args a) {
   typedef typename TI::Vec Vec;
   constexpr int YL_CAP = kYLdsBytes / (NT * (int)sizeof(Vec));
   constexpr int YL = YL_CAP < NSLOT ? YL_CAP : NSLOT;  // teacher slots kept in LDS
-  __shared__ float s_red[NW];
   __shared__ Stats s_st[NW];
   __shared__ Vec s_y[YL][NT];
   const int tid = threadIdx.x;
@@ -527,93 +539,121 @@ __global__ void __launch_bounds__(kRowThreads) k_row_dense_resident(Args a) {
     return;
   }
   const uint32_t nvec = (uint32_t)a.nvec;  // <= NSLOT * NT
-
-  Vec x[NSLOT];
-#pragma unroll
-  for (int s = 0; s < NSLOT; ++s) {
-    const uint32_t b = slot_base<NT>(s, nvec);
-    x[s] = ld_nt<TI>((const Vec*)zrow + b, slot_off<NT>(s, b, tid, nvec));
-  }
-#pragma unroll
-  for (int s = 0; s < NSLOT; ++s)
-    if (!slot_owns<NT>(s, slot_base<NT>(s, nvec), tid, nvec)) x[s] = neg_inf_vec<TI>();
-  // sweep 1a: student max over the registers
-  float mx[EPV];
-#pragma unroll
-  for (int e = 0; e < EPV; ++e) mx[e] = kNegInf;
-#pragma unroll
-  for (int s = 0; s < NSLOT; ++s) {
-    float f[EPV];
-    unpack<TI>(x[s], f);
-#pragma unroll
-    for (int e = 0; e < EPV; ++e) mx[e] = fmaxf(mx[e], f[e]);
-  }
-  float mz = mx[0];
-#pragma unroll
-  for (int e = 1; e < EPV; ++e) mz = fmaxf(mz, mx[e]);
-#pragma unroll
-  for (int s = 0; s < NSLOT; ++s) keep_packed(x[s]);
-  mz = block_max<NW>(mz, s_red);
-
-  // sweep 1b: stream y; student sums at the known max, teacher sums online.
-  // y is prefetched kYAhead slots ahead through a small ring; the scheduling
-  // barriers stop the compiler from hoisting every y load (76 more VGPRs).
-  const float nmz = -mz * kLog2e;
-  Stats st{mz, 0.f, 0.f, kNegInf, 0.f, 0.f};
-  Vec yq[kYAhead];
-  const uint32_t nvec1 = fresh_s(nvec);
-  const int tid1 = fresh_v(tid);
-  // teacher vector of slot s for this lane (whole slots take the plain
-  // address; a wave-uniform test)
-  auto y_load = [&](int s, uint32_t nv, int t) -> Vec {
-    if ((uint32_t)(s * NT + NT) <= nv) return ld_cached<TI>((const Vec*)yrow + s * NT, (uint32_t)t);
-    const uint32_t b = slot_base<NT>(s, nv);
-    return ld_cached<TI>((const Vec*)yrow + b, slot_off<NT>(s, b, t, nv));
+  // Slot s of a lane is vector s * NT + tid of the row, read and written
+  // through the slot's buffer resource: past the row's last vector, loads
+  // return zeros (replaced by -inf below) and gradient stores are dropped.
+  constexpr uint32_t kSlotIn = NT * sizeof(Vec), kSlotOut = NT * EPV * TO::BYTES;
+  const uint32_t in_bytes = nvec * (uint32_t)sizeof(Vec);
+  auto z_slot = [&](int s) { return slot_rsrc(zrow, in_bytes, s * kSlotIn); };
+  auto y_slot = [&](int s) { return slot_rsrc(yrow, in_bytes, s * kSlotIn); };
+  auto g_slot = [&](int s) {
+    return slot_rsrc(grow, nvec * (uint32_t)(EPV * TO::BYTES), s * kSlotOut);
   };
+  // the large variant takes only rows longer than the small one holds, so its
+  // first slots_small slots are always whole
+  constexpr int DT = TI::BYTES == 2 ? BF16 : F32;
+  constexpr int FULL = NSLOT == slots_large(DT) ? slots_small(DT) : 0;
+  auto in_row = [](int s, int t, uint32_t nv) {
+    return s < FULL || (uint32_t)(s * NT + t) < nv;
+  };
+
+  // sweep 1, one pass over both rows: per-lane sums of exp(z - oz) and
+  // exp(y - oy) and the estimator's cross term, at offsets oz, oy that start
+  // at a finite floor and are raised (with a rescale of the sums) only when
+  // an exponent exceeds kLazyRaise: a wave-uniform branch, taken for the
+  // first slot and rarely after.  The sums are exact at any offset; the
+  // margin bounds each term by 2^kLazyRaise.  The student row fills its
+  // registers kXAhead slots ahead of use and the teacher row streams through
+  // a ring kYAhead slots deep, so the first slot starts as soon as its own
+  // data has landed.  The scheduling barriers keep the loads in this order.
+  Vec x[NSLOT];
+  Vec yq[kYAhead];
+  Stats st;
+  {
+    const uint32_t nvec1 = fresh_s(nvec);
+    const int tid1 = fresh_v(tid);
+    const uint32_t vo1 = fresh_v((uint32_t)tid * (uint32_t)sizeof(Vec));
 #pragma unroll
-  for (int j = 0; j < kYAhead && j < NSLOT; ++j) yq[j] = y_load(j, nvec1, tid1);
-#pragma unroll
-  for (int s = 0; s < NSLOT; ++s) {
-    const uint32_t b = slot_base<NT>(s, nvec1);
-    Vec yv = yq[s % kYAhead];
-    if (s + kYAhead < NSLOT) yq[s % kYAhead] = y_load(s + kYAhead, nvec1, tid1);
-    if (s < YL) s_y[s][tid1] = yv;  // kept for sweep 2 (each lane reads back its own entry)
-    if (!slot_owns<NT>(s, b, tid1, nvec1)) yv = neg_inf_vec<TI>();
-    after(x[s], yv);
-    float fz[EPV], fy[EPV];
-    unpack<TI>(x[s], fz);
-    unpack<TI>(yv, fy);
-    float vmy = fy[0];
-#pragma unroll
-    for (int e = 1; e < EPV; ++e) vmy = fmaxf(vmy, fy[e]);
-    const float mny = fmaxf(st.my, vmy);
-    const float cy = rescale(st.my, mny);
-    // while every teacher entry so far is -inf, exp(y - 0) = 0 for this slot
-    const float nmy = mny != kNegInf ? -mny * kLog2e : 0.f;
-    float sy = st.sy * cy, tf = st.tf * cy;
-    // entries of zero weight (-inf, or an underflow) may have a NaN
-    // difference d: the legacy multiply gives 0 * d = 0 for any d
-#pragma unroll
-    for (int e = 0; e < EPV; ++e) {
-      const float pz = fast_exp2(fmaf(fz[e], kLog2e, nmz));
-      const float py = fast_exp2(fmaf(fy[e], kLog2e, nmy));
-      const float d = fz[e] - fy[e];
-      st.sz += pz;
-      sy += py;
-      // the reverse estimator needs E_p[z - y], the forward one E_q[y - z]
-      if constexpr (EST == RKL_DENSE)
-        st.tr += mul_zero_safe(pz, d);
-      else
-        tf -= mul_zero_safe(py, d);
+    for (int j = 0; j < kXAhead && j < NSLOT; ++j) {
+      x[j] = buf_ld<TI, kAuxNt>(z_slot(j), vo1);
+      if (j < kYAhead) yq[j] = buf_ld<TI, 0>(y_slot(j), vo1);
     }
-    st.my = mny;
-    st.sy = sy;
-    st.tf = tf;
-    __builtin_amdgcn_sched_barrier(0);
-  }
+    // -offset * log2(e) of each row, from the floor
+    float nz = kOffsetFloor, ny = kOffsetFloor;
+    float sz = 0.f, sy = 0.f, tx = 0.f;  // tx: E_p[z - y] (reverse) or E_q[y - z] (forward)
 #pragma unroll
-  for (int s = 0; s < NSLOT; ++s) keep_packed(x[s]);
-  st = block_merge<true, NW>(st, s_st);
+    for (int s = 0; s < NSLOT; ++s) {
+      if (s + kXAhead < NSLOT) x[s + kXAhead] = buf_ld<TI, kAuxNt>(z_slot(s + kXAhead), vo1);
+      Vec yv = yq[s % kYAhead];
+      if (s + kYAhead < NSLOT) yq[s % kYAhead] = buf_ld<TI, 0>(y_slot(s + kYAhead), vo1);
+      if (s < YL) s_y[s][tid1] = yv;  // kept for sweep 2 (each lane reads back its own entry)
+      if (!in_row(s, tid1, nvec1)) {
+        x[s] = neg_inf_vec<TI>();
+        yv = neg_inf_vec<TI>();
+      }
+      float fz[EPV], fy[EPV], az[EPV], ay[EPV];
+      unpack<TI>(x[s], fz);
+      unpack<TI>(yv, fy);
+#pragma unroll
+      for (int e = 0; e < EPV; ++e) {
+        az[e] = fmaf(fz[e], kLog2e, nz);
+        ay[e] = fmaf(fy[e], kLog2e, ny);
+      }
+      float hz = az[0], hy = ay[0];
+#pragma unroll
+      for (int e = 1; e < EPV; ++e) {
+        hz = fmaxf(hz, az[e]);
+        hy = fmaxf(hy, ay[e]);
+      }
+      if (__builtin_amdgcn_ballot_w64(hz > kLazyRaise || hy > kLazyRaise) != 0) {
+        // raise each offset to the slot's maximum where that is higher
+        float vz = fz[0], vy = fy[0];
+#pragma unroll
+        for (int e = 1; e < EPV; ++e) {
+          vz = fmaxf(vz, fz[e]);
+          vy = fmaxf(vy, fy[e]);
+        }
+        const float nz2 = fminf(nz, -vz * kLog2e), ny2 = fminf(ny, -vy * kLog2e);
+        const float cz = fast_exp2(nz2 - nz), cy = fast_exp2(ny2 - ny);
+        sz *= cz;
+        sy *= cy;
+        tx *= EST == RKL_DENSE ? cz : cy;
+        nz = nz2;
+        ny = ny2;
+#pragma unroll
+        for (int e = 0; e < EPV; ++e) {
+          az[e] = fmaf(fz[e], kLog2e, nz);
+          ay[e] = fmaf(fy[e], kLog2e, ny);
+        }
+      }
+      // entries of zero weight (-inf, or an underflow) may have a NaN
+      // difference d: the legacy multiply gives 0 * d = 0 for any d
+#pragma unroll
+      for (int e = 0; e < EPV; ++e) {
+        const float pz = fast_exp2(az[e]);
+        const float py = fast_exp2(ay[e]);
+        const float d = fz[e] - fy[e];
+        sz += pz;
+        sy += py;
+        if constexpr (EST == RKL_DENSE)
+          tx += mul_zero_safe(pz, d);
+        else
+          tx -= mul_zero_safe(py, d);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    // The offsets as values.  A lane that never left the floor reports -inf,
+    // which the merge's rescale treats exactly; the opaque copy makes the
+    // product a rounded value, so that the merge's offset differences are
+    // exactly 0 where two offsets are equal (left to the compiler, the
+    // product is fused into those differences and leaves its rounding error,
+    // about 1e23 at the floor).
+    constexpr float kLn2 = 0.6931471805599453f;
+    const float oz = fresh_v(-nz * kLn2), oy = fresh_v(-ny * kLn2);
+    st = Stats{nz == kOffsetFloor ? kNegInf : oz, sz, EST == RKL_DENSE ? tx : 0.f,
+               ny == kOffsetFloor ? kNegInf : oy, sy, EST == RKL_DENSE ? 0.f : tx};
+  }
+  st = block_merge_tree<true, NW>(st, s_st);
   const DenseRow d = dense_row<EST>(st);
   if (tid == 0) {
     a.loss[row] = d.loss;
@@ -622,30 +662,31 @@ __global__ void __launch_bounds__(kRowThreads) k_row_dense_resident(Args a) {
 
   // sweep 2: gradient from the resident z; y from LDS for the first YL slots,
   // a second read for the rest.  One copy per sign of gamma (a row-uniform
-  // branch), so the sign costs no instruction per element.
+  // branch), so the sign costs no instruction per element.  Lanes past the
+  // row's end compute values from -inf that their dropped stores discard.
   const DenseGrad k = dense_grad_consts(d, a.gamma);
   auto sweep2 = [&](auto neg) {
     constexpr bool NEG = decltype(neg)::value;
-    const uint32_t nvec2 = fresh_s(nvec);
     const int tid2 = fresh_v(tid);
+    const uint32_t vo2 = fresh_v((uint32_t)tid * (uint32_t)sizeof(Vec));
+    const uint32_t vg2 = fresh_v((uint32_t)tid * (uint32_t)(EPV * TO::BYTES));
 #pragma unroll
-    for (int j = 0; j < kYAhead && YL + j < NSLOT; ++j) yq[j] = y_load(YL + j, nvec2, tid2);
+    for (int j = 0; j < kYAhead && YL + j < NSLOT; ++j)
+      yq[j] = buf_ld<TI, 0>(y_slot(YL + j), vo2);
 #pragma unroll
     for (int s = 0; s < NSLOT; ++s) {
-      const uint32_t b = slot_base<NT>(s, nvec2);
       Vec yv;
       if (s < YL) {
         yv = s_y[s][tid2];
       } else {
         yv = yq[(s - YL) % kYAhead];
-        if (s + kYAhead < NSLOT) yq[(s - YL) % kYAhead] = y_load(s + kYAhead, nvec2, tid2);
+        if (s + kYAhead < NSLOT)
+          yq[(s - YL) % kYAhead] = buf_ld<TI, 0>(y_slot(s + kYAhead), vo2);
       }
       after(x[s], yv);
-      if (slot_owns<NT>(s, b, tid2, nvec2)) {
-        float g[EPV];
-        dense_grad<TI, EST, NEG>(x[s], yv, k, g);
-        store_vec<TI, TO>((char*)grow + (size_t)b * EPV * TO::BYTES, (uint32_t)tid2, g, EPV);
-      }
+      float g[EPV];
+      dense_grad<TI, EST, NEG>(x[s], yv, k, g);
+      buf_store<TO>(g_slot(s), vg2, g);
       __builtin_amdgcn_sched_barrier(0);
     }
   };
