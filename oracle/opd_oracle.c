@@ -217,6 +217,9 @@ static void mc_no_is(const double* z, int64_t V, double L, const int32_t* ids, c
  *   D_R = sum_a p_theta (log p_theta - log q),
  *   dD_R/dz_j = p_j ((log p_j - log q_j) - D_R)   (eq. reverse-kl-gradient
  *   pushed through the softmax Jacobian).
+ * A term whose weight is zero (q_j for D_F, p_j for D_R) is zero, by the
+ * convention 0 log(0/x) = 0 of the KL divergence: an action that both
+ * distributions give logit -inf drops out, as if absent from the vocabulary.
  */
 static void dense_kl(int reverse, const double* z, const double* y, int64_t V, double L,
                      double gamma, double* loss, double* grad) {
@@ -224,17 +227,18 @@ static void dense_kl(int reverse, const double* z, const double* y, int64_t V, d
   double kl = 0.0;
   for (int64_t j = 0; j < V; ++j) {
     const double logp = z[j] - L, logq = y[j] - Ly;
-    if (reverse)
-      kl += exp(logp) * (logp - logq);
-    else
-      kl += exp(logq) * (logq - logp);
+    const double w = reverse ? exp(logp) : exp(logq);
+    if (w != 0.0) kl += reverse ? w * (logp - logq) : w * (logq - logp);
   }
   *loss = kl;
   if (!grad) return;
   for (int64_t j = 0; j < V; ++j) {
     const double logp = z[j] - L, logq = y[j] - Ly;
     const double p = exp(logp), q = exp(logq);
-    grad[j] = reverse ? gamma * p * ((logp - logq) - kl) : gamma * (p - q);
+    if (reverse)
+      grad[j] = p != 0.0 ? gamma * p * ((logp - logq) - kl) : 0.0;
+    else
+      grad[j] = gamma * (p - q);
   }
 }
 

@@ -374,26 +374,27 @@ __device__ __forceinline__ void stats_add(Stats& s, const typename TI::Vec& xz,
     float vmy = fy[0];
 #pragma unroll
     for (int e = 1; e < EPV; ++e) vmy = fmaxf(vmy, fy[e]);
+    // each row on its own: while a row's maximum is -inf its terms are 0
+    // (offset 0 keeps exp(-inf) = 0 instead of exp(-inf + inf))
     const float mnz = fmaxf(s.mz, vm), mny = fmaxf(s.my, vmy);
-    if (mnz != kNegInf && mny != kNegInf) {
-      const float cz = rescale(s.mz, mnz), cy = rescale(s.my, mny);
-      float sz = s.sz * cz, tr = s.tr * cz, sy = s.sy * cy, tf = s.tf * cy;
-      const float nmz = -mnz * kLog2e, nmy = -mny * kLog2e;
+    const float cz = rescale(s.mz, mnz), cy = rescale(s.my, mny);
+    float sz = s.sz * cz, tr = s.tr * cz, sy = s.sy * cy, tf = s.tf * cy;
+    const float nmz = mnz != kNegInf ? -mnz * kLog2e : 0.f;
+    const float nmy = mny != kNegInf ? -mny * kLog2e : 0.f;
 #pragma unroll
-      for (int e = 0; e < EPV; ++e) {
-        const float pz = fast_exp2(fmaf(fz[e], kLog2e, nmz));
-        const float py = fast_exp2(fmaf(fy[e], kLog2e, nmy));
-        const float d = fz[e] - fy[e];
-        // tail elements are -inf in both rows: their weight is 0 but d is
-        // NaN, so they are excluded explicitly
-        if (pz != 0.f) tr = fmaf(pz, d, tr);
-        if (py != 0.f) tf = fmaf(py, -d, tf);
-        sz += pz;
-        sy += py;
-      }
-      s.mz = mnz; s.sz = sz; s.tr = tr;
-      s.my = mny; s.sy = sy; s.tf = tf;
+    for (int e = 0; e < EPV; ++e) {
+      const float pz = fast_exp2(fmaf(fz[e], kLog2e, nmz));
+      const float py = fast_exp2(fmaf(fy[e], kLog2e, nmy));
+      const float d = fz[e] - fy[e];
+      // an element that is -inf in both rows has weight 0 but d = NaN: the
+      // legacy multiply gives 0 * d = 0
+      tr += mul_zero_safe(pz, d);
+      tf -= mul_zero_safe(py, d);
+      sz += pz;
+      sy += py;
     }
+    s.mz = mnz; s.sz = sz; s.tr = tr;
+    s.my = mny; s.sy = sy; s.tf = tf;
   }
 }
 

@@ -82,7 +82,10 @@ __device__ __forceinline__ void dense_grad(const typename TI::Vec& xz, const typ
       const float q = fast_exp2(fmaf(fy[e], kLog2e, k.nLy));
       g[e] = NEG ? q - p : p - q;
     } else {
-      g[e] = NEG ? p * ((fy[e] - fz[e]) + k.ez) : p * ((fz[e] - fy[e]) - k.ez);
+      // p = 0 where both rows are -inf and the difference is NaN: the legacy
+      // multiply keeps that entry 0 (a term of zero weight is zero)
+      g[e] = NEG ? mul_zero_safe(p, (fy[e] - fz[e]) + k.ez)
+                 : mul_zero_safe(p, (fz[e] - fy[e]) - k.ez);
     }
   }
 }

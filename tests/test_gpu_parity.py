@@ -286,6 +286,58 @@ def test_validate_cache_counts_each_violation():
                               behav_logp=to_dev(beta)) == 3
 
 
+def _store(a: np.ndarray, dtype: int) -> np.ndarray:
+    """float32 rows in the stored format of dtype (bf16: RNE bits)."""
+    if dtype == synth.F32:
+        return np.ascontiguousarray(a, np.float32)
+    t = torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(torch.bfloat16)
+    return t.view(torch.int16).numpy().view(np.uint16).copy()
+
+
+def _wide_range_rows(V: int, seed: int, est: str):
+    """Dense-estimator rows whose maxima arrive late and far above the early
+    values: rising and falling ramps over +-60, spikes of +40 to +50 near the
+    end of the row, leading -inf blocks of different lengths (the one of the
+    distribution that weights the KL's terms is the longer, so the KL stays
+    finite), and a row that is -inf but for its last two entries."""
+    rng = np.random.default_rng(seed)
+    ramp = np.linspace(-60.0, 60.0, V)
+    z = np.empty((5, V)); y = np.empty((5, V))
+    z[0], y[0] = ramp, ramp[::-1] + 0.3 * rng.standard_normal(V)
+    z[1], y[1] = ramp[::-1], ramp + 0.3 * rng.standard_normal(V)
+    z[2], y[2] = rng.standard_normal(V), rng.standard_normal(V)
+    z[2, [V - 7, V - 1000, V // 2 + 3]] = [45.0, 40.0, 41.0]
+    y[2, [V - 5, V // 3]] = [50.0, 44.0]
+    z[3], y[3] = 2.0 * rng.standard_normal(V), 2.0 * rng.standard_normal(V)
+    long, short = (11 * V) // 20, (7 * V) // 20
+    z[3, :long if est == "rkl_dense" else short] = -np.inf
+    y[3, :short if est == "rkl_dense" else long] = -np.inf
+    z[4], y[4] = -np.inf, -np.inf
+    z[4, -2:], y[4, -2:] = [3.0, 1.0], [0.5, 2.5]
+    return z, y
+
+
+@pytest.mark.parametrize("est", DENSE)
+@pytest.mark.parametrize("dtype,V", [(synth.BF16, 151936), (synth.BF16, 65536),
+                                     (synth.F32, 50000), (synth.F32, 32768)],
+                         ids=["bf16-large", "bf16-small", "f32-large", "f32-small"])
+def test_dense_rows_with_late_and_far_maxima(dtype, V, est):
+    """The register-resident dense kernel keeps per-lane offsets that it raises
+    only when a value exceeds them by a wide margin; these rows force raises in
+    late slots, whole waves that never see a finite value, and large gaps
+    between the two rows' maxima."""
+    z, y = _wide_range_rows(V, V + dtype, est)
+    zs, ys = _store(z, dtype), _store(y, dtype)
+    say("wide-range %s V=%d %s" % ("bf16" if dtype else "f32", V, est))
+    ref = oracle.rows(est, oracle_dtype(dtype), zs, V, teacher_logits=ys, gamma=0.5)
+    assert np.isfinite(ref["loss"]).all()
+    w = synth.Workload("t_wide", N=5, V=V, dtype=dtype, estimators=(est,), dense_teacher=True)
+    for path, flags in PATHS.items():
+        out = run_gpu(to_dev(zs), est, None, None, None, to_dev(ys), flags=flags, grad_scale=0.5,
+                      want_lse=True)
+        compare("wide/%d/%s/%s" % (V, est, path), w, {}, est, out, ref)
+
+
 def test_nan_logits_propagate_to_their_row_only():
     w, d, _ = small_inputs("v1000", synth.F32)
     logits = d["logits"].copy()

@@ -53,6 +53,48 @@ def test_dense_kl_matches_scipy_entropy(seed):
     assert lse == pytest.approx(logsumexp(z), rel=1e-14)
 
 
+@pytest.mark.parametrize("est", ["fkl_dense", "rkl_dense"])
+@pytest.mark.parametrize("seed", range(3))
+def test_dense_kl_actions_at_minus_inf_in_both_rows_drop_out(est, seed):
+    """A term of zero weight is zero (the KL divergence's 0 log(0/x) = 0): an
+    action whose logit is -inf for both student and teacher contributes
+    nothing, so the row equals the row with those actions removed, and their
+    gradient entries are 0."""
+    rng = np.random.default_rng(200 + seed)
+    V = 29
+    z, y = rand_logits(rng, V), rand_logits(rng, V)
+    gone = rng.choice(V, size=9, replace=False)
+    keep = np.setdiff1d(np.arange(V), gone)
+    z[gone] = -np.inf
+    y[gone] = -np.inf
+    loss, g, lse, _ = oracle.row(est, z, y=y, gamma=0.5)
+    loss_r, g_r, lse_r, _ = oracle.row(est, z[keep], y=y[keep], gamma=0.5)
+    assert np.isfinite(loss) and loss == pytest.approx(loss_r, rel=1e-13, abs=1e-15)
+    assert lse == pytest.approx(lse_r, rel=1e-14)
+    assert np.all(g[gone] == 0.0)
+    np.testing.assert_allclose(g[keep], g_r, rtol=1e-12, atol=1e-15)
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_dense_kl_with_zero_weights_matches_scipy_entropy(seed):
+    """Actions that only the weighting distribution excludes (student -inf
+    where the teacher is finite, for D_R; the reverse for D_F): scipy's
+    entropy applies the same 0 log(0/x) = 0 convention."""
+    rng = np.random.default_rng(300 + seed)
+    V = 31
+    z, y = rand_logits(rng, V), rand_logits(rng, V)
+    zr = z.copy()
+    zr[rng.choice(V, size=8, replace=False)] = -np.inf
+    lr, gr, _, _ = oracle.row("rkl_dense", zr, y=y)
+    assert lr == pytest.approx(entropy(softmax(zr), softmax(y)), rel=1e-12, abs=1e-14)
+    assert np.all(gr[np.isneginf(zr)] == 0.0) and np.isfinite(gr).all()
+    yf = y.copy()
+    yf[rng.choice(V, size=8, replace=False)] = -np.inf
+    lf, gf, _, _ = oracle.row("fkl_dense", z, y=yf)
+    assert lf == pytest.approx(entropy(softmax(yf), softmax(z)), rel=1e-12, abs=1e-14)
+    np.testing.assert_allclose(gf, softmax(z) - softmax(yf), rtol=1e-12, atol=1e-15)
+
+
 # ---------------------------------------------------------------- finite differences
 
 
