@@ -59,6 +59,11 @@ def lib():
                                   ctypes.c_int]
         L.oracle_rows.restype = ctypes.c_int
         L.oracle_max_threads.restype = ctypes.c_int
+        L.oracle_support_coverage.argtypes = [P, i64, P, P, ctypes.c_int, P, P]
+        L.oracle_support_coverage.restype = ctypes.c_int
+        L.oracle_coverage_rows.argtypes = [ctypes.c_int, P, i64, i64, i64, P, P, ctypes.c_int, P,
+                                           P, ctypes.c_int]
+        L.oracle_coverage_rows.restype = ctypes.c_int
         L.oracle_cdf.argtypes = [P, i64, P]
         L.oracle_cdf.restype = ctypes.c_int
         L.oracle_sample_row.argtypes = [P, i64, P, ctypes.c_int, P, P, P]
@@ -131,6 +136,35 @@ def rows(est: str, dtype: int, logits: np.ndarray, V: int, *, ids=None, tau=None
     if rc != 0:
         raise ValueError("oracle_rows rejected its arguments (%d)" % rc)
     return out
+
+
+def support_coverage(z, ids, tau):
+    """(Z_p^S, Z_q^S) of one row in double: the student's and the teacher's
+    mass on the cached support (App. A.1's restricted normalisers)."""
+    z = np.ascontiguousarray(z, np.float64)
+    ids = np.ascontiguousarray(ids, np.int32)
+    tau = np.ascontiguousarray(tau, np.float64)
+    zp, zq = np.zeros(1), np.zeros(1)
+    if lib().oracle_support_coverage(_p(z), z.size, _p(ids), _p(tau), ids.size, _p(zp),
+                                     _p(zq)) != 0:
+        raise ValueError("oracle_support_coverage rejected its arguments")
+    return float(zp[0]), float(zq[0])
+
+
+def coverage_rows(dtype: int, logits: np.ndarray, V: int, ids, tau, mask=None,
+                  nthreads: int = 0) -> np.ndarray:
+    """[n, 2] (Z_p^S, Z_q^S) of stored rows (zeros for masked rows)."""
+    logits = np.ascontiguousarray(logits)
+    n, ld = logits.shape
+    ids = np.ascontiguousarray(ids, np.int32)
+    tau = np.ascontiguousarray(tau, np.float32)
+    mask = None if mask is None else np.ascontiguousarray(mask, np.uint8)
+    cov = np.zeros((n, 2), np.float64)
+    rc = lib().oracle_coverage_rows(dtype, _p(logits), n, V, ld, _p(ids), _p(tau), ids.shape[1],
+                                    _p(mask), _p(cov), nthreads)
+    if rc != 0:
+        raise ValueError("oracle_coverage_rows rejected its arguments (%d)" % rc)
+    return cov
 
 
 def max_threads() -> int:

@@ -293,6 +293,32 @@ int oracle_row(int est, const double* z, const double* y, int64_t V, const int32
   return 0;
 }
 
+/*
+ * Support coverage: the restricted normalisers of App. A.1 on the cached
+ * support S = {a_i},
+ *   Z_p^S = sum_{u in S} p_theta(u|s),     Z_q^S = sum_{u in S} q(u|s),
+ * the share of the student's and of the teacher's mass that S holds.  A
+ * stale support (Sec. 6, sparse top-k under rollout reuse) shows up as a
+ * student coverage that falls away from the teacher's.  q at a cached action
+ * is the cached full-vocabulary teacher probability exp(tau_i).  Each cached
+ * entry counts once (the support's ids are distinct by precondition).
+ */
+int oracle_support_coverage(const double* z, int64_t V, const int32_t* ids, const double* tau,
+                            int K, double* zp, double* zq) {
+  if (!z || !ids || !tau || !zp || !zq || V < 1 || K < 1) return -1;
+  for (int i = 0; i < K; ++i)
+    if (ids[i] < 0 || ids[i] >= V) return -1;
+  const double L = log_partition(z, V);
+  double sp = 0.0, sq = 0.0;
+  for (int i = 0; i < K; ++i) {
+    sp += exp(z[ids[i]] - L);
+    sq += exp(tau[i]);
+  }
+  *zp = sp;
+  *zq = sq;
+  return 0;
+}
+
 /* Exact widening of one stored logit to double. */
 static double widen(int dtype, const void* base, int64_t off) {
   if (dtype == ORACLE_BF16) {
@@ -363,6 +389,49 @@ int oracle_rows(int est, int dtype, const void* logits, const void* teacher_logi
     free(y);
     free(t);
     free(b);
+  }
+  return err;
+}
+
+/* Support coverage of stored rows: cov[2 r] = Z_p^S, cov[2 r + 1] = Z_q^S
+ * (0 and 0 for a masked row). */
+int oracle_coverage_rows(int dtype, const void* logits, int64_t n_rows, int64_t V, int64_t ld,
+                         const int32_t* ids, const float* tau, int K, const uint8_t* mask,
+                         double* cov, int nthreads) {
+  if (!logits || !ids || !tau || !cov || n_rows < 0 || V < 1 || ld < V || K < 1) return -1;
+  if (dtype != ORACLE_F32 && dtype != ORACLE_BF16) return -1;
+  int err = 0;
+  if (nthreads <= 0) nthreads = oracle_max_threads();
+#ifdef _OPENMP
+#pragma omp parallel num_threads(nthreads)
+#endif
+  {
+    double* z = (double*)malloc(sizeof(double) * (size_t)V);
+    double* t = (double*)malloc(sizeof(double) * (size_t)K);
+    if (!z || !t) {
+#ifdef _OPENMP
+#pragma omp atomic write
+#endif
+      err = -2;
+    } else {
+#ifdef _OPENMP
+#pragma omp for schedule(dynamic, 1)
+#endif
+      for (int64_t r = 0; r < n_rows; ++r) {
+        cov[2 * r] = cov[2 * r + 1] = 0.0;
+        if (mask && mask[r] == 0) continue;
+        for (int64_t j = 0; j < V; ++j) z[j] = widen(dtype, logits, r * ld + j);
+        for (int i = 0; i < K; ++i) t[i] = (double)tau[r * K + i];
+        if (oracle_support_coverage(z, V, ids + r * K, t, K, cov + 2 * r, cov + 2 * r + 1)) {
+#ifdef _OPENMP
+#pragma omp atomic write
+#endif
+          err = -1;
+        }
+      }
+    }
+    free(z);
+    free(t);
   }
   return err;
 }

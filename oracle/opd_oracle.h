@@ -53,6 +53,15 @@ int oracle_rows(int est, int dtype, const void* logits, const void* teacher_logi
                 int K, const uint8_t* mask, double gamma, double eps, double* loss, double* grad,
                 double* lse, double* gathered, int nthreads);
 
+/* Support coverage (App. A.1's restricted normalisers): Z_p^S = sum over the
+ * cached support of p_theta, Z_q^S = sum of exp(tau_i).  The batch form
+ * writes [n_rows, 2] (Z_p^S, Z_q^S), zeros for masked rows. */
+int oracle_support_coverage(const double* z, int64_t V, const int32_t* ids, const double* tau,
+                            int K, double* zp, double* zq);
+int oracle_coverage_rows(int dtype, const void* logits, int64_t n_rows, int64_t V, int64_t ld,
+                         const int32_t* ids, const float* tau, int K, const uint8_t* mask,
+                         double* cov, int nthreads);
+
 /* Building the cache (Sec. 4.1, Stages 1 and 2).  Rows in double unless
  * stored.  See opd_oracle.c for the definitions.
  *   oracle_cdf         F[j] = sum_{l<=j} softmax(z)_l, summed in index order
