@@ -12,12 +12,20 @@ Prints one JSON line on stdout:
   roofline    HBM roofline of the loss kernel: algorithmic bytes per launch
               (one read of the logits, one write of the gradient, the cache)
               over the mean launch time measured with HIP events on the
-              launch stream, against the 8 TB/s MI355X peak
-  two_read_model  the same launch priced with a second read of each row for
-              the estimators whose gradient is dense (MC, truncated top-k,
-              dense): the bytes a kernel that re-reads the row would move
+              launch stream, against the 8 TB/s MI355X peak; also the same
+              rate as a fraction of a plain device copy measured in the same
+              process (frac_of_copy)
+  accounting_model  the launch priced with a second read of each row for the
+              estimators whose gradient is dense (MC, truncated top-k,
+              dense), as a two-read/one-write accounting counts it.  The
+              kernels hold the row on chip and do not move those bytes, so
+              this is bookkeeping, not a bandwidth figure
   cpu_baseline  the oracle on a bounded sample of the same workload, on the
-              host cores
+              host cores, plus a one-thread figure on 1,024 rows
+Working sets under 1 GiB (which the 256 MB Infinity Cache could partly hold
+between steps) are rotated over several copies of the inputs and outputs, so
+consecutive steps read and write different memory; config.buffer_sets says how
+many.
 
 --op sample|topk|score times one of the cache-building calls instead (Stage
 1 draws with their log-probs, the top-k support, or scoring at cached ids)
@@ -145,6 +153,20 @@ def cpu_diag_baseline(w, d, lse, gathered, seq):
                       "%.2f s wall on 1 thread" % (w.N, el)}
 
 
+def dominant_kernels(op: str, est: str, w, split: bool):
+    """Names of the kernels a launch runs (as rocprofv3 lists them)."""
+    if op == "loss":
+        if split:
+            return ["k_split_stats", "k_split_write"]
+        if est in ("fkl_topk", "rkl_topk"):
+            return ["k_fill_zero", "k_topk_sparse"]
+        if est in ("fkl_dense", "rkl_dense"):
+            return ["k_row_dense_resident"]
+        return ["k_row_resident"]
+    return {"sample": ["k_sample_stream"], "topk": ["k_topk_stream", "k_topk"],
+            "score": ["k_score"], "diag": ["k_diag_*"]}[op]
+
+
 def read_traffic(est_key: str, op: str):
     """Measured HBM bytes per launch from the committed counter summary, if it
     was taken on the current sources of the op's kernels."""
@@ -157,6 +179,34 @@ def read_traffic(est_key: str, op: str):
     if e is None or e.get("kernel_hash") != kernel_hash(op):
         return None
     return e.get("bytes_per_launch")
+
+
+def single_thread_baseline(w, est, d, rows: int = 1024):
+    """The oracle on one thread over the first `rows` rows."""
+    r = cpu_baseline(w, est, d, rows, 1)
+    return {"value": r["value"], "unit": "tokens/s", "rows": min(rows, w.N), "threads": 1}
+
+
+def copy_peak(dev, stream, mib: int = 2048):
+    """GB/s of a plain device-to-device copy of `mib` MiB (read + write bytes)."""
+    import torch
+
+    n = mib * (1 << 20) // 4
+    a = torch.ones(n, dtype=torch.float32, device=dev)
+    b = torch.empty_like(a)
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(10):
+        b.copy_(a)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    gbs = 2 * n * 4 * 10 / (e0.elapsed_time(e1) / 1e3) / 1e9
+    del a, b
+    torch.cuda.empty_cache()
+    return gbs
 
 
 def cpu_baseline(w, est, d, rows: int, threads: int, chunk: int = 512):
@@ -204,8 +254,10 @@ def main():
     ap.add_argument("--cpu-rows", type=int, default=0, help="0 = every row")
     ap.add_argument("--cpu-threads", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--calib-copy", type=int, default=0,
-                    help="also time a plain device copy of this many MiB (counter calibration)")
+    ap.add_argument("--copy-mib", type=int, default=2048,
+                    help="size of the plain device copy timed for frac_of_copy (0: skip)")
+    ap.add_argument("--min-set-gib", type=float, default=1.0,
+                    help="rotate input/output copies until the timed steps span this many GiB")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -243,31 +295,52 @@ def main():
             return torch.from_numpy(a.view(np.int16)).to(dev).view(torch.bfloat16)
         return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
 
-    logits = dev_t(d["logits"])
-    kw = {}
-    if est in SUPPORT:
-        kw = dict(idx=dev_t(d["topk_idx"]), teacher_logp=dev_t(d["topk_tau"]))
-    elif est.startswith("rkl_mc"):
-        m = 1 if est == "rkl_mc1" else w.M
-        kw = dict(sampled_ids=dev_t(d["mc_ids"][:, :m]), teacher_logp=dev_t(d["mc_tau"][:, :m]),
-                  behav_logp=dev_t(d["mc_beta"][:, :m]))
-    else:
-        kw = dict(teacher_logits=dev_t(d["teacher_logits"]))
     mask_np = d["mask"]
     mask = dev_t(mask_np) if w.ragged else None
     n_valid = int(mask_np.sum())
     N = w.N
-    out = {"loss": torch.empty(N, dtype=torch.float32, device=dev),
-           "dlogits": torch.empty((N, w.V), dtype=torch.float32, device=dev)}
-    nbytes = opd.workspace_bytes(N, w.V, w.dtype, est, w.k, w.M)
-    ws = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev) if nbytes else None
+    in_b = 2 if w.dtype == 1 else 4
     stream = torch.cuda.current_stream()
+    copy_gbs = copy_peak(dev, stream, args.copy_mib) if args.copy_mib else None
+
+    def loss_inputs():
+        kw = {}
+        if est in SUPPORT:
+            kw = dict(idx=dev_t(d["topk_idx"]), teacher_logp=dev_t(d["topk_tau"]))
+        elif est.startswith("rkl_mc"):
+            m = 1 if est == "rkl_mc1" else w.M
+            kw = dict(sampled_ids=dev_t(d["mc_ids"][:, :m]),
+                      teacher_logp=dev_t(d["mc_tau"][:, :m]),
+                      behav_logp=dev_t(d["mc_beta"][:, :m]))
+        else:
+            kw = dict(teacher_logits=dev_t(d["teacher_logits"]))
+        return kw
+
+    logits = dev_t(d["logits"])
+    kw = loss_inputs()
     u_np = None
+    sets = 1
     if op == "loss":
+        # one buffer set: logits (and teacher logits), cache, loss and gradient
+        set_bytes = N * w.V * (in_b * (2 if "teacher_logits" in kw else 1) + 4)
+        sets = max(1, -(-int(args.min_set_gib * (1 << 30)) // set_bytes))
+        bufs = []
+        for i in range(sets):
+            bufs.append({"logits": logits if i == 0 else logits.clone(),
+                         "kw": kw if i == 0 else {k: v.clone() for k, v in kw.items()},
+                         "out": {"loss": torch.empty(N, dtype=torch.float32, device=dev),
+                                 "dlogits": torch.empty((N, w.V), dtype=torch.float32,
+                                                        device=dev)}})
+        nbytes = opd.workspace_bytes(N, w.V, w.dtype, est, w.k, w.M)
+        ws = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev) if nbytes else None
+        counter = [0]
+
         def step():
-            opd.loss_fwd_bwd(logits, est, mask=mask, out=out, workspace=ws, stream=stream, **kw)
+            b = bufs[counter[0] % sets]
+            counter[0] += 1
+            opd.loss_fwd_bwd(b["logits"], est, mask=mask, out=b["out"], workspace=ws,
+                             stream=stream, **b["kw"])
     else:
-        del out
         if op == "sample":
             u_np = np.stack([synth.uniforms(w.seed + 1, synth.STREAM_SAMPLE, r, w.M)
                              for r in range(N)])
@@ -295,6 +368,7 @@ def main():
 
             def step():
                 opd.score_actions(logits, ids_dev, mask=mask, stream=stream)
+        nbytes = 0
 
     for _ in range(args.warmup):
         step()
@@ -343,7 +417,8 @@ def main():
                    "tokens": N, "valid_tokens": n_valid,
                    "vocab": w.V, "logits_dtype": "bf16" if w.dtype == 1 else "f32",
                    "dlogits_dtype": "f32", "k": w.k, "M": w.M,
-                   "path": "split" if nbytes and op == "loss" else "rowwise"},
+                   "path": "split" if nbytes and op == "loss" else "rowwise",
+                   "buffer_sets": sets},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": achieved / PEAK_HBM_GBS,
                      "traffic": traffic,
@@ -352,33 +427,24 @@ def main():
                      "min_launch_ms": min(launch_ms)},
     }
     res["roofline"]["median_launch_ms"] = sorted(launch_ms)[len(launch_ms) // 2]
+    res["roofline"]["kernels"] = dominant_kernels(op, est, w, nbytes > 0)
+    if copy_gbs:
+        res["roofline"]["copy_GBps"] = copy_gbs
+        res["roofline"]["frac_of_copy"] = achieved / copy_gbs
     if op == "loss":
         model = alg + second_read_bytes(w, est, n_valid)
-        res["two_read_model"] = {"bytes_per_launch": model,
-                                 "GBps": model / mean_launch_s / 1e9,
-                                 "frac": model / mean_launch_s / 1e9 / PEAK_HBM_GBS}
-    if args.calib_copy:
-        n = args.calib_copy * (1 << 20) // 4
-        a = torch.ones(n, dtype=torch.float32, device=dev)
-        b = torch.empty_like(a)
-        for _ in range(3):
-            b.copy_(a)
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        for _ in range(10):
-            b.copy_(a)
-        e1.record(stream)
-        torch.cuda.synchronize()
-        copy_gbs = 2 * n * 4 * 10 / (e0.elapsed_time(e1) / 1e3) / 1e9
-        res["copy_calibration"] = {"bytes_per_copy": 2 * n * 4, "GBps": copy_gbs,
-                                   "frac_of_copy": achieved / copy_gbs}
+        res["accounting_model"] = {
+            "bytes_per_launch": model, "GBps": model / mean_launch_s / 1e9,
+            "frac": model / mean_launch_s / 1e9 / PEAK_HBM_GBS,
+            "note": "prices a second read of each row that the kernel does not perform "
+                    "(the row is held in registers); bookkeeping, not achieved bandwidth"}
     if not args.no_cpu_baseline:
         del logits
         torch.cuda.empty_cache()
         log("timing the oracle ...")
         if op == "loss":
             res["cpu_baseline"] = cpu_baseline(w, est, d, args.cpu_rows, args.cpu_threads)
+            res["cpu_baseline"]["single_thread"] = single_thread_baseline(w, est, d)
         elif op == "diag":
             res["cpu_baseline"] = cpu_diag_baseline(w, d, lse_dev.cpu().numpy(),
                                                     gat_dev.cpu().numpy(), seq)

@@ -23,6 +23,8 @@
  *    [0, V), NaN or infinite logits) never fault the device: an out-of-range
  *    id makes that row's loss NaN and fills its dlogits row with NaN, and
  *    NaN/Inf logits propagate into that row's outputs.
+ *  - N may be as large as INT32_MAX: calls whose grid would exceed HIP's
+ *    limit of 2^32 work-items launch over consecutive row chunks.
  *  - Results are deterministic: repeated calls with the same inputs produce
  *    bitwise-identical outputs (fixed-order reductions, no float atomics).
  *  - Entry points hold no mutable global state and are safe to call from
@@ -38,7 +40,7 @@
 extern "C" {
 #endif
 
-#define OPD_VERSION 4
+#define OPD_VERSION 5
 /* Largest cached support size k, and largest sample count M. */
 #define OPD_K_MAX 256
 
@@ -53,7 +55,8 @@ typedef enum opd_status {
   OPD_ERR_ESTIMATOR = -7, /* unknown estimator */
   OPD_ERR_FLAGS = -8,     /* unknown or contradictory flag bits */
   OPD_ERR_HIP = -9,       /* a HIP runtime call or kernel launch failed */
-  OPD_ERR_PARAM = -10     /* invalid scalar option (clip_eps of a clipped estimator) */
+  OPD_ERR_PARAM = -10     /* invalid scalar option (clip_eps of a clipped estimator), or
+                             coverage_out for an estimator without a cached support */
 } opd_status;
 
 /*
@@ -201,6 +204,16 @@ typedef struct opd_opts {
  *                 estimators, requesting it adds one read of the logits.
  *   gathered_out  [N, k or M] fp32 student logits at the cached ids (exact
  *                 widening), nullable; not produced by the dense estimators.
+ *   coverage_out  [N, 2] fp32 support coverage, nullable: the restricted
+ *                 normalisers of App. A.1 on the cached support S,
+ *                 Z_p^S = sum_{a in S} p_theta(a|s) (the student's mass on S)
+ *                 and Z_q^S = sum_i exp(teacher_logp[t, i]) (the teacher's),
+ *                 each cached entry counted once; 0 and 0 for a masked token.
+ *                 A stale support (Sec. 6) shows as Z_p^S falling away from
+ *                 Z_q^S.  Only the estimators that read a support (the
+ *                 renormalised and truncated top-k) take it (else
+ *                 OPD_ERR_PARAM); for the renormalised ones it adds one read
+ *                 of the logits, as lse_out does.
  *   workspace     device scratch for the split-vocabulary path, nullable;
  *   workspace_bytes  its size.  The split path is taken for small N (or when
  *                 forced) only if workspace_bytes >= opd_workspace_bytes(...);
@@ -211,7 +224,7 @@ typedef struct opd_opts {
 int opd_loss_fwd_bwd(const void* logits, int32_t dtype, int64_t N, int64_t V, int64_t ld,
                      const opd_cache* cache, int32_t estimator, int32_t k, int32_t M,
                      const uint8_t* mask, const opd_opts* opts, float* loss, void* dlogits,
-                     float* lse_out, float* gathered_out, void* workspace,
+                     float* lse_out, float* gathered_out, float* coverage_out, void* workspace,
                      size_t workspace_bytes, void* stream);
 
 /*
@@ -315,7 +328,8 @@ int opd_score_actions(const void* logits, int32_t dtype, int64_t N, int64_t V, i
  * outputs.  The workspace (size from opd_mc_diag_workspace_bytes, 16-byte
  * aligned) holds intermediates; the quantile is exact (radix selection with
  * integer histograms); sums run in a fixed order.
- * Errors: OPD_ERR_SHAPE (N), OPD_ERR_SUPPORT (M outside [1, OPD_K_MAX]),
+ * Errors: OPD_ERR_SHAPE (N < 0 or N >= 2^32 / 64: the batch reductions run
+ * in one grid), OPD_ERR_SUPPORT (M outside [1, OPD_K_MAX]),
  * OPD_ERR_PARAM (quantile outside (0, 1], clip_eps negative or not finite,
  * more than 8 or invalid group sizes, seq_len < 0, ratio_seq without
  * seq_len), OPD_ERR_NULL, OPD_ERR_WORKSPACE, OPD_ERR_HIP.

@@ -77,7 +77,7 @@ def lib():
         L = ctypes.CDLL(LIB_PATH)
         P, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
         L.opd_loss_fwd_bwd.argtypes = [P, i32, i64, i64, i64, ctypes.POINTER(OpdCache), i32, i32,
-                                       i32, P, ctypes.POINTER(OpdOpts), P, P, P, P, P,
+                                       i32, P, ctypes.POINTER(OpdOpts), P, P, P, P, P, P,
                                        ctypes.c_size_t, P]
         L.opd_loss_fwd_bwd.restype = ctypes.c_int
         L.opd_workspace_bytes.argtypes = [i64, i64, i32, i32, i32, i32, ctypes.c_uint32]
@@ -130,8 +130,49 @@ def _stream(stream) -> ctypes.c_void_p:
 
 
 def _rowmajor(t: torch.Tensor, name: str):
-    if t.dim() != 2 or t.stride(1) != 1:
+    if not isinstance(t, torch.Tensor) or t.dim() != 2 or t.stride(1) != 1:
         raise ValueError("%s must be a 2-D tensor with unit column stride" % name)
+
+
+def _need(t, name: str, dtypes, shape, device=None):
+    """t must be a contiguous tensor of one of `dtypes` with exactly `shape`
+    (and, when given, on `device`): the library reads and writes it as a dense
+    row-major array of that element type."""
+    if not isinstance(t, torch.Tensor):
+        raise ValueError("%s must be a torch tensor" % name)
+    if t.dtype not in dtypes:
+        raise ValueError("%s must have dtype %s, got %s" %
+                         (name, " or ".join(str(d) for d in dtypes), t.dtype))
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError("%s must have shape %s, got %s" % (name, tuple(shape), tuple(t.shape)))
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    if device is not None and t.device != device:
+        raise ValueError("%s is on %s, the logits on %s" % (name, t.device, device))
+
+
+def _need_rows(t, name: str, dtype, N: int, V: int, ld: int, device=None):
+    """t must be an [N, >= V] tensor of `dtype` whose rows lie `ld` elements
+    apart with unit column stride: the library addresses row r at r * ld."""
+    if not isinstance(t, torch.Tensor):
+        raise ValueError("%s must be a torch tensor" % name)
+    if t.dtype != dtype:
+        raise ValueError("%s must have dtype %s, got %s" % (name, dtype, t.dtype))
+    if t.dim() != 2 or t.shape[0] != N or t.shape[1] < V:
+        raise ValueError("%s must have shape [%d, >= %d], got %s" % (name, N, V, tuple(t.shape)))
+    if N > 0 and (t.stride(1) != 1 or (N > 1 and t.stride(0) != ld)):
+        raise ValueError("%s must have row stride %d and unit column stride, got strides %s" %
+                         (name, ld, tuple(t.stride())))
+    if device is not None and t.device != device:
+        raise ValueError("%s is on %s, the logits on %s" % (name, t.device, device))
+
+
+_MASK_DTYPES = (torch.uint8, torch.bool)
+
+
+def _need_gpu(t: torch.Tensor, name: str):
+    if not t.is_cuda:
+        raise ValueError("%s must be a GPU tensor (the library runs HIP kernels only)" % name)
 
 
 def workspace_bytes(N: int, V: int, dtype: int, estimator: str, k: int = 0, M: int = 0,
@@ -143,47 +184,82 @@ def loss_fwd_bwd(logits: torch.Tensor, estimator: str, *, idx=None, sampled_ids=
                  teacher_logp=None, behav_logp=None, teacher_logits=None, mask=None,
                  grad_scale: float = 1.0, dlogits_dtype=torch.float32, flags: int = 0,
                  clip_eps: float = 0.2, want_lse: bool = False, want_gathered: bool = False,
-                 workspace=None, out=None, stream=None):
+                 want_coverage: bool = False, workspace=None, out=None, stream=None):
     """One fused forward+backward call of opd_loss_fwd_bwd.
 
     logits: [N, V] device tensor (a row-strided view of an [N, ld] buffer is
     fine).  Cache tensors are [N, k] / [N, M] device tensors.  Returns a dict
     with "loss" [N], "dlogits" [N, V] (a view of the [N, ld] buffer), and
-    "lse" / "gathered" when requested.  `workspace=None` allocates what the
+    "lse" / "gathered" / "coverage" ([N, 2]: Z_p^S, Z_q^S; estimators with a
+    cached support only) when requested.  `workspace=None` allocates what the
     split path needs; pass a tensor to supply your own (or an empty one to
     force the row-per-workgroup path).  `out` may hold preallocated "loss"
     and "dlogits" ([N, ld]) tensors.
     """
+    if estimator not in ESTIMATORS:
+        raise ValueError("unknown estimator %r" % (estimator,))
     est = ESTIMATORS[estimator]
     _rowmajor(logits, "logits")
     N, V = logits.shape
     ld = logits.stride(0) if N > 1 else V
     dev = logits.device
     dt = _dt(logits)
+    if dlogits_dtype not in (torch.float32, torch.bfloat16):
+        raise ValueError("dlogits_dtype must be torch.float32 or torch.bfloat16")
     odt = {torch.float32: F32, torch.bfloat16: BF16}[dlogits_dtype]
-    k = int(idx.shape[1]) if idx is not None else 0
-    M = int(sampled_ids.shape[1]) if sampled_ids is not None else 0
-    if teacher_logits is not None:
-        _rowmajor(teacher_logits, "teacher_logits")
-    cache = OpdCache(_ptr(idx), _ptr(sampled_ids), _ptr(teacher_logp), _ptr(behav_logp),
-                     _ptr(teacher_logits))
-    opts = OpdOpts(grad_scale, odt, flags, clip_eps)
+    ids = idx if estimator in TOPK else sampled_ids
+    if estimator in DENSE:
+        if teacher_logits is None:
+            raise ValueError("%s needs teacher_logits" % estimator)
+        _need_rows(teacher_logits, "teacher_logits", logits.dtype, N, V, ld, dev)
+    else:
+        if ids is None or teacher_logp is None:
+            raise ValueError("%s needs %s and teacher_logp" %
+                             (estimator, "idx" if estimator in TOPK else "sampled_ids"))
+        if ids.dim() != 2:
+            raise ValueError("%s must be a 2-D [N, K] tensor" %
+                             ("idx" if estimator in TOPK else "sampled_ids"))
+        K = int(ids.shape[1])
+        _need(ids, "idx" if estimator in TOPK else "sampled_ids", (torch.int32,), (N, K), dev)
+        _need(teacher_logp, "teacher_logp", (torch.float32,), (N, K), dev)
+        if behav_logp is not None:
+            _need(behav_logp, "behav_logp", (torch.float32,), (N, K), dev)
+    k = int(idx.shape[1]) if estimator in TOPK else 0
+    M = int(sampled_ids.shape[1]) if ids is not None and estimator not in TOPK else 0
+    if mask is not None:
+        _need(mask, "mask", _MASK_DTYPES, (N,), dev)
+    if workspace is not None:
+        _need(workspace, "workspace", (torch.uint8,), (workspace.numel(),), dev)
     if out is not None:
         loss, dbuf = out["loss"], out["dlogits"]
+        _need(loss, "out['loss']", (torch.float32,), (N,), dev)
+        _need_rows(dbuf, "out['dlogits']", dlogits_dtype, N, V, ld, dev)
     else:
+        loss = dbuf = None
+    _need_gpu(logits, "logits")
+    cache = OpdCache(_ptr(idx) if estimator in TOPK else None,
+                     _ptr(sampled_ids) if estimator not in TOPK and estimator not in DENSE else None,
+                     _ptr(teacher_logp), _ptr(behav_logp), _ptr(teacher_logits))
+    opts = OpdOpts(grad_scale, odt, flags, clip_eps)
+    if out is None:
         loss = torch.empty(N, dtype=torch.float32, device=dev)
         dbuf = torch.empty((N, ld), dtype=dlogits_dtype, device=dev)
     lse = torch.empty(N, dtype=torch.float32, device=dev) if want_lse else None
     K = k if estimator in TOPK else M
     gathered = (torch.empty((N, max(K, 1)), dtype=torch.float32, device=dev)
                 if want_gathered and estimator not in DENSE else None)
+    if want_coverage and estimator not in TOPK:
+        raise ValueError("support coverage exists for the estimators with a cached support only")
+    coverage = torch.empty((N, 2), dtype=torch.float32, device=dev) if want_coverage else None
     if workspace is None:
         nbytes = workspace_bytes(N, V, dt, estimator, k, M, flags)
-        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev) if nbytes else None
+        workspace = (torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
+                     if nbytes else None)
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     rc = lib().opd_loss_fwd_bwd(_ptr(logits), dt, N, V, ld, ctypes.byref(cache), est, k, M,
-                                _ptr(mask), ctypes.byref(opts), _ptr(loss), _ptr(dbuf), _ptr(lse),
-                                _ptr(gathered), _ptr(workspace) if ws_bytes else None, ws_bytes,
+                                _ptr(mask), ctypes.byref(opts), _ptr(loss), _ptr(dbuf),
+                                _ptr(lse), _ptr(gathered), _ptr(coverage),
+                                _ptr(workspace) if ws_bytes else None, ws_bytes,
                                 _stream(stream))
     if rc != 0:
         raise OpdError(rc, "opd_loss_fwd_bwd")
@@ -192,6 +268,8 @@ def loss_fwd_bwd(logits: torch.Tensor, estimator: str, *, idx=None, sampled_ids=
         res["lse"] = lse
     if gathered is not None:
         res["gathered"] = gathered[:, :K]
+    if coverage is not None:
+        res["coverage"] = coverage
     return res
 
 
@@ -199,8 +277,16 @@ def validate_cache(estimator: str, V: int, *, idx=None, sampled_ids=None, teache
                    behav_logp=None, stream=None) -> int:
     """Number of cache entries violating the estimator's preconditions (synchronises)."""
     ids = idx if idx is not None else sampled_ids
-    N, K = (0, 0) if ids is None else ids.shape
-    dev = (ids if ids is not None else teacher_logp).device
+    if not isinstance(ids, torch.Tensor) or ids.dim() != 2:
+        raise ValueError("validate_cache needs idx or sampled_ids as an [N, K] int32 tensor")
+    N, K = ids.shape
+    dev = ids.device
+    _need(ids, "idx" if idx is not None else "sampled_ids", (torch.int32,), (N, K), dev)
+    if teacher_logp is not None:
+        _need(teacher_logp, "teacher_logp", (torch.float32,), (N, K), dev)
+    if behav_logp is not None:
+        _need(behav_logp, "behav_logp", (torch.float32,), (N, K), dev)
+    _need_gpu(ids, "ids")
     counter = torch.zeros(1, dtype=torch.int32, device=dev)
     cache = OpdCache(_ptr(idx), _ptr(sampled_ids), _ptr(teacher_logp), _ptr(behav_logp), None)
     k = K if estimator in TOPK else 0
@@ -214,11 +300,14 @@ def validate_cache(estimator: str, V: int, *, idx=None, sampled_ids=None, teache
 
 # ---------------------------------------------------------------- building the cache
 
-def _row_call(logits: torch.Tensor):
+def _row_call(logits: torch.Tensor, mask=None):
     _rowmajor(logits, "logits")
     N, V = logits.shape
     ld = logits.stride(0) if N > 1 else V
-    return N, V, ld, _dt(logits)
+    dt = _dt(logits)
+    if mask is not None:
+        _need(mask, "mask", _MASK_DTYPES, (N,), logits.device)
+    return N, V, ld, dt
 
 
 def sample_actions(logits: torch.Tensor, uniforms: torch.Tensor, *, mask=None,
@@ -226,10 +315,12 @@ def sample_actions(logits: torch.Tensor, uniforms: torch.Tensor, *, mask=None,
     """M draws per row from softmax(logits) by inversion at the given uniforms
     ([N, M] float32 in [0, 1)).  Returns {"ids" [N, M] int32, "logp" [N, M]
     (log-probs at the draws), "lse" [N] when requested}."""
-    N, V, ld, dt = _row_call(logits)
-    if uniforms.dtype != torch.float32 or uniforms.dim() != 2 or not uniforms.is_contiguous():
+    N, V, ld, dt = _row_call(logits, mask)
+    if not isinstance(uniforms, torch.Tensor) or uniforms.dim() != 2:
         raise ValueError("uniforms must be a contiguous [N, M] float32 tensor")
     M = int(uniforms.shape[1])
+    _need(uniforms, "uniforms", (torch.float32,), (N, M), logits.device)
+    _need_gpu(logits, "logits")
     dev = logits.device
     ids = torch.empty((N, M), dtype=torch.int32, device=dev)
     logp = torch.empty((N, M), dtype=torch.float32, device=dev) if want_logp else None
@@ -250,7 +341,8 @@ def topk_support(logits: torch.Tensor, k: int, *, mask=None, want_logp: bool = T
                  want_lse: bool = False, stream=None) -> dict:
     """The k largest logits per row (descending, ties by lower index).  Returns
     {"idx" [N, k] int32, "logp" [N, k], "lse" [N] when requested}."""
-    N, V, ld, dt = _row_call(logits)
+    N, V, ld, dt = _row_call(logits, mask)
+    _need_gpu(logits, "logits")
     dev = logits.device
     idx = torch.empty((N, k), dtype=torch.int32, device=dev)
     logp = torch.empty((N, k), dtype=torch.float32, device=dev) if want_logp else None
@@ -270,10 +362,12 @@ def topk_support(logits: torch.Tensor, k: int, *, mask=None, want_logp: bool = T
 def score_actions(logits: torch.Tensor, ids: torch.Tensor, *, mask=None, want_lse: bool = False,
                   stream=None) -> dict:
     """log softmax(logits) at ids ([N, K] int32).  Returns {"logp" [N, K], "lse"}."""
-    N, V, ld, dt = _row_call(logits)
-    if ids.dtype != torch.int32 or ids.dim() != 2 or not ids.is_contiguous():
+    N, V, ld, dt = _row_call(logits, mask)
+    if not isinstance(ids, torch.Tensor) or ids.dim() != 2:
         raise ValueError("ids must be a contiguous [N, K] int32 tensor")
     K = int(ids.shape[1])
+    _need(ids, "ids", (torch.int32,), (N, K), logits.device)
+    _need_gpu(logits, "logits")
     dev = logits.device
     logp = torch.empty((N, K), dtype=torch.float32, device=dev)
     lse = torch.empty(N, dtype=torch.float32, device=dev) if want_lse else None
@@ -300,11 +394,17 @@ def mc_diagnostics(lse: torch.Tensor, gathered: torch.Tensor, teacher_logp: torc
     """Diagnostics of the MC estimator from an MC loss call's lse_out and
     gathered_out and the cache's teacher and behaviour log-probs (see
     opd_mc_diagnostics).  Returns the requested outputs as device tensors."""
+    if not isinstance(gathered, torch.Tensor) or gathered.dim() != 2:
+        raise ValueError("gathered must be a contiguous [N, M] float32 tensor")
     N, M = gathered.shape
+    dev = gathered.device
+    _need(lse, "lse", (torch.float32,), (N,), dev)
     for t, name in ((gathered, "gathered"), (teacher_logp, "teacher_logp"),
                     (behav_logp, "behav_logp")):
-        if t.dtype != torch.float32 or not t.is_contiguous() or tuple(t.shape) != (N, M):
-            raise ValueError("%s must be a contiguous [N, M] float32 tensor" % name)
+        _need(t, name, (torch.float32,), (N, M), dev)
+    if mask is not None:
+        _need(mask, "mask", _MASK_DTYPES, (N,), dev)
+    _need_gpu(gathered, "gathered")
     if want is None:
         want = DIAG_OUTPUTS if seq_len and len(group_sizes) else DIAG_OUTPUTS[:-1]
     gs = (ctypes.c_int32 * max(len(group_sizes), 1))(*group_sizes)

@@ -114,6 +114,58 @@ int64_t nvec_of(int64_t V, int32_t dt) {
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
+// A HIP grid holds fewer than 2^32 work-items: calls with more rows than one
+// grid takes run as consecutive launches over row chunks.
+constexpr int64_t kMaxGridLanes = 0xFFFFFFFFll;
+
+// The arguments of rows [r0, r0 + n) of a loss call: every row-indexed
+// pointer moves to row r0.
+Args loss_rows(const Args& a, int64_t r0, int64_t n, int in_bytes, int out_bytes) {
+  Args b = a;
+  b.N = n;
+  b.logits = (const char*)a.logits + r0 * a.ld * in_bytes;
+  if (a.teacher) b.teacher = (const char*)a.teacher + r0 * a.ld * in_bytes;
+  b.dlogits = (char*)a.dlogits + r0 * a.ld * out_bytes;
+  if (a.ids) b.ids = a.ids + r0 * a.K;
+  if (a.tau) b.tau = a.tau + r0 * a.K;
+  if (a.beta) b.beta = a.beta + r0 * a.K;
+  if (a.mask) b.mask = a.mask + r0;
+  b.loss = a.loss + r0;
+  if (a.lse_out) b.lse_out = a.lse_out + r0;
+  if (a.gathered_out) b.gathered_out = a.gathered_out + r0 * a.K;
+  if (a.coverage_out) b.coverage_out = a.coverage_out + 2 * r0;
+  if (a.ws) b.ws = a.ws + r0 * a.P * opd::kPartialFloats;
+  return b;
+}
+
+// The same for a cache-building call.
+opd::CacheArgs cache_rows(const opd::CacheArgs& a, int64_t r0, int64_t n, int in_bytes) {
+  opd::CacheArgs b = a;
+  b.N = n;
+  b.logits = (const char*)a.logits + r0 * a.ld * in_bytes;
+  if (a.u) b.u = a.u + r0 * a.K;
+  if (a.ids) b.ids = a.ids + r0 * a.K;
+  if (a.mask) b.mask = a.mask + r0;
+  if (a.ids_out) b.ids_out = a.ids_out + r0 * a.K;
+  if (a.logp) b.logp = a.logp + r0 * a.K;
+  if (a.lse_out) b.lse_out = a.lse_out + r0;
+  return b;
+}
+
+// Launches a cache-building op over row chunks that each fit one grid
+// (at most 1024 lanes per row).
+hipError_t launch_cache_chunks(const opd::CacheArgs& a, opd::CacheOp op, int32_t dtype,
+                               bool resident, hipStream_t s) {
+  const int64_t max_rows = kMaxGridLanes / opd::kRowThreads;
+  for (int64_t r0 = 0; r0 < a.N; r0 += max_rows) {
+    const int64_t n = a.N - r0 < max_rows ? a.N - r0 : max_rows;
+    const hipError_t e = opd::launch_cache(cache_rows(a, r0, n, elt_bytes(dtype)), op, dtype,
+                                           resident, s);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
 // Arguments shared by the cache-building entry points.
 int check_row_call(const void* logits, int32_t dtype, int64_t N, int64_t V, int64_t ld, int32_t K,
                    int64_t kmax) {
@@ -177,9 +229,13 @@ DiagLayout diag_layout(int64_t N, int32_t M, const int32_t* groups, int32_t n_gr
   return l;
 }
 
+// The diagnostics reduce over the whole batch in one grid of 64 lanes per
+// token, so one call takes fewer than 2^32 / 64 tokens.
+constexpr int64_t kDiagMaxRows = 0xFFFFFFFFll / 64;
+
 int check_diag(int64_t N, int32_t M, float q, float clip_eps, const int32_t* groups,
                int32_t n_groups, int64_t seq_len) {
-  if (N < 0 || N > INT32_MAX) return OPD_ERR_SHAPE;
+  if (N < 0 || N > kDiagMaxRows) return OPD_ERR_SHAPE;
   if (M < 1 || M > OPD_K_MAX) return OPD_ERR_SUPPORT;
   if (!(q > 0.0f && q <= 1.0f) || !(clip_eps >= 0.0f && clip_eps <= 3.0e38f)) return OPD_ERR_PARAM;
   if (n_groups < 0 || n_groups > opd::kDiagMaxGroups || seq_len < 0) return OPD_ERR_PARAM;
@@ -207,7 +263,7 @@ const char* opd_status_string(int status) {
     case OPD_ERR_ESTIMATOR: return "unknown estimator";
     case OPD_ERR_FLAGS: return "unknown or contradictory flags";
     case OPD_ERR_HIP: return "HIP runtime error";
-    case OPD_ERR_PARAM: return "invalid scalar option (clip_eps)";
+    case OPD_ERR_PARAM: return "invalid scalar option or output (clip_eps, coverage_out)";
   }
   return "unknown status";
 }
@@ -224,8 +280,21 @@ size_t opd_workspace_bytes(int64_t N, int64_t V, int32_t dtype, int32_t estimato
 int opd_loss_fwd_bwd(const void* logits, int32_t dtype, int64_t N, int64_t V, int64_t ld,
                      const opd_cache* cache, int32_t estimator, int32_t k, int32_t M,
                      const uint8_t* mask, const opd_opts* opts, float* loss, void* dlogits,
-                     float* lse_out, float* gathered_out, void* workspace,
+                     float* lse_out, float* gathered_out, float* coverage_out, void* workspace,
                      size_t workspace_bytes, void* stream) {
+  return opd::loss_call(logits, dtype, N, V, ld, cache, estimator, k, M, mask, opts, loss, dlogits,
+                        lse_out, gathered_out, coverage_out, workspace, workspace_bytes, stream);
+}
+
+}  // extern "C"
+
+namespace opd {
+
+int loss_call(const void* logits, int32_t dtype, int64_t N, int64_t V, int64_t ld,
+              const opd_cache* cache, int32_t estimator, int32_t k, int32_t M,
+              const uint8_t* mask, const opd_opts* opts, float* loss, void* dlogits,
+              float* lse_out, float* gathered_out, float* coverage_out, void* workspace,
+              size_t workspace_bytes, void* stream) {
   if (!valid_est(estimator)) return OPD_ERR_ESTIMATOR;
   const opd_opts o = opts ? *opts : opd_opts{1.0f, OPD_F32, 0u, 0.2f};
   if (dtype != OPD_F32 && dtype != OPD_BF16) return OPD_ERR_DTYPE;
@@ -234,6 +303,8 @@ int opd_loss_fwd_bwd(const void* logits, int32_t dtype, int64_t N, int64_t V, in
   if (int rc = check_shape(N, V, ld)) return rc;
   if (int rc = check_support(estimator, V, k, M)) return rc;
   if (est_clip(estimator) && !(o.clip_eps > 0.0f && o.clip_eps <= 3.0e38f)) return OPD_ERR_PARAM;
+  // support coverage exists only for the estimators that read a support
+  if (coverage_out && !est_support(estimator)) return OPD_ERR_PARAM;
   if (N == 0) return OPD_OK;
 
   if (!logits || !cache || !loss || !dlogits) return OPD_ERR_NULL;
@@ -264,10 +335,11 @@ int opd_loss_fwd_bwd(const void* logits, int32_t dtype, int64_t N, int64_t V, in
   Plan plan{false, 1, nvec, 0};
   if (split_wanted(N, o.flags)) {
     const Plan sp = split_plan(N, nvec);
-    if (workspace && workspace_bytes >= sp.ws_bytes && aligned16(workspace))
+    if (workspace && workspace_bytes >= sp.ws_bytes && aligned16(workspace)) {
       plan = sp;
-    else if (o.flags & OPD_FLAG_FORCE_SPLITV)
+    } else if (o.flags & OPD_FLAG_FORCE_SPLITV) {
       return OPD_ERR_WORKSPACE;
+    }
   }
 
   Args a{};
@@ -291,31 +363,47 @@ int opd_loss_fwd_bwd(const void* logits, int32_t dtype, int64_t N, int64_t V, in
   a.dlogits = dlogits;
   a.lse_out = lse_out;
   a.gathered_out = est_dense(estimator) ? nullptr : gathered_out;
+  a.coverage_out = coverage_out;
   a.ws = (float*)workspace;
   a.P = plan.P;
   a.chunk_vec = plan.chunk_vec;
 
-  // The renormalised top-k estimators need the row itself only for lse_out.
-  const bool read_row = !est_topk(estimator) || lse_out != nullptr;
+  // The renormalised top-k estimators need the row itself only for lse_out
+  // and the student's support coverage (both need L).
+  const bool read_row = !est_topk(estimator) || lse_out != nullptr || coverage_out != nullptr;
+  Path path = Path::RowStream;
+  // register-resident rows need whole vectors
+  if (tail == epv) {
+    if (nvec <= (int64_t)opd::slots_small(dtype) * opd::kRowThreads)
+      path = Path::RowResidentSmall;
+    else if (nvec <= (int64_t)opd::slots_large(dtype) * opd::kRowThreads)
+      path = Path::RowResidentLarge;
+  }
+  // rows per launch: the split grid has P workgroups of kSplitThreads lanes
+  // per row, the others at most kRowThreads lanes per row (the top-k zero
+  // fill chunks its own grid)
+  const int64_t lanes_per_row =
+      read_row && plan.split ? (int64_t)plan.P * opd::kSplitThreads : (int64_t)opd::kRowThreads;
+  const int64_t max_rows = kMaxGridLanes / lanes_per_row;
   hipStream_t s = (hipStream_t)stream;
-  hipError_t err;
-  if (!read_row) {
-    err = opd::launch_topk_sparse(a, kernel_est(estimator), dtype, o.dlogits_dtype, s);
-  } else if (plan.split) {
-    err = opd::launch_split(a, kernel_est(estimator), dtype, o.dlogits_dtype, read_row, s);
-  } else {
-    Path path = Path::RowStream;
-    // register-resident rows need whole vectors
-    if (tail == epv) {
-      if (nvec <= (int64_t)opd::slots_small(dtype) * opd::kRowThreads)
-        path = Path::RowResidentSmall;
-      else if (nvec <= (int64_t)opd::slots_large(dtype) * opd::kRowThreads)
-        path = Path::RowResidentLarge;
-    }
-    err = opd::launch_rowwise(a, kernel_est(estimator), dtype, o.dlogits_dtype, path, read_row, s);
+  hipError_t err = hipSuccess;
+  for (int64_t r0 = 0; r0 < N && err == hipSuccess; r0 += max_rows) {
+    const int64_t n = N - r0 < max_rows ? N - r0 : max_rows;
+    const Args b = loss_rows(a, r0, n, elt_bytes(dtype), elt_bytes(o.dlogits_dtype));
+    if (!read_row)
+      err = opd::launch_topk_sparse(b, kernel_est(estimator), dtype, o.dlogits_dtype, s);
+    else if (plan.split)
+      err = opd::launch_split(b, kernel_est(estimator), dtype, o.dlogits_dtype, read_row, s);
+    else
+      err = opd::launch_rowwise(b, kernel_est(estimator), dtype, o.dlogits_dtype, path, read_row,
+                                s);
   }
   return err == hipSuccess ? OPD_OK : OPD_ERR_HIP;
 }
+
+}  // namespace opd
+
+extern "C" {
 
 int opd_validate_cache(const opd_cache* cache, int32_t estimator, int64_t N, int64_t V,
                        int32_t k, int32_t M, int32_t* violations, void* stream) {
@@ -346,7 +434,7 @@ int opd_sample_actions(const void* logits, int32_t dtype, int64_t N, int64_t V, 
   // chunks of G vectors, so that a row's chunk sums fit in LDS
   a.G = (a.nvec + opd::kCdfChunks - 1) / opd::kCdfChunks;
   a.nchunk = (a.nvec + a.G - 1) / a.G;
-  const hipError_t err = opd::launch_cache(a, opd::CacheOp::Sample, dtype, row_fits(a.nvec, dtype),
+  const hipError_t err = launch_cache_chunks(a, opd::CacheOp::Sample, dtype, row_fits(a.nvec, dtype),
                                            (hipStream_t)stream);
   return err == hipSuccess ? OPD_OK : OPD_ERR_HIP;
 }
@@ -359,7 +447,7 @@ int opd_topk_support(const void* logits, int32_t dtype, int64_t N, int64_t V, in
   if (!logits || !idx) return OPD_ERR_NULL;
   opd::CacheArgs a = row_args(logits, dtype, N, V, ld, k, mask, logp, lse_out);
   a.ids_out = idx;
-  const hipError_t err = opd::launch_cache(a, opd::CacheOp::Topk, dtype, row_fits(a.nvec, dtype),
+  const hipError_t err = launch_cache_chunks(a, opd::CacheOp::Topk, dtype, row_fits(a.nvec, dtype),
                                            (hipStream_t)stream);
   return err == hipSuccess ? OPD_OK : OPD_ERR_HIP;
 }
@@ -372,7 +460,7 @@ int opd_score_actions(const void* logits, int32_t dtype, int64_t N, int64_t V, i
   if (!logits || !ids || !logp) return OPD_ERR_NULL;
   opd::CacheArgs a = row_args(logits, dtype, N, V, ld, K, mask, logp, lse_out);
   a.ids = ids;
-  const hipError_t err = opd::launch_cache(a, opd::CacheOp::Score, dtype, row_fits(a.nvec, dtype),
+  const hipError_t err = launch_cache_chunks(a, opd::CacheOp::Score, dtype, row_fits(a.nvec, dtype),
                                            (hipStream_t)stream);
   return err == hipSuccess ? OPD_OK : OPD_ERR_HIP;
 }

@@ -6,6 +6,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "../../include/opd.h"
+
 namespace opd {
 
 enum Est : int { FKL_TOPK = 0, RKL_TOPK = 1, RKL_MC1 = 2, RKL_MC = 3, FKL_DENSE = 4, RKL_DENSE = 5 };
@@ -58,6 +60,7 @@ struct Args {
   void* dlogits;
   float* lse_out;       // nullable
   float* gathered_out;  // nullable
+  float* coverage_out;  // [N, 2] nullable: Z_p^S, Z_q^S (estimators with a support)
   float* ws;            // split path partials [N, P, kPartialFloats]
   int P;                // split path chunks per row
   int64_t chunk_vec;    // split path vectors per chunk
@@ -131,6 +134,13 @@ hipError_t launch_rowwise(const Args& a, int est, int in_dt, int out_dt, Path pa
 hipError_t launch_split(const Args& a, int est, int in_dt, int out_dt, bool read_row,
                         hipStream_t stream);
 hipError_t launch_topk_sparse(const Args& a, int est, int in_dt, int out_dt, hipStream_t stream);
+// The body of the loss entry point.
+int loss_call(const void* logits, int32_t dtype, int64_t N, int64_t V, int64_t ld,
+              const ::opd_cache* cache, int32_t estimator, int32_t k, int32_t M,
+              const uint8_t* mask, const ::opd_opts* opts, float* loss, void* dlogits,
+              float* lse_out, float* gathered_out, float* coverage_out, void* workspace,
+              size_t workspace_bytes, void* stream);
+
 hipError_t launch_validate(const int32_t* ids, const float* tau, const float* beta, int64_t N,
                            int64_t V, int K, int check_dups, int32_t* violations,
                            hipStream_t stream);

@@ -326,6 +326,7 @@ __device__ void masked_row(const Args& a, int64_t row, void* grow, int64_t v0, i
     }
     if (a.gathered_out)
       for (int i = threadIdx.x; i < a.K; i += NT) a.gathered_out[row * a.K + i] = 0.f;
+    if (a.coverage_out && threadIdx.x < 2) a.coverage_out[2 * row + threadIdx.x] = 0.f;
   }
 }
 
@@ -343,6 +344,22 @@ __device__ __forceinline__ void finish_row(const Args& a, int64_t row, float L, 
     }
     if (a.gathered_out)
       for (int i = lane; i < a.K; i += 64) a.gathered_out[row * a.K + i] = c.z[i];
+    if (a.coverage_out) {
+      // support coverage (App. A.1's restricted normalisers): the student's
+      // mass Z_p^S = sum_i exp(z_{a_i} - L) and the teacher's Z_q^S =
+      // sum_i exp(tau_i) on the cached support
+      float zp = 0.f, zq = 0.f;
+      for (int i = lane; i < a.K; i += 64) {
+        zp += expf(c.z[i] - L);
+        zq += expf(c.t[i]);
+      }
+      zp = wave_sum(zp);
+      zq = wave_sum(zq);
+      if (lane == 0) {
+        a.coverage_out[2 * row] = zp;
+        a.coverage_out[2 * row + 1] = zq;
+      }
+    }
   }
 }
 
@@ -1079,8 +1096,8 @@ template <class TI, class TO, int EST>
 hipError_t topk_sparse_t(const Args& a, hipStream_t s) {
   if constexpr (is_topk(EST)) {
     const int64_t bpr = (a.nvec + kFillThreads - 1) / kFillThreads;
-    // row chunks keep every grid under 2^31 workgroups
-    const int64_t rows_per_launch = ((int64_t)1 << 31) / bpr;
+    // row chunks keep every grid under 2^32 work-items
+    const int64_t rows_per_launch = (int64_t)0xFFFFFFFFll / (bpr * kFillThreads);
     for (int64_t r0 = 0; r0 < a.N; r0 += rows_per_launch) {
       const int64_t n = a.N - r0 < rows_per_launch ? a.N - r0 : rows_per_launch;
       hipLaunchKernelGGL((k_fill_zero<TO>), dim3((unsigned)(n * bpr)), dim3(kFillThreads), 0, s, a,

@@ -1,16 +1,10 @@
 """Shared helpers of the GPU parity tests: device copies of generated inputs,
 one call through the C ABI, the oracle on the same inputs, and the
-comparison at the stated tolerances.
-
-Tolerances (per token loss): |gpu - ref| <= rtol * (|ref| + s), rtol = 1e-5
-for fp32 logits and 1e-3 for bf16 logits (fp32 accumulation).  s is the
-natural magnitude of the terms the loss sums: 1 for the top-k and dense KLs
-(their weights sum to one), (1/M) sum_i rho_i (|A_i| + 1) for the MC
-surrogates (A_theta or A_old), whose value can cancel to near zero while their
-terms do not, and (1/M) sum_i (|A_i| + |log p_i| + 1) for the surrogate
-without importance ratios, whose terms are products A_i log p_i.
-Gradient: |gpu - ref| <= 1e-4 for fp32 output; bf16 output adds one bf16 ulp
-(2^-8 relative).  Gathered logits are compared bit for bit.
+comparison at the bounds of tolerances.py (per-token loss: the stated
+relative tolerances plus the fp32 evaluation's own bound; gradient: every
+element within 1e-4 and within GRAD_RTOL of its natural magnitude; gathered
+logits bit for bit).  The gradient comparison runs on the GPU in torch,
+chunk by chunk, against the oracle's values copied there.
 """
 from __future__ import annotations
 
@@ -22,6 +16,7 @@ import torch
 import oracle
 import paper_2606_24143_amd as opd
 import synth
+import tolerances
 
 DEV = torch.device("cuda:0")
 TOPK = ("fkl_topk", "rkl_topk")             # renormalised on S
@@ -69,42 +64,49 @@ def run_gpu(logits_dev, est, ids, tau, beta, teacher_dev=None, mask=None, **kw):
 
 
 def loss_scale(est, ids, tau, beta, ref):
-    """Per-row s of the loss tolerance (see module docstring)."""
-    n = ref["loss"].shape[0]
-    if est not in MC:
-        return np.ones(n)
-    lp = ref["gathered"] - ref["lse"][:, None]
-    tau = tau.astype(np.float64)
-    if est == "rkl_mc_nois":
-        return (np.abs(tau - lp) + np.abs(lp) + 1.0).mean(axis=1)
-    beta = beta.astype(np.float64)
-    A = tau - beta if est in ("rkl_mc_old", "rkl_mc_old_clip") else tau - lp
-    rho = np.exp(lp - beta)
-    return (rho * (np.abs(A) + 1.0)).mean(axis=1)
+    """Per-row s of the loss bounds (tolerances.loss_scale)."""
+    return tolerances.loss_scale(est, ref["lse"], ref.get("gathered"), tau, beta)
 
 
 def check_loss(name, got, ref_loss, scale, rtol, mask=None):
-    got = np.asarray(got, np.float64)
-    err = np.abs(got - ref_loss)
-    tol = rtol * (np.abs(ref_loss) + scale)
-    bad = ~(err <= tol)
-    if mask is not None:
-        assert np.all(got[mask == 0] == 0.0), name + ": masked rows must have loss 0"
-    if bad.any():
-        i = int(np.argmax(np.where(bad, err / np.maximum(tol, 1e-30), 0)))
-        raise AssertionError("%s: loss row %d got %.9g ref %.9g (tol %.3g); %d bad rows" %
-                             (name, i, got[i], ref_loss[i], tol[i], int(bad.sum())))
+    r = tolerances.loss_check(got, ref_loss, scale, rtol, mask)
+    say("%s: loss max err/(|ref|+s) %.3g, max plain relative err %.3g (%d rows)" %
+        (name, r["max_scaled_rel"], r["max_plain_rel"], r["plain_rows"]))
+    assert r.get("masked_nonzero", 0) == 0, name + ": masked rows must have loss 0"
+    assert r["scaled"] == 0 and r["plain"] == 0 and r["arith"] == 0, (
+        "%s: loss outside its bounds (%d scaled, %d plain-relative, %d fp32-arithmetic rows); "
+        "max err/(|ref|+s) %.3g" % (name, r["scaled"], r["plain"], r["arith"],
+                                    r["max_scaled_rel"]))
 
 
-def check_grad(name, got, ref_grad, bf16_out=False, atol=1e-4):
-    got = np.asarray(got, np.float64)
-    err = np.abs(got - ref_grad)
-    tol = atol + (2.0 ** -8 * np.abs(ref_grad) if bf16_out else 0.0)
-    bad = ~(err <= tol)
-    if bad.any():
-        idx = np.unravel_index(int(np.argmax(np.where(bad, err - tol, -np.inf))), err.shape)
-        raise AssertionError("%s: dlogits %s got %.9g ref %.9g; %d bad entries" %
-                             (name, idx, got[idx], ref_grad[idx], int(bad.sum())))
+def widen_dev(stored, V: int) -> torch.Tensor:
+    """Stored rows (uint16 bf16 bits or float32, [n, ld]) as float64 on the GPU."""
+    return to_dev(stored)[:, :V].to(torch.float64)
+
+
+def grad_mag(est, z_dev, ref, ids, tau, beta, y_dev=None, gamma=1.0, mask=None):
+    """tolerances.grad_magnitude on the GPU from the oracle's outputs."""
+    return tolerances.grad_magnitude(est, z_dev, ref["lse"], gathered=ref.get("gathered"),
+                                     ids=ids, tau=tau, beta=beta, y=y_dev, loss=ref["loss"],
+                                     gamma=gamma, mask=mask)
+
+
+def check_grad(name, got, ref_grad, mag, bf16_out=False, row0=0):
+    """Every element of a gradient block (got: GPU tensor) against the
+    oracle's (numpy or tensor) at the per-element bound; returns the largest
+    err / bound."""
+    if not isinstance(got, torch.Tensor):
+        got = torch.from_numpy(np.asarray(got, np.float64))
+    got = got.to(DEV)
+    ref = tolerances.as_t(ref_grad, DEV)
+    bad, worst, (r, c) = tolerances.grad_check(got, ref, mag.to(DEV), bf16_out)
+    if bad:
+        raise AssertionError("%s: dlogits [%d, %d] got %.9g ref %.9g (bound %.3g); %d bad entries"
+                             % (name, row0 + r, c, float(got[r, c]), float(ref[r, c]),
+                                float(min(tolerances.GRAD_ATOL,
+                                          tolerances.GRAD_RTOL * float(mag[r, c]) +
+                                          tolerances.GRAD_FLOOR)), bad))
+    return worst
 
 
 def dlogits_f64(t: torch.Tensor) -> np.ndarray:

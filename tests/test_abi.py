@@ -52,7 +52,8 @@ def test_status_strings():
 
 
 def call(logits=FAKE, dtype=1, N=4, V=1024, ld=None, cache="mc", est=3, k=16, M=4, mask=None,
-         opts=None, loss=FAKE, dlogits=FAKE, lse=None, gathered=None, ws=None, ws_bytes=0):
+         opts=None, loss=FAKE, dlogits=FAKE, lse=None, gathered=None, coverage=None, ws=None,
+         ws_bytes=0):
     ld = V if ld is None else ld
     if cache == "mc":
         c = OpdCache(None, FAKE, FAKE, FAKE, None)
@@ -65,7 +66,7 @@ def call(logits=FAKE, dtype=1, N=4, V=1024, ld=None, cache="mc", est=3, k=16, M=
     cp = None if c is None else ctypes.byref(c)
     op = None if opts is None else ctypes.byref(opts)
     return opd.lib().opd_loss_fwd_bwd(logits, dtype, N, V, ld, cp, est, k, M, mask, op, loss,
-                                      dlogits, lse, gathered, ws, ws_bytes, None)
+                                      dlogits, lse, gathered, coverage, ws, ws_bytes, None)
 
 
 @pytest.mark.parametrize("kw,code", [
@@ -109,6 +110,8 @@ def call(logits=FAKE, dtype=1, N=4, V=1024, ld=None, cache="mc", est=3, k=16, M=
     (dict(est=6, opts=OpdOpts(1.0, 0, 0, float("inf"))), PARAM),
     (dict(est=7, cache=OpdCache(None, FAKE, FAKE, None, None)), NULL),  # A_old needs behav_logp
     (dict(est=9, M=0), SUPPORT),
+    (dict(coverage=FAKE), PARAM),                # coverage needs a cached support (MC here)
+    (dict(est=4, cache="dense", coverage=FAKE), PARAM),
     (dict(N=8, opts=OpdOpts(1.0, 0, 4)), WORKSPACE),  # split path forced, no workspace
     (dict(N=8, opts=OpdOpts(1.0, 0, 4), ws=FAKE, ws_bytes=16), WORKSPACE),
 ])

@@ -17,7 +17,8 @@ import oracle
 import paper_2606_24143_amd as opd
 import synth
 from gpu_common import (DENSE, DEV, MC, SUPPORT, TOPK, TRUNC, cache_arrays, check_grad, check_loss,
-                        dlogits_f64, loss_scale, oracle_dtype, rtol_for, run_gpu, say, to_dev)
+                        dlogits_f64, grad_mag, loss_scale, oracle_dtype, rtol_for, run_gpu, say,
+                        to_dev, widen_dev)
 
 pytestmark = pytest.mark.gpu
 
@@ -51,11 +52,20 @@ def small_inputs(shape: str, dtype: int):
     return w, d, mask
 
 
-def compare(name, w, d, est, out, ref, mask=None, bf16_out=False):
+def compare(name, w, d, est, out, ref, mask=None, bf16_out=False, gamma=1.0, logits=None,
+            teacher=None):
+    """Loss, every gradient element, lse and gathered logits against the
+    oracle.  logits / teacher: the stored rows (default d's)."""
     ids, tau, beta = cache_arrays(d, est)
+    logits = d["logits"] if logits is None else logits
+    if est in DENSE and teacher is None:
+        teacher = d["teacher_logits"]
     check_loss(name, out["loss"].cpu().numpy(), ref["loss"],
                loss_scale(est, ids, tau, beta, ref), rtol_for(w.dtype), mask)
-    check_grad(name, dlogits_f64(out["dlogits"]), ref["grad"], bf16_out=bf16_out)
+    mag = grad_mag(est, widen_dev(logits, w.V), ref, ids, tau, beta,
+                   widen_dev(teacher, w.V) if est in DENSE else None, gamma, mask)
+    worst = check_grad(name, out["dlogits"], ref["grad"], mag, bf16_out=bf16_out)
+    say("%s: dlogits max err/bound %.3g" % (name, worst))
     if "lse" in out:
         lse = out["lse"].cpu().numpy().astype(np.float64)
         valid = ref["lse"] != 0
@@ -87,7 +97,7 @@ def test_parity_small(shape, dtype, est, path):
     out = run_gpu(logits, est, ids, tau, beta, teacher, mask=mask, grad_scale=0.75,
                   flags=PATHS[path], want_lse=True, want_gathered=est not in DENSE)
     ref = oracle_for(w, d, est, mask, gamma=0.75)
-    compare("%s/%s/%s" % (shape, est, path), w, d, est, out, ref, mask)
+    compare("%s/%s/%s" % (shape, est, path), w, d, est, out, ref, mask, gamma=0.75)
 
 
 @pytest.mark.parametrize("gamma", [-0.5, 0.0, 3.0])
@@ -107,7 +117,8 @@ def test_grad_scale_sign_and_zero(shape, est, gamma):
     for path, flags in PATHS.items():
         out = run_gpu(logits, est, ids, tau, beta, teacher, mask=mask, grad_scale=gamma,
                       flags=flags)
-        compare("%s/%s/%s/gamma=%g" % (shape, est, path, gamma), w, d, est, out, ref, mask)
+        compare("%s/%s/%s/gamma=%g" % (shape, est, path, gamma), w, d, est, out, ref, mask,
+                gamma=gamma)
         if gamma == 0.0:
             assert not out["dlogits"].any(), "a zero gradient scale leaves dlogits zero"
 
@@ -145,6 +156,39 @@ def test_support_sizes(est, K):
         compare("%s/K=%d" % (est, K), w, d, est, out, oracle_for(w, d, est, None))
         if est in TOPK and K == 1:
             assert not out["loss"].any() and not out["dlogits"].any()
+
+
+COV_RTOL = 3e-5  # fp32 sums of at most 256 exponentials whose arguments carry L's error
+
+
+def check_coverage(name, got, ref, mask=None):
+    got = np.asarray(got, np.float64)
+    err = np.abs(got - ref)
+    assert np.all(err <= COV_RTOL * np.abs(ref) + 1e-30), (
+        "%s: support coverage off by %.3g relative" % (name, np.max(err / np.maximum(ref, 1e-30))))
+    if mask is not None:
+        assert not got[mask == 0].any()
+
+
+@pytest.mark.parametrize("est", SUPPORT)
+@pytest.mark.parametrize("dtype", [synth.F32, synth.BF16], ids=["f32", "bf16"])
+@pytest.mark.parametrize("shape", ["v1000", "v3001_tail", "v151936", "v200000_wide"])
+def test_support_coverage(shape, dtype, est):
+    """Z_p^S and Z_q^S (App. A.1) against the oracle on every path; for the
+    renormalised estimators without lse_out the request alone makes the call
+    read the rows.  The loss and gradient stay what they are without it."""
+    w, d, mask = small_inputs(shape, dtype)
+    N, V, ld = SHAPES[shape]
+    say("coverage %s %s %s" % (shape, "bf16" if dtype else "f32", est))
+    logits = to_dev(d["logits"])[:, :V]
+    ids, tau, _ = cache_arrays(d, est)
+    ref = oracle.coverage_rows(oracle_dtype(dtype), d["logits"], V, ids, tau, mask=mask)
+    for path, flags in PATHS.items():
+        out = run_gpu(logits, est, ids, tau, None, mask=mask, flags=flags, want_coverage=True)
+        check_coverage("%s/%s/%s" % (shape, est, path), out["coverage"].cpu().numpy(), ref, mask)
+        base = run_gpu(logits, est, ids, tau, None, mask=mask, flags=flags)
+        assert torch.equal(out["loss"], base["loss"])
+        assert torch.equal(out["dlogits"], base["dlogits"])
 
 
 @pytest.mark.parametrize("eps", [0.02, 0.2, 1e9])
@@ -226,7 +270,9 @@ def test_padding_columns_and_skip_masked_rows_untouched():
         check_loss("pad", loss.cpu().numpy(), ref["loss"],
                    loss_scale("rkl_mc", ids, tau, beta, ref), rtol_for(w.dtype), mask)
         keep = mask != 0
-        check_grad("pad", b[keep, :V].astype(np.float64), ref["grad"][keep])
+        mag = grad_mag("rkl_mc", widen_dev(d["logits"], V), ref, ids, tau, beta, mask=mask)
+        check_grad("pad", torch.from_numpy(b[keep, :V].astype(np.float64)), ref["grad"][keep],
+                   mag[torch.from_numpy(keep).to(DEV)])
 
 
 def test_topk_full_support_matches_dense_on_gpu():
@@ -335,7 +381,8 @@ def test_dense_rows_with_late_and_far_maxima(dtype, V, est):
     for path, flags in PATHS.items():
         out = run_gpu(to_dev(zs), est, None, None, None, to_dev(ys), flags=flags, grad_scale=0.5,
                       want_lse=True)
-        compare("wide/%d/%s/%s" % (V, est, path), w, {}, est, out, ref)
+        compare("wide/%d/%s/%s" % (V, est, path), w, {}, est, out, ref, gamma=0.5, logits=zs,
+                teacher=ys)
 
 
 def test_nan_logits_propagate_to_their_row_only():
@@ -382,50 +429,82 @@ FULL = ["n512_v32000_f32_topk16_mc4", "n8192_v151936_bf16_topk32_peaked",
         "n256_v151936_bf16_mc16_smallbatch", "n16384_v151936_bf16_dense"]
 
 
+CHUNK = 1024
+
+
+def full_runs(w):
+    """(estimator, flags, with lse/gathered outputs) runs of a full-size
+    workload.  Every estimator runs with lse_out and gathered_out (for the MC
+    and dense estimators the kernel path the benchmark times, plus two small
+    stores); the renormalised top-k estimators also run without them, which
+    is their write-only path and the configuration the benchmark times.
+    Small batches also run the split-vocabulary path."""
+    runs = []
+    for est in w.estimators:
+        if est in TOPK:
+            runs.append((est, 0, False))
+        runs.append((est, 0, True))
+    if w.N <= 1024:
+        runs += [(est, opd.FLAG_FORCE_SPLITV, True) for est in w.estimators]
+    return runs
+
+
 @pytest.mark.parametrize("name", FULL)
 def test_parity_full_size(name):
-    """Every row's loss and log-partition against the oracle; the gradient on
-    a sample of rows (first, last, and a seeded spread); the gradient row-sum
-    (zero for every estimator, since softmax ignores a constant shift) on
-    every row."""
+    """Every row of every output against the oracle: loss and log-partition
+    per row, gathered logits bit for bit, and every gradient element at the
+    per-element bound (oracle rows in chunks of CHUNK, compared on the GPU);
+    plus the zero row-sum of every gradient row."""
     w = synth.WORKLOADS[name]
     say("full-size %s: generating" % name)
     d = synth.generate(w)
     mask = d["mask"]
+    N, V = w.N, w.V
     logits = to_dev(d["logits"])
     teacher = to_dev(d["teacher_logits"]) if w.dense_teacher else None
-    rng = np.random.default_rng(w.seed)
-    rows = np.unique(np.concatenate([[0, w.N - 1], rng.choice(w.N, min(w.N, 40), replace=False)]))
-    # the default path (what the benchmark times); small batches also run the
-    # split-vocabulary path
-    runs = [(est, 0) for est in w.estimators]
-    if w.N <= 1024:
-        runs += [(est, opd.FLAG_FORCE_SPLITV) for est in w.estimators]
-    for est, flags in runs:
-        say("full-size %s %s flags=%d" % (name, est, flags))
+    dense = w.dense_teacher
+    for est, flags, aux in full_runs(w):
+        say("full-size %s %s flags=%d aux=%d" % (name, est, flags, aux))
         ids, tau, beta = cache_arrays(d, est)
-        out = run_gpu(logits, est, ids, tau, beta, teacher, mask=mask, want_lse=True,
-                      want_gathered=est not in DENSE, flags=flags)
-        ref = oracle.rows(est, oracle_dtype(w.dtype), d["logits"], w.V, ids=ids, tau=tau,
-                          beta=beta, teacher_logits=d.get("teacher_logits"), mask=mask,
-                          want_grad=False)
-        check_loss(name + "/" + est, out["loss"].cpu().numpy(), ref["loss"],
-                   loss_scale(est, ids, tau, beta, ref), rtol_for(w.dtype), mask)
+        out = run_gpu(logits, est, ids, tau, beta, teacher, mask=mask, want_lse=aux,
+                      want_gathered=aux and est not in DENSE, flags=flags,
+                      want_coverage=aux and est in SUPPORT)
+        if aux and est in SUPPORT:
+            check_coverage("%s/%s" % (name, est), out["coverage"].cpu().numpy(),
+                           oracle.coverage_rows(oracle_dtype(w.dtype), d["logits"], V, ids, tau,
+                                                mask=mask), mask)
+        ref_loss, ref_lse = np.zeros(N), np.zeros(N)
+        ref_gat = [] if est not in DENSE else None
+        worst = 0.0
+        for r0 in range(0, N, CHUNK):
+            sl = slice(r0, min(N, r0 + CHUNK))
+            c_ids, c_tau, c_beta = [None if a is None else a[sl] for a in (ids, tau, beta)]
+            ref = oracle.rows(est, oracle_dtype(w.dtype), d["logits"][sl], V, ids=c_ids,
+                              tau=c_tau, beta=c_beta,
+                              teacher_logits=d["teacher_logits"][sl] if est in DENSE else None,
+                              mask=mask[sl])
+            ref_loss[sl], ref_lse[sl] = ref["loss"], ref["lse"]
+            if ref_gat is not None:
+                ref_gat.append(ref["gathered"])
+            mag = grad_mag(est, logits[sl, :V].double(), ref, c_ids, c_tau, c_beta,
+                           teacher[sl, :V].double() if est in DENSE else None, 1.0, mask[sl])
+            worst = max(worst, check_grad("%s/%s" % (name, est), out["dlogits"][sl],
+                                          ref["grad"], mag, row0=r0))
+            del ref, mag
+        say("%s/%s flags=%d: dlogits max err/bound %.3g over every element" %
+            (name, est, flags, worst))
+        gat_ref = {"lse": ref_lse, "gathered": None if ref_gat is None else np.concatenate(ref_gat)}
+        check_loss("%s/%s" % (name, est), out["loss"].cpu().numpy(), ref_loss,
+                   loss_scale(est, ids, tau, beta, gat_ref), rtol_for(w.dtype), mask)
         valid = mask != 0
-        np.testing.assert_allclose(out["lse"].cpu().numpy()[valid], ref["lse"][valid], rtol=2e-6)
-        if est not in DENSE:
-            assert np.array_equal(out["gathered"].cpu().numpy().astype(np.float64),
-                                  ref["gathered"])
+        if aux:
+            lse = out["lse"].cpu().numpy().astype(np.float64)
+            np.testing.assert_allclose(lse[valid], ref_lse[valid], rtol=2e-6)
+            assert np.all(lse[~valid] == 0.0)
+            if est not in DENSE:
+                assert np.array_equal(out["gathered"].cpu().numpy().astype(np.float64),
+                                      gat_ref["gathered"]), "gathered logits not bit-exact"
         rs = out["dlogits"].sum(dim=1, dtype=torch.float64).cpu().numpy()
         assert np.all(np.abs(rs) < 1e-4), "gradient rows must sum to zero"
-        sub = {k: (v[rows] if isinstance(v, np.ndarray) and v.shape[:1] == (w.N,) else v)
-               for k, v in d.items()}
-        s_ids, s_tau, s_beta = cache_arrays(sub, est)
-        ref_s = oracle.rows(est, oracle_dtype(w.dtype), sub["logits"], w.V, ids=s_ids, tau=s_tau,
-                            beta=s_beta, teacher_logits=sub.get("teacher_logits"),
-                            mask=sub["mask"])
-        idx = torch.from_numpy(rows).to(DEV)
-        check_grad(name + "/" + est, dlogits_f64(out["dlogits"].index_select(0, idx)),
-                   ref_s["grad"])
         del out
         torch.cuda.empty_cache()
