@@ -55,8 +55,10 @@ typedef enum opd_status {
   OPD_ERR_ESTIMATOR = -7, /* unknown estimator */
   OPD_ERR_FLAGS = -8,     /* unknown or contradictory flag bits */
   OPD_ERR_HIP = -9,       /* a HIP runtime call or kernel launch failed */
-  OPD_ERR_PARAM = -10     /* invalid scalar option (clip_eps of a clipped estimator), or
+  OPD_ERR_PARAM = -10,    /* invalid scalar option (clip_eps of a clipped estimator), or
                              coverage_out for an estimator without a cached support */
+  OPD_ERR_SCRATCH = -11   /* opd_loss_fwd_bwd_noalloc: the call needs more scratch than
+                             OPD_NOALLOC_SCRATCH_BYTES */
 } opd_status;
 
 /*
@@ -226,6 +228,38 @@ int opd_loss_fwd_bwd(const void* logits, int32_t dtype, int64_t N, int64_t V, in
                      const uint8_t* mask, const opd_opts* opts, float* loss, void* dlogits,
                      float* lse_out, float* gathered_out, float* coverage_out, void* workspace,
                      size_t workspace_bytes, void* stream);
+
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * fused forward + backward as opd_loss_fwd_bwd, with the same arguments
+ * except the workspace, the same kernels and bitwise the same results.  The
+ * split-vocabulary path keeps its per-(row, chunk) statistics in a static
+ * device array of OPD_NOALLOC_SCRATCH_BYTES that the library holds on each
+ * GPU it runs on until the process ends (its address is looked up once per
+ * device, on the first call that needs it, with that device current).  The
+ * call allocates nothing: no hipMalloc, hipFree or allocating library call.
+ *   - A call whose split path needs more than OPD_NOALLOC_SCRATCH_BYTES
+ *     (opd_workspace_bytes(...) of the same arguments) returns
+ *     OPD_ERR_SCRATCH when the split path is forced (OPD_FLAG_FORCE_SPLITV);
+ *     unforced, such a call runs the row-per-workgroup path, which needs no
+ *     scratch.  (Unforced calls below 128 rows need at most 272 KiB.)
+ *   - Every record the split path reads is written earlier in the same call,
+ *     so nothing carries over from the previous call's contents.
+ *   - All calls on one GPU share that GPU's array: calls that overlap in time
+ *     on one GPU (on different streams, or from several host threads) race
+ *     and may return wrong results.  Serialise them.
+ * Other errors as for opd_loss_fwd_bwd.
+ */
+#define OPD_NOALLOC_SCRATCH_BYTES (1u << 20)
+int opd_loss_fwd_bwd_noalloc(const void* logits, int32_t dtype, int64_t N, int64_t V, int64_t ld,
+                             const opd_cache* cache, int32_t estimator, int32_t k, int32_t M,
+                             const uint8_t* mask, const opd_opts* opts, float* loss,
+                             void* dlogits, float* lse_out, float* gathered_out,
+                             float* coverage_out, void* stream);
+
+/* OPD_NOALLOC_SCRATCH_BYTES of the built library. */
+size_t opd_noalloc_scratch_bytes(void);
 
 /*
  * Bytes of workspace opd_loss_fwd_bwd uses for these arguments (0 when the

@@ -32,10 +32,12 @@ K_MAX = 256
 
 STATUS = {0: "OPD_OK", -1: "OPD_ERR_NULL", -2: "OPD_ERR_SHAPE", -3: "OPD_ERR_SUPPORT",
           -4: "OPD_ERR_DTYPE", -5: "OPD_ERR_ALIGN", -6: "OPD_ERR_WORKSPACE",
-          -7: "OPD_ERR_ESTIMATOR", -8: "OPD_ERR_FLAGS", -9: "OPD_ERR_HIP", -10: "OPD_ERR_PARAM"}
+          -7: "OPD_ERR_ESTIMATOR", -8: "OPD_ERR_FLAGS", -9: "OPD_ERR_HIP", -10: "OPD_ERR_PARAM",
+          -11: "OPD_ERR_SCRATCH"}
 
 # every symbol include/opd.h declares
-EXPORTS = ("opd_loss_fwd_bwd", "opd_workspace_bytes", "opd_validate_cache", "opd_sample_actions",
+EXPORTS = ("opd_loss_fwd_bwd", "opd_loss_fwd_bwd_noalloc", "opd_noalloc_scratch_bytes",
+           "opd_workspace_bytes", "opd_validate_cache", "opd_sample_actions",
            "opd_topk_support", "opd_score_actions", "opd_mc_diag_workspace_bytes",
            "opd_mc_diagnostics", "opd_status_string", "opd_version")
 
@@ -80,6 +82,12 @@ def lib():
                                        i32, P, ctypes.POINTER(OpdOpts), P, P, P, P, P, P,
                                        ctypes.c_size_t, P]
         L.opd_loss_fwd_bwd.restype = ctypes.c_int
+        L.opd_loss_fwd_bwd_noalloc.argtypes = [P, i32, i64, i64, i64, ctypes.POINTER(OpdCache),
+                                               i32, i32, i32, P, ctypes.POINTER(OpdOpts), P, P,
+                                               P, P, P, P]
+        L.opd_loss_fwd_bwd_noalloc.restype = ctypes.c_int
+        L.opd_noalloc_scratch_bytes.argtypes = []
+        L.opd_noalloc_scratch_bytes.restype = ctypes.c_size_t
         L.opd_workspace_bytes.argtypes = [i64, i64, i32, i32, i32, i32, ctypes.c_uint32]
         L.opd_workspace_bytes.restype = ctypes.c_size_t
         L.opd_validate_cache.argtypes = [ctypes.POINTER(OpdCache), i32, i64, i64, i32, i32, P, P]
@@ -184,7 +192,8 @@ def loss_fwd_bwd(logits: torch.Tensor, estimator: str, *, idx=None, sampled_ids=
                  teacher_logp=None, behav_logp=None, teacher_logits=None, mask=None,
                  grad_scale: float = 1.0, dlogits_dtype=torch.float32, flags: int = 0,
                  clip_eps: float = 0.2, want_lse: bool = False, want_gathered: bool = False,
-                 want_coverage: bool = False, workspace=None, out=None, stream=None):
+                 want_coverage: bool = False, workspace=None, out=None, stream=None,
+                 no_alloc: bool = False):
     """One fused forward+backward call of opd_loss_fwd_bwd.
 
     logits: [N, V] device tensor (a row-strided view of an [N, ld] buffer is
@@ -194,7 +203,9 @@ def loss_fwd_bwd(logits: torch.Tensor, estimator: str, *, idx=None, sampled_ids=
     cached support only) when requested.  `workspace=None` allocates what the
     split path needs; pass a tensor to supply your own (or an empty one to
     force the row-per-workgroup path).  `out` may hold preallocated "loss"
-    and "dlogits" ([N, ld]) tensors.
+    and "dlogits" ([N, ld]) tensors.  `no_alloc=True` calls
+    opd_loss_fwd_bwd_noalloc instead, whose split path uses the library's
+    static scratch (no workspace is allocated or passed).
     """
     if estimator not in ESTIMATORS:
         raise ValueError("unknown estimator %r" % (estimator,))
@@ -251,18 +262,26 @@ def loss_fwd_bwd(logits: torch.Tensor, estimator: str, *, idx=None, sampled_ids=
     if want_coverage and estimator not in TOPK:
         raise ValueError("support coverage exists for the estimators with a cached support only")
     coverage = torch.empty((N, 2), dtype=torch.float32, device=dev) if want_coverage else None
-    if workspace is None:
-        nbytes = workspace_bytes(N, V, dt, estimator, k, M, flags)
-        workspace = (torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
-                     if nbytes else None)
-    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
-    rc = lib().opd_loss_fwd_bwd(_ptr(logits), dt, N, V, ld, ctypes.byref(cache), est, k, M,
-                                _ptr(mask), ctypes.byref(opts), _ptr(loss), _ptr(dbuf),
-                                _ptr(lse), _ptr(gathered), _ptr(coverage),
-                                _ptr(workspace) if ws_bytes else None, ws_bytes,
-                                _stream(stream))
-    if rc != 0:
-        raise OpdError(rc, "opd_loss_fwd_bwd")
+    if no_alloc:
+        rc = lib().opd_loss_fwd_bwd_noalloc(_ptr(logits), dt, N, V, ld, ctypes.byref(cache), est,
+                                            k, M, _ptr(mask), ctypes.byref(opts), _ptr(loss),
+                                            _ptr(dbuf), _ptr(lse), _ptr(gathered),
+                                            _ptr(coverage), _stream(stream))
+        if rc != 0:
+            raise OpdError(rc, "opd_loss_fwd_bwd_noalloc")
+    else:
+        if workspace is None:
+            nbytes = workspace_bytes(N, V, dt, estimator, k, M, flags)
+            workspace = (torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
+                         if nbytes else None)
+        ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+        rc = lib().opd_loss_fwd_bwd(_ptr(logits), dt, N, V, ld, ctypes.byref(cache), est, k, M,
+                                    _ptr(mask), ctypes.byref(opts), _ptr(loss), _ptr(dbuf),
+                                    _ptr(lse), _ptr(gathered), _ptr(coverage),
+                                    _ptr(workspace) if ws_bytes else None, ws_bytes,
+                                    _stream(stream))
+        if rc != 0:
+            raise OpdError(rc, "opd_loss_fwd_bwd")
     res = {"loss": loss, "dlogits": dbuf[:, :V]}
     if lse is not None:
         res["lse"] = lse

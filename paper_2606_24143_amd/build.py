@@ -10,7 +10,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libopd.so")
 SOURCES = [os.path.join(CSRC, "opd_kernels.hip"), os.path.join(CSRC, "opd_cache_kernels.hip"),
-           os.path.join(CSRC, "opd_diag_kernels.hip"), os.path.join(CSRC, "opd_api.cpp")]
+           os.path.join(CSRC, "opd_diag_kernels.hip"), os.path.join(CSRC, "opd_noalloc.hip"),
+           os.path.join(CSRC, "opd_api.cpp")]
 HEADERS = [os.path.join(CSRC, "opd_internal.h"), os.path.join(CSRC, "opd_device.h"),
            os.path.join(ROOT, "include", "opd.h")]
 

@@ -264,6 +264,8 @@ const char* opd_status_string(int status) {
     case OPD_ERR_FLAGS: return "unknown or contradictory flags";
     case OPD_ERR_HIP: return "HIP runtime error";
     case OPD_ERR_PARAM: return "invalid scalar option or output (clip_eps, coverage_out)";
+    case OPD_ERR_SCRATCH:
+      return "the call needs more scratch than the no-allocation entry point holds";
   }
   return "unknown status";
 }
@@ -283,7 +285,8 @@ int opd_loss_fwd_bwd(const void* logits, int32_t dtype, int64_t N, int64_t V, in
                      float* lse_out, float* gathered_out, float* coverage_out, void* workspace,
                      size_t workspace_bytes, void* stream) {
   return opd::loss_call(logits, dtype, N, V, ld, cache, estimator, k, M, mask, opts, loss, dlogits,
-                        lse_out, gathered_out, coverage_out, workspace, workspace_bytes, stream);
+                        lse_out, gathered_out, coverage_out, workspace, workspace_bytes, nullptr,
+                        0, stream);
 }
 
 }  // extern "C"
@@ -294,7 +297,7 @@ int loss_call(const void* logits, int32_t dtype, int64_t N, int64_t V, int64_t l
               const opd_cache* cache, int32_t estimator, int32_t k, int32_t M,
               const uint8_t* mask, const opd_opts* opts, float* loss, void* dlogits,
               float* lse_out, float* gathered_out, float* coverage_out, void* workspace,
-              size_t workspace_bytes, void* stream) {
+              size_t workspace_bytes, ScratchFn scratch, size_t scratch_bytes, void* stream) {
   if (!valid_est(estimator)) return OPD_ERR_ESTIMATOR;
   const opd_opts o = opts ? *opts : opd_opts{1.0f, OPD_F32, 0u, 0.2f};
   if (dtype != OPD_F32 && dtype != OPD_BF16) return OPD_ERR_DTYPE;
@@ -335,7 +338,17 @@ int loss_call(const void* logits, int32_t dtype, int64_t N, int64_t V, int64_t l
   Plan plan{false, 1, nvec, 0};
   if (split_wanted(N, o.flags)) {
     const Plan sp = split_plan(N, nvec);
-    if (workspace && workspace_bytes >= sp.ws_bytes && aligned16(workspace)) {
+    if (scratch) {
+      // the no-allocation entry point: the library's static scratch array,
+      // looked up only now that every argument has been checked
+      if (sp.ws_bytes <= scratch_bytes) {
+        workspace = scratch();
+        if (!workspace) return OPD_ERR_HIP;
+        plan = sp;
+      } else if (o.flags & OPD_FLAG_FORCE_SPLITV) {
+        return OPD_ERR_SCRATCH;
+      }
+    } else if (workspace && workspace_bytes >= sp.ws_bytes && aligned16(workspace)) {
       plan = sp;
     } else if (o.flags & OPD_FLAG_FORCE_SPLITV) {
       return OPD_ERR_WORKSPACE;

@@ -134,12 +134,16 @@ hipError_t launch_rowwise(const Args& a, int est, int in_dt, int out_dt, Path pa
 hipError_t launch_split(const Args& a, int est, int in_dt, int out_dt, bool read_row,
                         hipStream_t stream);
 hipError_t launch_topk_sparse(const Args& a, int est, int in_dt, int out_dt, hipStream_t stream);
-// The body of the loss entry point.
+// The body of the loss entry points.  `scratch`, when not NULL, supplies the
+// split path's workspace (at most scratch_bytes) from the library's static
+// array instead of `workspace`; it is called only after every argument check.
+typedef void* (*ScratchFn)();
 int loss_call(const void* logits, int32_t dtype, int64_t N, int64_t V, int64_t ld,
               const ::opd_cache* cache, int32_t estimator, int32_t k, int32_t M,
               const uint8_t* mask, const ::opd_opts* opts, float* loss, void* dlogits,
               float* lse_out, float* gathered_out, float* coverage_out, void* workspace,
-              size_t workspace_bytes, void* stream);
+              size_t workspace_bytes,
+              ScratchFn scratch, size_t scratch_bytes, void* stream);
 
 hipError_t launch_validate(const int32_t* ids, const float* tau, const float* beta, int64_t N,
                            int64_t V, int K, int check_dups, int32_t* violations,

@@ -45,7 +45,7 @@ def test_version_matches_header():
 
 
 def test_status_strings():
-    for code in range(-10, 1):
+    for code in range(-11, 1):
         s = opd.status_string(code)
         assert s and s != "unknown status"
     assert opd.status_string(-100) == "unknown status"
