@@ -188,25 +188,31 @@ def single_thread_baseline(w, est, d, rows: int = 1024):
 
 
 def copy_peak(dev, stream, mib: int = 2048):
-    """GB/s of a plain device-to-device copy of `mib` MiB (read + write bytes)."""
+    """GB/s (bytes read + written) of plain device copies of `mib` MiB of
+    output: fp32 to fp32 (the runtime's copy) and bf16 to fp32 (torch's
+    elementwise conversion, the loss kernels' own 2 + 4 bytes per element).
+    Returns {pattern: GB/s}."""
     import torch
 
     n = mib * (1 << 20) // 4
-    a = torch.ones(n, dtype=torch.float32, device=dev)
-    b = torch.empty_like(a)
-    for _ in range(3):
-        b.copy_(a)
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
-    for _ in range(10):
-        b.copy_(a)
-    e1.record(stream)
-    torch.cuda.synchronize()
-    gbs = 2 * n * 4 * 10 / (e0.elapsed_time(e1) / 1e3) / 1e9
-    del a, b
+    out = torch.empty(n, dtype=torch.float32, device=dev)
+    res = {}
+    for name, src in (("f32_to_f32", torch.ones(n, dtype=torch.float32, device=dev)),
+                      ("bf16_to_f32", torch.ones(n, dtype=torch.bfloat16, device=dev))):
+        for _ in range(3):
+            out.copy_(src)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(10):
+            out.copy_(src)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        res[name] = (src.element_size() + 4) * n * 10 / (e0.elapsed_time(e1) / 1e3) / 1e9
+        del src
+    del out
     torch.cuda.empty_cache()
-    return gbs
+    return res
 
 
 def cpu_baseline(w, est, d, rows: int, threads: int, chunk: int = 512):
@@ -256,6 +262,10 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-mib", type=int, default=2048,
                     help="size of the plain device copy timed for frac_of_copy (0: skip)")
+    ap.add_argument("--rows", type=int, default=0,
+                    help="time only the first ROWS rows of the workload (0 = all)")
+    ap.add_argument("--path", default="auto", choices=("auto", "rowwise", "split"),
+                    help="force the loss call's path (the split path gets its workspace)")
     ap.add_argument("--min-set-gib", type=float, default=1.0,
                     help="rotate input/output copies until the timed steps span this many GiB")
     args = ap.parse_args()
@@ -278,6 +288,11 @@ def main():
         sys.exit(1)
     dev = torch.device("cuda:0")
     w = synth.WORKLOADS[args.workload]
+    if args.rows:
+        # rows are generated independently from the seed: the first ROWS rows
+        w = w.replace(N=min(args.rows, w.N))
+    path_flags = {"auto": 0, "rowwise": opd.FLAG_FORCE_ROWWISE, "split": opd.FLAG_FORCE_SPLITV}[
+        args.path]
     est = args.estimator or w.estimators[0]
     op = args.op
     if op == "topk" and w.k == 0 or op in ("sample", "score", "diag") and w.M == 0:
@@ -301,7 +316,8 @@ def main():
     N = w.N
     in_b = 2 if w.dtype == 1 else 4
     stream = torch.cuda.current_stream()
-    copy_gbs = copy_peak(dev, stream, args.copy_mib) if args.copy_mib else None
+    copies = copy_peak(dev, stream, args.copy_mib) if args.copy_mib else None
+    copy_gbs = max(copies.values()) if copies else None
 
     def loss_inputs():
         kw = {}
@@ -331,7 +347,7 @@ def main():
                          "out": {"loss": torch.empty(N, dtype=torch.float32, device=dev),
                                  "dlogits": torch.empty((N, w.V), dtype=torch.float32,
                                                         device=dev)}})
-        nbytes = opd.workspace_bytes(N, w.V, w.dtype, est, w.k, w.M)
+        nbytes = opd.workspace_bytes(N, w.V, w.dtype, est, w.k, w.M, path_flags)
         ws = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev) if nbytes else None
         counter = [0]
 
@@ -339,7 +355,7 @@ def main():
             b = bufs[counter[0] % sets]
             counter[0] += 1
             opd.loss_fwd_bwd(b["logits"], est, mask=mask, out=b["out"], workspace=ws,
-                             stream=stream, **b["kw"])
+                             stream=stream, flags=path_flags, **b["kw"])
     else:
         if op == "sample":
             u_np = np.stack([synth.uniforms(w.seed + 1, synth.STREAM_SAMPLE, r, w.M)
@@ -418,6 +434,7 @@ def main():
                    "vocab": w.V, "logits_dtype": "bf16" if w.dtype == 1 else "f32",
                    "dlogits_dtype": "f32", "k": w.k, "M": w.M,
                    "path": "split" if nbytes and op == "loss" else "rowwise",
+                   "first_rows_of": synth.WORKLOADS[args.workload].N if args.rows else None,
                    "buffer_sets": sets},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": achieved / PEAK_HBM_GBS,
@@ -430,6 +447,7 @@ def main():
     res["roofline"]["kernels"] = dominant_kernels(op, est, w, nbytes > 0)
     if copy_gbs:
         res["roofline"]["copy_GBps"] = copy_gbs
+        res["roofline"]["copy_patterns_GBps"] = copies
         res["roofline"]["frac_of_copy"] = achieved / copy_gbs
     if op == "loss":
         model = alg + second_read_bytes(w, est, n_valid)
