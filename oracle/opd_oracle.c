@@ -450,10 +450,13 @@ int oracle_coverage_rows(int dtype, const void* logits, int64_t n_rows, int64_t 
 int oracle_cdf(const double* z, int64_t V, double* F) {
   if (!z || !F || V < 1) return -1;
   const double L = log_partition(z, V);
-  double acc = 0.0;
+  /* The running sum is kept in long double (64-bit significand): summed in
+   * double, its rounding error grows to about V 2^-53 of the total, which at
+   * V = 151,936 exceeds the error of a device CDF evaluated in double. */
+  long double acc = 0.0L;
   for (int64_t j = 0; j < V; ++j) {
-    acc += exp(z[j] - L);
-    F[j] = acc;
+    acc += (long double)exp(z[j] - L);
+    F[j] = (double)acc;
   }
   return 0;
 }
