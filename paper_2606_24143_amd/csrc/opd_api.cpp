@@ -189,8 +189,6 @@ opd::CacheArgs row_args(const void* logits, int32_t dtype, int64_t N, int64_t V,
   a.mask = mask;
   a.logp = logp;
   a.lse_out = lse_out;
-  a.G = 1;
-  a.nchunk = a.nvec;
   return a;
 }
 
@@ -444,9 +442,6 @@ int opd_sample_actions(const void* logits, int32_t dtype, int64_t N, int64_t V, 
   opd::CacheArgs a = row_args(logits, dtype, N, V, ld, M, mask, logp, lse_out);
   a.u = uniforms;
   a.ids_out = sampled_ids;
-  // chunks of G vectors, so that a row's chunk sums fit in LDS
-  a.G = (a.nvec + opd::kCdfChunks - 1) / opd::kCdfChunks;
-  a.nchunk = (a.nvec + a.G - 1) / a.G;
   const hipError_t err = launch_cache_chunks(a, opd::CacheOp::Sample, dtype, row_fits(a.nvec, dtype),
                                            (hipStream_t)stream);
   return err == hipSuccess ? OPD_OK : OPD_ERR_HIP;

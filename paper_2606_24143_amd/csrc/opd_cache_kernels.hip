@@ -125,23 +125,6 @@ template <int CTRL>
 __device__ __forceinline__ float dpp_move(float v) {
   return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, false));
 }
-__device__ __forceinline__ float wave_incl_scan(float x) {
-  const int lane = threadIdx.x & 63, rl = lane & 15;
-  float t;
-  t = dpp_move<0x111>(x);  // row_shr:1
-  if (rl >= 1) x += t;
-  t = dpp_move<0x112>(x);  // row_shr:2
-  if (rl >= 2) x += t;
-  t = dpp_move<0x114>(x);  // row_shr:4
-  if (rl >= 4) x += t;
-  t = dpp_move<0x118>(x);  // row_shr:8
-  if (rl >= 8) x += t;
-  t = dpp_move<0x142>(x);  // row_bcast:15
-  if ((lane & 31) >= 16) x += t;
-  t = dpp_move<0x143>(x);  // row_bcast:31
-  if (lane >= 32) x += t;
-  return x;
-}
 
 __device__ __forceinline__ uint32_t block_add_u32(uint32_t v, uint32_t* red) {
 #pragma unroll
@@ -156,222 +139,105 @@ __device__ __forceinline__ uint32_t block_add_u32(uint32_t v, uint32_t* red) {
 }
 
 // ---------------------------------------------------------------- sampling
-
-// Chunk sums of exp(z - m) in index order (chunk = G consecutive vectors),
-// the inclusive prefix of each thread's run of C consecutive chunks, and
-// the wave totals of the runs.
-struct CdfLds {
-  float ls[kCdfChunks];
-  float p[NT];
-  float wt[NW];
-  float red[NW];
-};
-
-enum Pick : int { kCross = 0, kFirst = 1, kLast = 2 };
-
-__device__ __forceinline__ int64_t last_positive(const CdfLds& c, uint32_t lo, uint32_t hi) {
-  for (uint32_t q = hi; q > lo; --q)
-    if (c.ls[q - 1] > 0.f) return q - 1;
-  return -1;
-}
-__device__ __forceinline__ int64_t first_positive(const CdfLds& c, uint32_t lo, uint32_t hi) {
-  for (uint32_t q = lo; q < hi; ++q)
-    if (c.ls[q] > 0.f) return q;
-  return -1;
-}
-
-// One draw: the first element whose cumulative mass exceeds t, located run
-// -> chunk -> element.  Each level subtracts the mass before the chosen
-// entry; where rounding leaves no crossing at a level, the nearest entry of
-// nonzero mass is taken instead, so a drawn element always has positive
-// probability.
-template <class TI>
-__device__ int64_t draw_one(const CdfLds& c, const void* zrow, uint32_t nvec, int tail, uint32_t G,
-                            uint32_t nchunk, uint32_t C, float t, float S, float nm) {
-  int64_t ch;
-  float r = 0.f;
-  int pick = kLast;
-  if (t < S) {
-    // The run prefixes come from a parallel scan and need not be monotone to
-    // the last bit; this bisection keeps p[hi] > t and p[lo - 1] <= t, so it
-    // ends on a crossing either way.
-    uint32_t lo = 0, hi = NT - 1;
-    while (lo < hi) {
-      const uint32_t mid = (lo + hi) >> 1;
-      if (c.p[mid] > t)
-        hi = mid;
-      else
-        lo = mid + 1;
-    }
-    r = fmaxf(t - (lo ? c.p[lo - 1] : 0.f), 0.f);
-    const uint32_t r0 = min(lo * C, nchunk), r1 = min(r0 + C, nchunk);
-    float cum = 0.f;
-    uint32_t q = r0;
-    for (; q < r1; ++q) {
-      const float nc = cum + c.ls[q];
-      if (nc > r) break;
-      cum = nc;
-    }
-    if (q < r1) {
-      ch = q;
-      r = fmaxf(r - cum, 0.f);
-      pick = kCross;
-    } else {
-      ch = last_positive(c, r0, r1);
-      if (ch < 0) {
-        ch = first_positive(c, r1, nchunk);
-        pick = kFirst;
-        if (ch < 0) {
-          ch = last_positive(c, 0, r0);
-          pick = kLast;
-        }
-      }
-    }
-  } else {
-    ch = last_positive(c, 0, nchunk);
-  }
-  // element level, with the same sums as the chunk level
-  const uint32_t v0 = (uint32_t)ch * G, v1 = min(v0 + G, nvec);
-  float cum = 0.f;
-  int64_t first = -1, last = -1, cross = -1;
-  for (uint32_t v = v0; v < v1; ++v) {
-    float f[4];
-    unpack<TI>(load_vec<TI>(zrow, v, nvec, tail), f);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const float w = ez(f[e], nm);
-      const int64_t j = (int64_t)v * 4 + e;
-      if (w > 0.f) {
-        if (first < 0) first = j;
-        last = j;
-      }
-      const float nc = cum + w;
-      if (cross < 0 && nc > r) cross = j;
-      cum = nc;
-    }
-  }
-  if (pick == kFirst) return first;
-  if (pick == kCross && cross >= 0) return cross;
-  return last;
-}
-
-template <class TI, int NSLOT>
-__global__ void __launch_bounds__(NT) k_sample(CacheArgs a) {
-  __shared__ CdfLds c;
-  const int tid = threadIdx.x;
-  const int64_t row = xcd_remap(blockIdx.x, gridDim.x);
-  const int M = a.K;
-  if (a.mask && a.mask[row] == 0) {
-    for (int i = tid; i < M; i += NT) {
-      a.ids_out[row * M + i] = 0;
-      if (a.logp) a.logp[row * M + i] = 0.f;
-    }
-    if (tid == 0 && a.lse_out) a.lse_out[row] = 0.f;
-    return;
-  }
-  const void* zrow = (const char*)a.logits + row * a.ld * TI::BYTES;
-  const uint32_t nvec = (uint32_t)a.nvec, G = (uint32_t)a.G, nchunk = (uint32_t)a.nchunk;
-  float m, nm;
-  if constexpr (NSLOT > 0) {
-    // G == 1: chunk q is vector q
-    typename TI::Vec x[NSLOT];
-    load_row<TI, NSLOT>(zrow, nvec, a.tail, tid, x);
-    m = block_max<NW>(lane_max<TI, NSLOT>(x), c.red);
-#pragma unroll
-    for (int s = 0; s < NSLOT; ++s) keep_packed(x[s]);
-    nm = -m * kLog2e;
-#pragma unroll
-    for (int s = 0; s < NSLOT; ++s) {
-      const uint32_t b = slot_base<NT>(s, nvec);
-      if ((uint32_t)(s * NT + NT) <= nvec || slot_owns<NT>(s, b, tid, nvec))
-        c.ls[b + tid] = vec_sumexp<TI>(x[s], nm, 0.f);
-    }
-  } else {
-    float mx = kNegInf;
-    for (uint32_t v = tid; v < nvec; v += NT) {
-      float f[4];
-      unpack<TI>(load_vec<TI>(zrow, v, nvec, a.tail), f);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) mx = fmaxf(mx, f[e]);
-    }
-    m = block_max<NW>(mx, c.red);
-    nm = -m * kLog2e;
-    for (uint32_t q = tid; q < nchunk; q += NT) {
-      const uint32_t v1 = min(q * G + G, nvec);
-      float acc = 0.f;
-      for (uint32_t v = q * G; v < v1; ++v) acc = vec_sumexp<TI>(load_vec<TI>(zrow, v, nvec, a.tail), nm, acc);
-      c.ls[q] = acc;
-    }
-  }
-  __syncthreads();
-
-  // runs of C consecutive chunks per thread, and their block-wide prefix
-  const uint32_t C = (nchunk + NT - 1) / NT;
-  {
-    const uint32_t r0 = min((uint32_t)tid * C, nchunk), r1 = min(r0 + C, nchunk);
-    float run = 0.f;
-    for (uint32_t q = r0; q < r1; ++q) run += c.ls[q];
-    const float incl = wave_incl_scan(run);
-    if ((tid & 63) == 63) c.wt[tid >> 6] = incl;
-    __syncthreads();
-    float before = 0.f;
-    for (int w = 0; w < (tid >> 6); ++w) before += c.wt[w];
-    c.p[tid] = before + incl;
-  }
-  float S = 0.f;
-#pragma unroll
-  for (int w = 0; w < NW; ++w) S += c.wt[w];  // equals p[NT - 1] bit for bit
-  __syncthreads();
-
-  const float L = m + logf(S);
-  if (tid == 0 && a.lse_out) a.lse_out[row] = L;
-  // a NaN or +inf logit, or a row of -inf, leaves S NaN: no distribution
-  const bool defined = S > 0.f && S <= 3.4028235e38f;
-  for (int i = tid; i < M; i += NT) {
-    const float u = a.u[row * M + i];
-    int32_t id = -1;
-    float lp = __builtin_nanf("");
-    if (defined && u >= 0.f && u < 1.f) {
-      const int64_t j = draw_one<TI>(c, zrow, nvec, a.tail, G, nchunk, C, u * S, S, nm);
-      id = (int32_t)j;
-      lp = load_elem<TI>(zrow, j) - L;
-    }
-    a.ids_out[row * M + i] = id;
-    if (a.logp) a.logp[row * M + i] = lp;
-  }
-}
-
-// ---------------------------------------------------------------- sampling, streamed
-
-// Draws read each row once, so the common case is organised for overlap
-// rather than residency: 256-lane workgroups with about 17 KiB of LDS,
-// several per CU, so one row's prefix and draws overlap other rows' reads.
-// The index-order CDF is kept as chunk records.  A chunk is 128 consecutive
-// vectors (512 elements); the 16 lanes of one DPP row load it with eight
-// instructions, each covering 16 consecutive vectors (128 bytes of bf16), so
-// every load is coalesced.  Its record is the chunk max m_q (a DPP row max)
-// and s_q = sum exp(z - m_q) (per-lane sums in load order, then a DPP row
-// scan).  After the row, each record is scaled to the row max M
-// (s'_q = s_q f_q, f_q = exp(m_q - M)), each thread sums its run of C
-// consecutive chunks in order, and a block scan gives the run prefixes.  One
-// wavefront per draw then finds the run (ballot over the prefixes), the
-// chunk (a wave scan of the run's records and a ballot), and the element (a
-// wave scan over the chunk in index order, two vectors per lane, at the same
-// weights exp(z - m_q) f_q).  Where rounding leaves no crossing at a level,
-// the nearest entry of nonzero mass is taken, as in the resident kernel.
+// Draws by inversion of the index-order CDF of softmax(z) (Sec. 4.1, Stage 1:
+// the rollout samples at temperature 1 with no top-p or top-k truncation,
+// App. B): draw i is the first index whose cumulative probability exceeds
+// u_i.  The CDF is evaluated in double precision, so a draw is the one exact
+// arithmetic gives unless u_i lies within about 1e-14 of a cumulative value.
+//
+// One 256-lane workgroup per row, several per CU; the row is read once.  It
+// is cut into at most 2048 chunks of CV = G * 128 consecutive vectors (G * 512
+// elements; G = 1 up to V = 1,048,576).  The 16 lanes of one DPP row take one
+// chunk in steps of 128 vectors, eight coalesced loads per lane per step
+// (each instruction covers 16 consecutive vectors).  A chunk's record is its
+// maximum m_q (fp32, exact) and s_q = sum exp(z - m_q) in double.  After the
+// row, each record is scaled to the row maximum M (s'_q = s_q f_q, f_q =
+// exp(m_q - M)), each thread sums a run of C consecutive chunks, and a block
+// scan gives the run prefixes.  One wavefront per draw then finds the run
+// (a ballot over the prefixes), the chunk (a wave scan of the run's records)
+// and the element (wave scans over the chunk in index order, two vectors per
+// lane, with the very terms the record summed).  Where rounding leaves no
+// crossing at a level, the nearest entry of nonzero mass is taken, so a drawn
+// id always has positive probability.
 constexpr int kSmpThreads = 256;
 constexpr int kSmpWaves = kSmpThreads / 64;
-constexpr int kSmpLoads = 8;                          // loads per lane per chunk
-constexpr int kSmpChunkVecs = 16 * kSmpLoads;         // vectors per chunk (128)
-constexpr int kSmpMaxChunks = 2048;                   // records per row: V <= 1,048,576
+constexpr int kSmpLoads = 8;                   // loads per lane per step
+constexpr int kSmpStepVecs = 16 * kSmpLoads;   // vectors per DPP-row step (128)
+constexpr int kSmpMaxChunks = 2048;            // records per row
+
+// exp(z - m) in double for a logit z <= m (z = -inf gives 0; NaN and +inf
+// logits are caught by the rows' fp32 checks), table-driven (Tang, ACM TOMS
+// 15(2), 1989): z - m = (n / 32) ln 2 + r with |r| below about ln 2 / 64,
+// exp(z - m) = 2^(n >> 5) 2^((n & 31) / 32) exp(r), and exp(r) by its Taylor
+// polynomial to r^5 (truncation below 3e-15 relative).  Only the reduced
+// argument r needs double precision: n may be any integer near
+// (z - m) 32 / ln 2, so it comes from fp32 arithmetic, and it enters the
+// double arithmetic through its bits (2^52 + 2^31 + n has n in its low word)
+// rather than a conversion.  ln 2 / 32 is split in the Cody-Waite way (the
+// high part's 32 significant bits make n times it exact for |n| < 2^21).
+// 2^(n >> 5) goes into the exponent field by an integer add; below 2^-1000
+// the term is 0 (such terms are below 1e-300 of the largest).  The 32 table
+// entries fill one row of the LDS banks, so the lanes' lookups never
+// conflict.
+constexpr int kExpTab = 32;
+constexpr float kInvStepF = 46.16624130844683f;              // 32 / ln 2
+constexpr double kStepHi = 6.93147180369123816490e-01 / 32.0;
+constexpr double kStepLo = 1.90821492927058770002e-10 / 32.0;
+constexpr double kMagic = 4503601774854144.0;                // 2^52 + 2^31
 
 struct SmpLds {
-  float m[kSmpMaxChunks];  // chunk max
-  float s[kSmpMaxChunks];  // chunk sum at its max; then at the row max
-  float p[kSmpThreads];    // inclusive prefix of the runs
-  float wt[kSmpWaves];
+  double s[kSmpMaxChunks];  // chunk sum at its max; then at the row max
+  float m[kSmpMaxChunks];   // chunk max
+  double p[kSmpThreads];    // inclusive prefix of the runs
+  double tab[kExpTab];      // 2^(j / 32)
+  double wt[kSmpWaves];
   float red[kSmpWaves];
 };
+
+// The term for one fp32 logit z against the chunk max m (md = m in double).
+// The single expression both the chunk records and the draws use, so the
+// draws recompute bit for bit the terms the records summed.
+__device__ __forceinline__ double term(float z, float m, double md, const double* tab) {
+  // n: an integer within about 0.5 of (z - m) 32 / ln 2 (z - m is rounded
+  // relative to itself, not to m).  Below -32000 (z - m < -693, a term below
+  // 1e-301 of the largest; also -inf) the term is 0, and n is clamped only so
+  // that the conversion stays defined.
+  const float x = (z - m) * kInvStepF;
+  const bool live = x > -32000.f;
+  const int n = (int)__builtin_rintf(fmaxf(x, -32000.f));
+  const double nd =
+      __builtin_bit_cast(double, (0x4330000000000000ull | (uint64_t)(uint32_t)(n + 0x80000000u))) -
+      kMagic;
+  const double d = (double)z - md;
+  double r = fma(-nd, kStepHi, d);
+  r = fma(-nd, kStepLo, r);
+  double p = fma(r, 1.0 / 120.0, 1.0 / 24.0);
+  p = fma(p, r, 1.0 / 6.0);
+  p = fma(p, r, 0.5);
+  p = fma(p, r, 1.0);
+  p = fma(p, r, 1.0);
+  const double t = tab[n & (kExpTab - 1)] * p;  // in [0.98, 2.05]
+  const int k = n >> 5;                          // >= -1000 where live
+  const uint64_t bits = __builtin_bit_cast(uint64_t, t) + ((uint64_t)(int64_t)k << 52);
+  return live ? __builtin_bit_cast(double, bits) : 0.0;
+}
+
+// exp(x) for one double x <= 0 (the row-max scale of a chunk record),
+// through the same steps
+__device__ __forceinline__ double exp_neg(double x, const double* tab) {
+  const float xs = (float)x * kInvStepF;
+  const bool live = xs > -32000.f;
+  const int n = (int)__builtin_rintf(fmaxf(xs, -32000.f));
+  const double nd = (double)n;
+  double r = fma(-nd, kStepHi, x);
+  r = fma(-nd, kStepLo, r);
+  double p = fma(r, 1.0 / 120.0, 1.0 / 24.0);
+  p = fma(p, r, 1.0 / 6.0);
+  p = fma(p, r, 0.5);
+  p = fma(p, r, 1.0);
+  p = fma(p, r, 1.0);
+  return live ? __builtin_ldexp(tab[n & (kExpTab - 1)] * p, n >> 5) : 0.0;
+}
 
 // max over the 16 lanes of a DPP row, in every lane of the row
 __device__ __forceinline__ float row16_max(float x) {
@@ -381,23 +247,27 @@ __device__ __forceinline__ float row16_max(float x) {
   x = fmaxf(x, dpp_move<0x4E>(x));   // quad_perm [2,3,0,1]
   return x;
 }
-// inclusive prefix sum within each DPP row of 16 lanes
-__device__ __forceinline__ float row16_scan(float x) {
-  const int rl = threadIdx.x & 15;
-  float t;
-  t = dpp_move<0x111>(x);  // row_shr:1
-  if (rl >= 1) x += t;
-  t = dpp_move<0x112>(x);  // row_shr:2
-  if (rl >= 2) x += t;
-  t = dpp_move<0x114>(x);  // row_shr:4
-  if (rl >= 4) x += t;
-  t = dpp_move<0x118>(x);  // row_shr:8
-  if (rl >= 8) x += t;
+// sum over the 16 lanes of a DPP row (butterfly, fixed order), in every lane
+__device__ __forceinline__ double row16_sum(double x) {
+#pragma unroll
+  for (int o = 8; o >= 1; o >>= 1) x += __shfl_xor(x, o, 64);
+  return x;
+}
+// inclusive prefix sum over the 64 lanes of a wavefront, in double
+__device__ __forceinline__ double wave_incl_scan_f64(double x) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const double t = __shfl_up(x, o, 64);
+    if (lane >= o) x += t;
+  }
   return x;
 }
 
 __device__ __forceinline__ int first_lane(uint64_t b) { return b ? __ffsll((long long)b) - 1 : -1; }
 __device__ __forceinline__ int last_lane(uint64_t b) { return b ? 63 - __clzll((long long)b) : -1; }
+
+enum Pick : int { kCross = 0, kFirst = 1, kLast = 2 };
 
 // First (or last) chunk in [lo, hi) with positive mass, by wave ballots; -1 if none.
 __device__ __forceinline__ int64_t chunk_positive(const SmpLds& c, int64_t lo, int64_t hi,
@@ -406,27 +276,46 @@ __device__ __forceinline__ int64_t chunk_positive(const SmpLds& c, int64_t lo, i
   if (!last) {
     for (int64_t b = lo; b < hi; b += 64) {
       const int64_t q = b + lane;
-      const int f = first_lane(__ballot(q < hi && c.s[q] > 0.f));
+      const int f = first_lane(__ballot(q < hi && c.s[q] > 0.0));
       if (f >= 0) return b + f;
     }
   } else {
     for (int64_t b = hi; b > lo; b -= 64) {
       const int64_t q = b - 64 + lane;
-      const int l = last_lane(__ballot(q >= lo && q < b && c.s[q] > 0.f));
+      const int l = last_lane(__ballot(q >= lo && q < b && c.s[q] > 0.0));
       if (l >= 0) return b - 64 + l;
     }
   }
   return -1;
 }
 
+// The eight terms of this lane's two vectors of the 128-vector step that
+// starts at vector v0 (vectors at or past the chunk end c1 give 0).
+template <class TI>
+__device__ __forceinline__ void step_terms(const void* zrow, uint32_t v0, uint32_t c1,
+                                           uint32_t nvec, int tail, float mq, const double* tab,
+                                           double (&w)[8]) {
+  const double md = (double)mq;
+  const uint32_t v = v0 + 2u * (uint32_t)(threadIdx.x & 63);
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const bool in = v + h < c1;  // inside the chunk (and so the row)
+    float f[4];
+    unpack<TI>(in ? load_vec<TI>(zrow, v + h, nvec, tail) : neg_inf_vec<TI>(), f);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) w[4 * h + e] = in ? term(f[e], mq, md, tab) : 0.0;
+  }
+}
+
 // One draw by one wavefront (the result is wave-uniform): the first element
 // whose cumulative mass exceeds t = u * S.
 template <class TI>
 __device__ int64_t smp_draw(const SmpLds& c, const void* zrow, uint32_t nvec, int tail,
-                            uint32_t nchunk, uint32_t C, float t, float S, float nM) {
+                            uint32_t CV, uint32_t nchunk, uint32_t C, double t, double S,
+                            double Md) {
   const int lane = threadIdx.x & 63;
   int64_t q = -1;
-  float r = 0.f;
+  double r = 0.0;
   int pick = kLast;
   if (t < S) {
     // run: the first i with p[i] > t (each lane looks at 4 entries)
@@ -436,20 +325,20 @@ __device__ int64_t smp_draw(const SmpLds& c, const void* zrow, uint32_t nvec, in
       if (c.p[4 * lane + k] > t) li = 4 * lane + k;
     const int fl = first_lane(__ballot(li >= 0));
     const int i = __shfl(li, fl < 0 ? 0 : fl, 64);  // fl >= 0: p[255] = S > t
-    r = fmaxf(t - (i ? c.p[i - 1] : 0.f), 0.f);
+    r = fmax(t - (i ? c.p[i - 1] : 0.0), 0.0);
     // chunk within the run (C <= 8 chunks, one per lane)
     const uint32_t r0 = min((uint32_t)i * C, nchunk), r1 = min(r0 + C, nchunk);
     const uint32_t qq = r0 + (uint32_t)lane;
-    const float sq = qq < r1 ? c.s[qq] : 0.f;
-    const float incl = wave_incl_scan(sq);
+    const double sq = qq < r1 ? c.s[qq] : 0.0;
+    const double incl = wave_incl_scan_f64(sq);
     const int cl = first_lane(__ballot(qq < r1 && incl > r));
     if (cl >= 0) {
-      const float before = cl > 0 ? __shfl(incl, cl - 1, 64) : 0.f;
+      const double before = cl > 0 ? __shfl(incl, cl - 1, 64) : 0.0;
       q = r0 + cl;
-      r = fmaxf(r - before, 0.f);
+      r = fmax(r - before, 0.0);
       pick = kCross;
     } else {
-      const int ll = last_lane(__ballot(qq < r1 && sq > 0.f));
+      const int ll = last_lane(__ballot(qq < r1 && sq > 0.0));
       if (ll >= 0) {
         q = r0 + ll;
       } else {
@@ -465,62 +354,149 @@ __device__ int64_t smp_draw(const SmpLds& c, const void* zrow, uint32_t nvec, in
     q = chunk_positive(c, 0, nchunk, true);
   }
   if (q < 0) return -1;  // no chunk of positive mass (excluded by S > 0)
-  // element within chunk q: lane l holds vectors 2l and 2l + 1 of the chunk
-  // (elements 8l .. 8l + 7, in index order)
+  // element within chunk q, in steps of 128 vectors: lane l holds vectors
+  // 2l and 2l + 1 of the step (elements 8l .. 8l + 7, in index order)
   const float mq = c.m[q];
-  const float nmq = -mq * kLog2e, fq = fast_exp2(fmaf(mq, kLog2e, nM));
-  const uint32_t v = (uint32_t)q * kSmpChunkVecs + 2u * (uint32_t)lane;
-  float wl[8];
-#pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    const bool in = v + h < nvec;
-    float f[4];
-    unpack<TI>(in ? load_vec<TI>(zrow, v + h, nvec, tail) : neg_inf_vec<TI>(), f);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) wl[4 * h + e] = in ? ez(f[e], nmq) : 0.f;
-  }
-  float lsum = 0.f;
-  int e_first = -1, e_last = -1;
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    lsum += wl[e];
-    if (wl[e] > 0.f) {
-      if (e_first < 0) e_first = e;
-      e_last = e;
-    }
-  }
-  int vl = -1, el = -1;  // chosen lane and element in it
+  const double fq = exp_neg((double)mq - Md, c.tab);
+  const uint32_t c0 = (uint32_t)q * CV, c1 = min(c0 + CV, nvec);
   if (pick == kCross) {
-    const float incl = wave_incl_scan(lsum);
-    vl = first_lane(__ballot(incl * fq > r));
-    if (vl >= 0) {
-      float cum = vl > 0 ? __shfl(incl, vl - 1, 64) : 0.f;
-      int ec = -1;
+    double acc = 0.0;  // unscaled mass of the earlier steps
+    for (uint32_t v0 = c0; v0 < c1; v0 += kSmpStepVecs) {
+      double w[8];
+      step_terms<TI>(zrow, v0, c1, nvec, tail, mq, c.tab, w);
+      double lsum = 0.0;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        cum += wl[e];
-        if (ec < 0 && cum * fq > r) ec = e;
+      for (int e = 0; e < 8; ++e) lsum += w[e];
+      const double incl = acc + wave_incl_scan_f64(lsum);
+      const int vl = first_lane(__ballot(incl * fq > r));
+      if (vl >= 0) {
+        double cum = vl > 0 ? __shfl(incl, vl - 1, 64) : acc;
+        int ec = -1;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          cum += w[e];
+          if (ec < 0 && cum * fq > r) ec = e;
+        }
+        const int el = __shfl(ec, vl, 64);
+        if (el >= 0) return ((int64_t)v0 + 2 * vl) * 4 + el;
+        break;  // rounding: no element crossing in that lane
       }
-      el = __shfl(ec, vl, 64);
-      if (el < 0) vl = -1;  // rounding: no element crossing in that lane
+      acc = __shfl(incl, 63, 64);
     }
-    if (vl < 0) pick = kLast;
+    pick = kLast;  // rounding left no crossing: the last entry of mass
   }
-  if (pick == kFirst) {
-    vl = first_lane(__ballot(e_first >= 0));
-    el = __shfl(e_first, vl < 0 ? 0 : vl, 64);
-  } else if (pick == kLast) {
-    vl = last_lane(__ballot(e_last >= 0));
-    el = __shfl(e_last, vl < 0 ? 0 : vl, 64);
+  // first (or last) element of positive mass in the chunk
+  const bool last = pick == kLast;
+  const uint32_t nsteps = (c1 - c0 + kSmpStepVecs - 1) / kSmpStepVecs;
+  for (uint32_t k = 0; k < nsteps; ++k) {
+    const uint32_t v0 = c0 + (last ? nsteps - 1 - k : k) * kSmpStepVecs;
+    double w[8];
+    step_terms<TI>(zrow, v0, c1, nvec, tail, mq, c.tab, w);
+    int ef = -1, eb = -1;
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      if (w[e] > 0.0) {
+        if (ef < 0) ef = e;
+        eb = e;
+      }
+    const int vl = last ? last_lane(__ballot(eb >= 0)) : first_lane(__ballot(ef >= 0));
+    if (vl >= 0) return ((int64_t)v0 + 2 * vl) * 4 + __shfl(last ? eb : ef, vl, 64);
   }
-  if (vl < 0 || el < 0) return -1;
-  return ((int64_t)q * kSmpChunkVecs + 2 * vl) * 4 + el;
+  return -1;
 }
 
-template <class TI>
-__global__ void __launch_bounds__(kSmpThreads) k_sample_stream(CacheArgs a) {
-  constexpr int T = kSmpThreads, W = kSmpWaves, R = kSmpLoads, CV = kSmpChunkVecs;
+// The chunk pass of one DPP row over chunk q (vectors [q CV, q CV + CV)): the
+// chunk max and the double sum of exp(z - max), in every lane of the row.
+// WIDE (more than one step per chunk) takes a max pass and a term pass over
+// the chunk; otherwise the step's eight vectors stay in registers.
+template <class TI, bool WIDE>
+__device__ __forceinline__ void chunk_record(const void* zrow, uint32_t q, uint32_t CV,
+                                             uint32_t nvec, int tail, const double* tab,
+                                             float& mq_out, double& sq_out) {
   typedef typename TI::Vec Vec;
+  constexpr int R = kSmpLoads;
+  const uint32_t rl = threadIdx.x & 15;
+  const bool ragged = tail != TI::EPV;
+  const uint32_t c0 = q * CV, c1 = min(c0 + CV, nvec);
+  Vec x[R];
+  // all R loads are issued before any is used; lanes past the chunk, and
+  // elements past V, then become -inf through per-dword selects
+  auto load_step = [&](uint32_t s0) {
+#pragma unroll
+    for (int b = 0; b < R; ++b) {
+      const uint32_t v = s0 + rl + 16u * b;
+      if constexpr (WIDE)
+        x[b] = ld_cached<TI>(zrow, min(v, nvec - 1));
+      else
+        x[b] = ld_nt<TI>(zrow, min(v, nvec - 1));
+    }
+#pragma unroll
+    for (int b = 0; b < R; ++b) {
+      const uint32_t v = s0 + rl + 16u * b;
+      const Vec t = tail_masked<TI>(x[b], tail);
+      const Vec n = neg_inf_vec<TI>();
+      const bool out = v >= c1, last = ragged && v == nvec - 1;
+#pragma unroll
+      for (int d = 0; d < (int)(sizeof(Vec) / 4); ++d)
+        x[b][d] = out ? n[d] : (last ? t[d] : x[b][d]);
+    }
+  };
+  // the plain sum of the elements turns NaN for a NaN in the chunk (and for
+  // +inf with -inf; +inf alone shows as an infinite maximum): either leaves
+  // the row without a distribution
+  float chk = 0.f;
+  auto step_max = [&]() {
+    float lm = kNegInf;
+#pragma unroll
+    for (int b = 0; b < R; ++b) {
+      float f[4];
+      unpack<TI>(x[b], f);
+      lm = fmaxf(lm, fmaxf(fmaxf(f[0], f[1]), fmaxf(f[2], f[3])));
+      chk += (f[0] + f[1]) + (f[2] + f[3]);
+    }
+    return lm;
+  };
+  auto step_sum = [&](float m, double acc) {
+    const double md = (double)m;
+#pragma unroll
+    for (int b = 0; b < R; ++b) {
+      float f[4];
+      unpack<TI>(x[b], f);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) acc += term(f[e], m, md, tab);
+    }
+    return acc;
+  };
+  float lm = kNegInf;
+  if constexpr (!WIDE) {
+    load_step(c0);
+    lm = step_max();
+  } else {
+    for (uint32_t s0 = c0; s0 < c1; s0 += kSmpStepVecs) {
+      load_step(s0);
+      lm = fmaxf(lm, step_max());
+    }
+  }
+  const float mq = row16_max(lm);
+  double ls = 0.0;
+  const bool undefined = __ballot(chk != chk || mq == __builtin_huge_valf()) != 0;
+  if (mq != kNegInf && !undefined) {  // an all -inf chunk has no mass
+    if constexpr (!WIDE) {
+      ls = step_sum(mq, 0.0);
+    } else {
+      for (uint32_t s0 = c0; s0 < c1; s0 += kSmpStepVecs) {
+        load_step(s0);
+        ls = step_sum(mq, ls);
+      }
+    }
+  }
+  mq_out = mq;
+  sq_out = undefined ? __builtin_nan("") : row16_sum(ls);
+}
+
+template <class TI, bool WIDE>
+__global__ void __launch_bounds__(kSmpThreads) k_sample(CacheArgs a) {
+  constexpr int T = kSmpThreads, W = kSmpWaves;
   __shared__ SmpLds c;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int64_t row = xcd_remap(blockIdx.x, gridDim.x);
@@ -533,88 +509,69 @@ __global__ void __launch_bounds__(kSmpThreads) k_sample_stream(CacheArgs a) {
     if (tid == 0 && a.lse_out) a.lse_out[row] = 0.f;
     return;
   }
+  if (tid < kExpTab) c.tab[tid] = exp2((double)tid / kExpTab);
+  __syncthreads();
   const void* zrow = (const char*)a.logits + row * a.ld * TI::BYTES;
   const uint32_t nvec = (uint32_t)a.nvec;
+  const uint32_t steps = (nvec + kSmpStepVecs - 1) / kSmpStepVecs;
+  const uint32_t G = (steps + kSmpMaxChunks - 1) / kSmpMaxChunks;  // steps per chunk
+  const uint32_t CV = G * kSmpStepVecs;
   const uint32_t nchunk = (nvec + CV - 1) / CV;  // <= kSmpMaxChunks
-  const bool ragged = a.tail != TI::EPV;
 
   // one pass over the row: DPP row k of wave w takes chunks 4 w + k,
-  // 4 w + k + 4 W, ...; its lane l loads vectors 16 b + l of the chunk
+  // 4 w + k + 4 W, ...
   const uint32_t rowk = (uint32_t)lane >> 4, rl = (uint32_t)lane & 15;
   float lmax = kNegInf;
   for (uint32_t q0 = 4u * w; q0 < nchunk; q0 += 4u * W) {  // wave-uniform
     const uint32_t q = q0 + rowk;
-    const uint32_t v0 = q * CV + rl;
-    Vec x[R];
-#pragma unroll
-    for (int b = 0; b < R; ++b) x[b] = ld_nt<TI>(zrow, min(v0 + 16u * b, nvec - 1));
-    float lm = kNegInf;
-#pragma unroll
-    for (int b = 0; b < R; ++b) {
-      const uint32_t v = v0 + 16u * b;
-      if (v >= nvec) x[b] = neg_inf_vec<TI>();
-      else if (ragged && v == nvec - 1) x[b] = tail_masked<TI>(x[b], a.tail);
-      float f[4];
-      unpack<TI>(x[b], f);
-      lm = fmaxf(lm, fmaxf(fmaxf(f[0], f[1]), fmaxf(f[2], f[3])));
-    }
-    const float mq = row16_max(lm);
-    float ls = 0.f;
-    if (mq != kNegInf) {  // an all -inf chunk has no mass (and no NaN)
-      const float nm = -mq * kLog2e;
-#pragma unroll
-      for (int b = 0; b < R; ++b) {
-        float f[4];
-        unpack<TI>(x[b], f);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) ls += ez(f[e], nm);
-      }
-    }
-    const float sq = row16_scan(ls);
+    float mq;
+    double sq;
+    chunk_record<TI, WIDE>(zrow, min(q, nchunk - 1), CV, nvec, a.tail, c.tab, mq, sq);
     if (rl == 15 && q < nchunk) {
       c.m[q] = mq;
       c.s[q] = sq;
     }
-    lmax = fmaxf(lmax, lm);
+    if (q < nchunk) lmax = fmaxf(lmax, mq);
   }
   const float Mx = block_max<W>(lmax, c.red);  // ends with a barrier: records visible
-  const float nM = -Mx * kLog2e;
+  const double Md = (double)Mx;
   // records at the row max; runs of C consecutive chunks per thread
   const uint32_t C = (nchunk + T - 1) / T;
   {
     const uint32_t r0 = min((uint32_t)tid * C, nchunk), r1 = min(r0 + C, nchunk);
-    float run = 0.f;
+    double run = 0.0;
     for (uint32_t q = r0; q < r1; ++q) {
       const float mq = c.m[q];
-      const float sq = mq == kNegInf ? 0.f : c.s[q] * fast_exp2(fmaf(mq, kLog2e, nM));
+      const double sq = mq == kNegInf ? 0.0 : c.s[q] * exp_neg((double)mq - Md, c.tab);
+      // (a NaN record keeps S NaN: the row has no distribution)
       c.s[q] = sq;
       run += sq;
     }
-    const float incl = wave_incl_scan(run);
+    const double incl = wave_incl_scan_f64(run);
     if (lane == 63) c.wt[w] = incl;
     __syncthreads();
-    float before = 0.f;
+    double before = 0.0;
     for (int k = 0; k < w; ++k) before += c.wt[k];
     c.p[tid] = before + incl;
   }
-  float S = 0.f;
+  double S = 0.0;
 #pragma unroll
   for (int k = 0; k < W; ++k) S += c.wt[k];  // equals p[T - 1] bit for bit
   __syncthreads();
 
-  const float L = Mx + logf(S);
-  if (tid == 0 && a.lse_out) a.lse_out[row] = L;
+  const double L = Md + log(S);
+  if (tid == 0 && a.lse_out) a.lse_out[row] = (float)L;
   // a NaN or +inf logit, or a row of -inf, leaves S NaN or 0: no distribution
-  const bool defined = S > 0.f && S <= 3.4028235e38f;
+  const bool defined = S > 0.0 && S <= 1.7976931348623157e308;
   for (int i = w; i < M; i += W) {  // one draw per wavefront
     const float u = a.u[row * M + i];
     int32_t id = -1;
     float lp = __builtin_nanf("");
     if (defined && u >= 0.f && u < 1.f) {
-      const int64_t j = smp_draw<TI>(c, zrow, nvec, a.tail, nchunk, C, u * S, S, nM);
+      const int64_t j = smp_draw<TI>(c, zrow, nvec, a.tail, CV, nchunk, C, (double)u * S, S, Md);
       if (j >= 0) {
         id = (int32_t)j;
-        lp = load_elem<TI>(zrow, j) - L;
+        lp = (float)((double)load_elem<TI>(zrow, j) - L);
       }
     }
     if (lane == 0) {
@@ -923,38 +880,57 @@ __global__ void __launch_bounds__(NT) k_topk(CacheArgs a) {
 // The top-k support of rows of at least 16,384 entries, for k <= 64, reads
 // each row once: 256-lane workgroups with about 38 KiB of LDS, four per CU.
 // Each lane keeps the running maximum of the values it has seen.  After each
-// tile of 8 coalesced loads per lane, the k-th largest of the wave's 64
-// running maxima (a radix select over their order keys by ballots) is a
-// lower bound on the row's k-th largest (k lanes have each seen an element
-// at least that large), updated every fourth tile; the bound only rises.
-// Elements not below the wave's current bound, and NaNs, are appended to
-// its LDS buffer by ballot compaction, skipping every vector whose maximum
-// is below the bound in all lanes.  At the end the largest of the four wave
-// bounds is still a lower bound, every element at or above it is in some
-// buffer, and a block sort of those (at most 256) gives the support.  A row
-// whose buffers overflow (many equal large values) or that leaves more than
-// 256 candidates is marked, and a second launch runs the resident kernel on
-// the marked rows only.
+// tile of 8 coalesced loads per lane, and before any of the tile's elements
+// is kept, the wave raises its bound to the k-th largest of its 64 running
+// maxima (k lanes have each seen an element at least that large, so it is a
+// lower bound on the row's k-th largest; found by a radix select over order
+// keys with ballots, 16 key bits for bf16 rows), and to the largest bound
+// any wave of the workgroup has published in LDS (each is such a lower
+// bound).  The bound only rises.  A lane then keeps, in its own LDS slots,
+// the elements of the tile not below the bound (and NaNs): no cross-lane
+// compaction in the stream.  At the end the largest wave bound is still a
+// lower bound, every element at or above it is in some lane's slots, and a
+// block sort of those (at most 256) gives the support.  A row whose lane
+// slots overflow (many equal large values) or that leaves more than 256
+// candidates is marked, and a second launch runs the resident kernel on the
+// marked rows only.
 constexpr int kTkThreads = 256;
 constexpr int kTkWaves = kTkThreads / 64;
 constexpr int kTkLoads = 8;    // vector loads per lane per tile
-constexpr int kTkCap = 1024;   // candidates per wave
+constexpr int kTkSlots = 16;   // candidate slots per lane
 constexpr int kTkMaxK = 64;    // one running maximum per lane bounds k
 constexpr int64_t kTkMinVec = 4096;
 
 struct TkLds {
-  uint64_t buf[kTkWaves][kTkCap];
+  uint64_t buf[kTkSlots][kTkThreads];  // lane-private candidate slots
   uint64_t sbuf[2][kTkThreads];
   uint64_t sel[kTkThreads];
-  uint32_t cnt[kTkWaves];
-  uint32_t theta[kTkWaves];
+  uint32_t theta[kTkWaves];            // published wave bounds (order keys)
   uint32_t nsel;
+  uint32_t over;
   Stats st[kTkWaves];
 };
+
+// The largest key t (low KEEP bits zero) with at least k of the wave's rk
+// >= t: the k-th largest rk, rounded down to the key bits that vary.
+template <int LOWBITS>
+__device__ __forceinline__ uint32_t wave_kth_key(uint32_t rk, int k) {
+  uint32_t t = 0;
+#pragma unroll
+  for (int bit = 31; bit >= LOWBITS; --bit) {
+    const uint32_t c = t | (1u << bit);
+    if ((uint32_t)__popcll(__ballot(rk >= c)) >= (uint32_t)k) t = c;
+  }
+  return t;
+}
 
 template <class TI, bool LSE>
 __global__ void __launch_bounds__(kTkThreads) k_topk_stream(CacheArgs a) {
   constexpr int T = kTkThreads, W = kTkWaves, B = kTkLoads;
+  // bf16 values widened to fp32 have 16 zero low bits, so their order keys
+  // vary in the top 16 bits only (a negative value's low key bits are ones,
+  // which a threshold with zero low bits still admits)
+  constexpr int LOWBITS = TI::BYTES == 2 ? 16 : 0;
   typedef typename TI::Vec Vec;
   __shared__ TkLds sh;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -968,15 +944,20 @@ __global__ void __launch_bounds__(kTkThreads) k_topk_stream(CacheArgs a) {
     if (tid == 0 && a.lse_out) a.lse_out[row] = 0.f;
     return;
   }
+  if (lane == 0) sh.theta[w] = 0u;
+  if (tid == 0) {
+    sh.nsel = 0u;
+    sh.over = 0u;
+  }
+  __syncthreads();
   const void* zrow = (const char*)a.logits + row * a.ld * TI::BYTES;
   const uint32_t nvec = (uint32_t)a.nvec;  // >= kTkMinVec: every wave's first tile is full
   const uint32_t V32 = (uint32_t)a.V;
   float run = kNegInf;  // this lane's running maximum (NaN ignored)
   uint32_t theta = 0;   // the wave's bound as an order key (wave-uniform)
   float thf = kNegInf;  // the same bound as a value
-  uint32_t nb = 0;      // the wave's candidates so far (wave-uniform)
+  uint32_t cnt = 0;     // this lane's candidates so far
   float m = kNegInf, sum = 0.f;
-  uint32_t tile = 0;
   for (uint32_t t0 = (uint32_t)w * 64 * B; t0 < nvec; t0 += W * 64 * B) {  // wave-uniform
     Vec xb[B];
 #pragma unroll
@@ -992,19 +973,13 @@ __global__ void __launch_bounds__(kTkThreads) k_topk_stream(CacheArgs a) {
           if (!(v < nvec && v * 4u + e < V32)) f[e] = kNegInf;
       }
     };
-    // pass 1: vector maxima (NaN ignored) and the tile's
-    float vm[B];
     float tmx = kNegInf;
 #pragma unroll
     for (int b = 0; b < B; ++b) {
       float f[4];
       vals(b, f);
-      vm[b] = fmaxf(fmaxf(f[0], f[1]), fmaxf(f[2], f[3]));
-      tmx = fmaxf(tmx, vm[b]);
+      tmx = fmaxf(tmx, fmaxf(fmaxf(f[0], f[1]), fmaxf(f[2], f[3])));
     }
-    // NaN (or +inf) in this lane's part of the tile: the tile's sum of
-    // exponentials is NaN; without the sums, tested element by element
-    bool nan = false;
     if constexpr (LSE) {
       const float mn = fmaxf(m, tmx);
       if (mn != kNegInf) {
@@ -1017,93 +992,63 @@ __global__ void __launch_bounds__(kTkThreads) k_topk_stream(CacheArgs a) {
 #pragma unroll
           for (int e = 0; e < 4; ++e) acc += fast_exp2(fmaf(f[e], kLog2e, nm));
         }
-        nan = acc != acc;
         sum = fmaf(sum, rescale(m, mn), acc);
         m = mn;
       }
-    } else {
-#pragma unroll
-      for (int b = 0; b < B; ++b) {
-        float f[4];
-        vals(b, f);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) nan = nan || f[e] != f[e];
-      }
     }
     run = fmaxf(run, tmx);
-    // every fourth tile: k lanes of this wave have each seen a value at
-    // least the k-th largest running maximum, found bit by bit with ballots
-    // (the bound only rises)
-    if ((tile++ & 3) == 0) {
-      const uint32_t rk = order_key(__float_as_uint(run));
-      if ((uint32_t)__popcll(__ballot(rk > theta)) >= (uint32_t)k) {
-        uint32_t t = 0;
-        for (int bit = 31; bit >= 0; --bit) {
-          const uint32_t c = t | (1u << bit);
-          if ((uint32_t)__popcll(__ballot(rk >= c)) >= (uint32_t)k) t = c;
-        }
-        theta = t;
-        thf = key_value(t);
-      }
+    // raise the bound before keeping any of the tile's elements
+    const uint32_t rk = order_key(__float_as_uint(run));
+    if ((uint32_t)__popcll(__ballot(rk > theta)) >= (uint32_t)k) {  // wave-uniform
+      theta = wave_kth_key<LOWBITS>(rk, k);
+      if (lane == 0) sh.theta[w] = theta;
     }
-    // candidates: every element not below the bound, and every NaN
-    // (!(x < bound) holds for both); vectors whose maximum is below the
-    // bound and that hold no NaN are skipped by the whole wave
+    uint32_t pub = theta;
+#pragma unroll
+    for (int q = 0; q < W; ++q) pub = max(pub, sh.theta[q]);
+    theta = __builtin_amdgcn_readfirstlane(pub);
+    thf = key_value(theta);
+    // keep every element not below the bound, and every NaN (!(x < bound)
+    // holds for both), in this lane's slots
 #pragma unroll
     for (int b = 0; b < B; ++b) {
-      if (__ballot(!(vm[b] < thf) || nan)) {  // wave-uniform
-        const uint32_t v = t0 + 64u * b + lane;
-        float f[4];
-        vals(b, f);
+      float f[4];
+      vals(b, f);
+      const uint32_t v = t0 + 64u * b + lane;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const bool take = !(f[e] < thf) && (full || (v < nvec && v * 4u + e < V32));
-          const uint64_t mask = __ballot(take);
-          if (mask) {  // wave-uniform
-            const uint32_t pos = nb + (uint32_t)__popcll(mask & ((1ull << lane) - 1ull));
-            if (take && pos < (uint32_t)kTkCap)
-              sh.buf[w][pos] = ((uint64_t)order_key(__float_as_uint(f[e])) << 32) |
+      for (int e = 0; e < 4; ++e) {
+        if (!(f[e] < thf) && (full || (v < nvec && v * 4u + e < V32))) {
+          if (cnt < (uint32_t)kTkSlots)
+            sh.buf[cnt][tid] = ((uint64_t)order_key(__float_as_uint(f[e])) << 32) |
                                (0xFFFFFFFFu - (v * 4u + e));
-            nb += (uint32_t)__popcll(mask);
-          }
+          ++cnt;
         }
       }
     }
   }
-  if (lane == 0) {
-    sh.cnt[w] = nb;
-    sh.theta[w] = theta;
-  }
-  if (tid == 0) sh.nsel = 0u;
+  if (cnt > (uint32_t)kTkSlots) sh.over = 1u;
   float L = 0.f;
   if constexpr (LSE) {
     Stats st = stats_empty();
     st.mz = m;
     st.sz = sum;
-    st = block_merge<false, W>(st, sh.st);  // barriers: counts and bounds visible
+    st = block_merge<false, W>(st, sh.st);  // barriers: bounds and slots visible
     L = st.mz + logf(st.sz);
   } else {
     __syncthreads();
   }
   uint32_t tstar = 0;
-  bool overflow = false;
 #pragma unroll
-  for (int q = 0; q < W; ++q) {
-    tstar = max(tstar, sh.theta[q]);
-    overflow = overflow || sh.cnt[q] > (uint32_t)kTkCap;
-  }
+  for (int q = 0; q < W; ++q) tstar = max(tstar, sh.theta[q]);
+  const bool overflow = sh.over != 0u;
   if (!overflow) {
-    // every element with key >= tstar is in some buffer: each wave's bound
-    // never exceeded tstar while it appended
-#pragma unroll
-    for (int q = 0; q < W; ++q) {
-      const uint32_t n = sh.cnt[q];
-      for (uint32_t i = tid; i < n; i += T) {
-        const uint64_t e = sh.buf[q][i];
-        if ((uint32_t)(e >> 32) >= tstar) {
-          const uint32_t pos = atomicAdd(&sh.nsel, 1u);
-          if (pos < (uint32_t)T) sh.sel[pos] = e;
-        }
+    // every element with key >= tstar is in some lane's slots: no wave's
+    // bound exceeded tstar while it kept elements
+    for (uint32_t i = 0; i < cnt; ++i) {
+      const uint64_t e = sh.buf[i][tid];
+      if ((uint32_t)(e >> 32) >= tstar) {
+        const uint32_t pos = atomicAdd(&sh.nsel, 1u);
+        if (pos < (uint32_t)T) sh.sel[pos] = e;
       }
     }
   }
@@ -1204,7 +1149,6 @@ hipError_t launch_op(const CacheArgs& a, CacheOp op, hipStream_t stream) {
   const dim3 grid((unsigned)a.N), block(NT);
   switch (op) {
     case CacheOp::Sample:
-      hipLaunchKernelGGL((k_sample<TI, NSLOT>), grid, block, 0, stream, a);
       break;
     case CacheOp::Topk:
       if (a.logp || a.lse_out)
@@ -1220,10 +1164,14 @@ hipError_t launch_op(const CacheArgs& a, CacheOp op, hipStream_t stream) {
 
 template <class TI>
 hipError_t launch_dt(const CacheArgs& a, CacheOp op, bool resident, hipStream_t stream) {
-  if (op == CacheOp::Sample &&
-      (a.nvec + kSmpChunkVecs - 1) / kSmpChunkVecs <= (int64_t)kSmpMaxChunks) {
-    hipLaunchKernelGGL((k_sample_stream<TI>), dim3((unsigned)a.N), dim3(kSmpThreads), 0, stream,
-                       a);
+  if (op == CacheOp::Sample) {
+    // more than one 128-vector step per chunk above 2048 steps per row
+    if ((a.nvec + kSmpStepVecs - 1) / kSmpStepVecs <= (int64_t)kSmpMaxChunks)
+      hipLaunchKernelGGL((k_sample<TI, false>), dim3((unsigned)a.N), dim3(kSmpThreads), 0,
+                         stream, a);
+    else
+      hipLaunchKernelGGL((k_sample<TI, true>), dim3((unsigned)a.N), dim3(kSmpThreads), 0,
+                         stream, a);
     return hipGetLastError();
   }
   if (op == CacheOp::Score) {

@@ -70,8 +70,6 @@ enum class Path { RowResidentSmall, RowResidentLarge, RowStream, Split };
 
 // Building the cache (opd_sample_actions, opd_topk_support, opd_score_actions).
 enum class CacheOp { Sample, Topk, Score };
-// Chunk sums of a row that the sampler keeps in LDS: 38 * 1024 floats (152 KiB).
-constexpr int kCdfChunks = 38 * kRowThreads;
 // Top-k candidates kept in LDS before the exact counting fallback.
 constexpr int kTopkCand = 4096;
 
@@ -87,8 +85,6 @@ struct CacheArgs {
   int32_t* ids_out;     // [N, K] draws or support (sampling, top-k)
   float* logp;          // [N, K] log-probs at the ids; nullable except for scoring
   float* lse_out;       // [N] nullable
-  int64_t G;            // sampler: vectors per CDF chunk
-  int64_t nchunk;       // sampler: chunks per row
   int redo;             // top-k: only the rows the streamed kernel marked
 };
 
