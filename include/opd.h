@@ -243,7 +243,7 @@ int opd_loss_fwd_bwd(const void* logits, int32_t dtype, int64_t N, int64_t V, in
  *     (opd_workspace_bytes(...) of the same arguments) returns
  *     OPD_ERR_SCRATCH when the split path is forced (OPD_FLAG_FORCE_SPLITV);
  *     unforced, such a call runs the row-per-workgroup path, which needs no
- *     scratch.  (Unforced calls below 128 rows need at most 272 KiB.)
+ *     scratch.  (Unforced split calls, below 64 rows, need at most 126 KiB.)
  *   - Every record the split path reads is written earlier in the same call,
  *     so nothing carries over from the previous call's contents.
  *   - All calls on one GPU share that GPU's array: calls that overlap in time

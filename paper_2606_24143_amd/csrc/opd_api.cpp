@@ -13,11 +13,14 @@ using opd::Args;
 using opd::Path;
 
 // Below this many rows the split-vocabulary path runs (when it has a
-// workspace): fewer rows than about half the 256 CUs leave the chip idle.
-// Measured on MI355X (16-sample MC, V = 151,936): split is faster at N = 16
-// and 64, the row-per-workgroup path from N = 128 up (N = 256: 54 us against
-// 64 us, since a row held in registers is read once).
-constexpr int64_t kSplitMaxRows = 128;
+// workspace): so few rows leave most of the 256 CUs idle, and splitting the
+// rows over more workgroups outweighs the split path's second read of each
+// row.  Measured on MI355X (16-sample MC, V = 151,936 bf16, inputs rotated
+// so no step finds the last one's rows in the Infinity Cache), mean time per
+// call, split against row path: N = 16: 24.8 against 30.5 us; 24: 23.5
+// against 29.7; 32: 24.6 against 31.0; 48: 28.3 against 29.6; 64: 32.5
+// against 31.0; 128: 54.8 against 37.2.
+constexpr int64_t kSplitMaxRows = 64;
 // Workgroups the split path aims for, and its largest chunk count.
 constexpr int64_t kSplitTargetGroups = 8192;
 constexpr int kSplitMaxChunks = 64;

@@ -127,14 +127,15 @@ def test_workspace_sizing():
     L = opd.lib()
     ws = L.opd_workspace_bytes
     # small N takes the split path: N * P * 8 floats
-    b = ws(64, 151936, 1, 3, 0, 16, 0)
-    assert b > 0 and b % (64 * 32) == 0
-    P = b // (64 * 32)
+    b = ws(48, 151936, 1, 3, 0, 16, 0)
+    assert b > 0 and b % (48 * 32) == 0
+    P = b // (48 * 32)
     assert 1 <= P <= 64
-    # larger N or forced row-wise: none
+    # from 64 rows, or forced row-wise: none
+    assert ws(64, 151936, 1, 3, 0, 16, 0) == 0
     assert ws(256, 151936, 1, 3, 0, 16, 0) == 0
     assert ws(32768, 151936, 1, 3, 0, 16, 0) == 0
-    assert ws(64, 151936, 1, 3, 0, 16, 2) == 0
+    assert ws(48, 151936, 1, 3, 0, 16, 2) == 0
     # forced split at large N
     assert ws(32768, 151936, 1, 3, 0, 16, 4) > 0
     # invalid arguments: 0

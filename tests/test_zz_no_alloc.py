@@ -78,7 +78,7 @@ def _call(d, est, mask, flags, no_alloc):
 
 # (rows of the first call, rows of the second, flags): the split path chosen
 # for small N, the split path forced at a larger N, and the row-wise path
-CASES = [(100, 24, 0), (700, 130, opd.FLAG_FORCE_SPLITV), (300, 200, 0)]
+CASES = [(48, 24, 0), (700, 130, opd.FLAG_FORCE_SPLITV), (300, 200, 0)]
 
 
 @pytest.mark.gpu
@@ -91,7 +91,7 @@ def test_noalloc_matches_the_allocating_entry_point(est, case):
     for step, N in enumerate((n1, n2)):
         w, d, mask = _inputs(N, V, seed=11 + step)
         want = opd.workspace_bytes(N, V, w.dtype, est, 16, 8, flags)
-        assert (want > 0) == (flags != 0 or N < 128)
+        assert (want > 0) == (flags != 0 or N < 64)
         assert want <= opd.lib().opd_noalloc_scratch_bytes()
         a = _call(d, est, mask, flags, no_alloc=False)
         b = _call(d, est, mask, flags, no_alloc=True)
