@@ -263,8 +263,9 @@ size_t opd_noalloc_scratch_bytes(void);
 
 /*
  * Bytes of workspace opd_loss_fwd_bwd uses for these arguments (0 when the
- * call takes the row-per-workgroup path).  Pure host function: the answer
- * depends only on its arguments.  Invalid arguments return 0.
+ * call takes the row-per-workgroup path): the split-vocabulary path's
+ * per-(row, chunk) statistics records, N * P * 32 bytes.  Pure host function:
+ * the answer depends only on its arguments.  Invalid arguments return 0.
  */
 size_t opd_workspace_bytes(int64_t N, int64_t V, int32_t dtype, int32_t estimator, int32_t k,
                            int32_t M, uint32_t flags);
@@ -272,10 +273,19 @@ size_t opd_workspace_bytes(int64_t N, int64_t V, int32_t dtype, int32_t estimato
 /*
  * Checks a cache against the preconditions of the estimator and ADDS the
  * number of violations to *violations (a device int32 the caller zeroes):
- * ids outside [0, V), repeated ids within a top-k row, and non-finite
- * teacher_logp (and behav_logp for MC).  Each bad entry counts once, each
- * repeated top-k pair once.  Stream-ordered; read the counter after
- * synchronising.  Dense estimators have no cache to check (returns OPD_OK).
+ *   - ids outside [0, V);
+ *   - repeated ids within a top-k row: a support S is a set of actions, and
+ *     the restricted normalisers and renormalised distributions on S
+ *     (App. A.1) count each action once.  Repeats within an MC row are legal,
+ *     since the m samples are drawn iid with replacement (Sec. 6.2; App. E),
+ *     and are not counted;
+ *   - non-finite teacher_logp (and behav_logp for the estimators with an
+ *     importance ratio or A_old): a log-probability the cache records for an
+ *     action it holds is finite.
+ * Each bad entry counts once, each repeated top-k pair once.  Stream-ordered;
+ * read the counter after synchronising.  Dense estimators have no cache to
+ * check (returns OPD_OK).  Errors: OPD_ERR_ESTIMATOR, OPD_ERR_SHAPE,
+ * OPD_ERR_SUPPORT, OPD_ERR_NULL, OPD_ERR_HIP.
  */
 int opd_validate_cache(const opd_cache* cache, int32_t estimator, int64_t N, int64_t V,
                        int32_t k, int32_t M, int32_t* violations, void* stream);
@@ -390,7 +400,8 @@ int opd_mc_diagnostics(const float* lse, const float* gathered, const float* tea
                        int32_t n_groups, int64_t seq_len, const opd_mc_diag* out, void* workspace,
                        size_t workspace_bytes, void* stream);
 
-/* Static description of a status code ("ok", "null pointer", ...). */
+/* Static description of a status code ("ok", "null pointer", ...); a code
+ * outside opd_status gives "unknown status".  Never NULL. */
 const char* opd_status_string(int status);
 
 /* OPD_VERSION of the built library. */
