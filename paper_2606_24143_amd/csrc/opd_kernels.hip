@@ -537,9 +537,13 @@ constexpr float kLazyRaise = 24.f;
 // so a lane's first value above that raises it (a row whose every logit is
 // below it reads as a row of -inf)
 constexpr float kOffsetFloor = 3e38f;
-// LDS that holds the first teacher slots between the sweeps: only the rest
-// of the teacher row is read a second time.
+// LDS that holds the first teacher slots between the sweeps, and the number
+// of teacher slots after those that stay in registers: only the rest of the
+// teacher row is read a second time.
 constexpr int kYLdsBytes = 144 * 1024;
+// Twelve registers per lane hold three bf16 slots (1.5 of fp32) with no
+// spill in any variant; sixteen spill in the fp32 build.
+constexpr int kYRegVgprs = 12;
 
 template <class TI, class TO, int EST, int NSLOT>
 __global__ void __launch_bounds__(kRowThreads) k_row_dense_resident(Args a) {
@@ -547,6 +551,10 @@ __global__ void __launch_bounds__(kRowThreads) k_row_dense_resident(Args a) {
   typedef typename TI::Vec Vec;
   constexpr int YL_CAP = kYLdsBytes / (NT * (int)sizeof(Vec));
   constexpr int YL = YL_CAP < NSLOT ? YL_CAP : NSLOT;  // teacher slots kept in LDS
+  // teacher slots kept in registers (after the LDS ones)
+  constexpr int YR_WANT = kYRegVgprs / (int)(sizeof(Vec) / 4);
+  constexpr int YR = YL + YR_WANT < NSLOT ? YR_WANT : NSLOT - YL;
+  constexpr int YK = YL + YR;  // slots not read a second time
   __shared__ Stats s_st[NW];
   __shared__ Vec s_y[YL][NT];
   const int tid = threadIdx.x;
@@ -588,6 +596,7 @@ __global__ void __launch_bounds__(kRowThreads) k_row_dense_resident(Args a) {
   // data has landed.  The scheduling barriers keep the loads in this order.
   Vec x[NSLOT];
   Vec yq[kYAhead];
+  Vec yr[YR > 0 ? YR : 1];
   Stats st;
   {
     const uint32_t nvec1 = fresh_s(nvec);
@@ -607,6 +616,7 @@ __global__ void __launch_bounds__(kRowThreads) k_row_dense_resident(Args a) {
       Vec yv = yq[s % kYAhead];
       if (s + kYAhead < NSLOT) yq[s % kYAhead] = buf_ld<TI, 0>(y_slot(s + kYAhead), vo1);
       if (s < YL) s_y[s][tid1] = yv;  // kept for sweep 2 (each lane reads back its own entry)
+      else if (s < YK) yr[s - YL] = yv;
       if (!in_row(s, tid1, nvec1)) {
         x[s] = neg_inf_vec<TI>();
         yv = neg_inf_vec<TI>();
@@ -691,17 +701,19 @@ __global__ void __launch_bounds__(kRowThreads) k_row_dense_resident(Args a) {
     const uint32_t vo2 = fresh_v((uint32_t)tid * (uint32_t)sizeof(Vec));
     const uint32_t vg2 = fresh_v((uint32_t)tid * (uint32_t)(EPV * TO::BYTES));
 #pragma unroll
-    for (int j = 0; j < kYAhead && YL + j < NSLOT; ++j)
-      yq[j] = buf_ld<TI, 0>(y_slot(YL + j), vo2);
+    for (int j = 0; j < kYAhead && YK + j < NSLOT; ++j)
+      yq[j] = buf_ld<TI, 0>(y_slot(YK + j), vo2);
 #pragma unroll
     for (int s = 0; s < NSLOT; ++s) {
       Vec yv;
       if (s < YL) {
         yv = s_y[s][tid2];
+      } else if (s < YK) {
+        yv = yr[s - YL];
       } else {
-        yv = yq[(s - YL) % kYAhead];
+        yv = yq[(s - YK) % kYAhead];
         if (s + kYAhead < NSLOT)
-          yq[(s - YL) % kYAhead] = buf_ld<TI, 0>(y_slot(s + kYAhead), vo2);
+          yq[(s - YK) % kYAhead] = buf_ld<TI, 0>(y_slot(s + kYAhead), vo2);
       }
       after(x[s], yv);
       float g[EPV];
