@@ -163,7 +163,7 @@ def dominant_kernels(op: str, est: str, w, split: bool):
         if est in ("fkl_dense", "rkl_dense"):
             return ["k_row_dense_resident"]
         return ["k_row_resident"]
-    return {"sample": ["k_sample_stream"], "topk": ["k_topk_stream", "k_topk"],
+    return {"sample": ["k_sample"], "topk": ["k_topk_stream", "k_topk"],
             "score": ["k_score"], "diag": ["k_diag_*"]}[op]
 
 

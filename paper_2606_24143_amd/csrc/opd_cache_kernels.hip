@@ -15,6 +15,8 @@
 // there; wider rows are streamed.
 #include <math.h>
 
+#include <type_traits>
+
 #include "opd_device.h"
 
 namespace opd {
@@ -26,6 +28,16 @@ constexpr int NW = NT / 64;
 constexpr int32_t kTopkRedo = -2;
 
 // ---------------------------------------------------------------- rows
+
+// max of three fp32 values by the hardware instruction, without the quieting
+// of signalling NaNs that fmaxf adds for inputs of unknown origin (where it
+// is used, a NaN input is caught another way)
+__device__ __forceinline__ float max3_raw(float a, float b, float c) {
+  float r;
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+
 
 // Elements [valid, 4) of a vector replaced by -inf, without branches (the
 // masks depend only on the wave-uniform count).
@@ -165,25 +177,24 @@ constexpr int kSmpLoads = 8;                   // loads per lane per step
 constexpr int kSmpStepVecs = 16 * kSmpLoads;   // vectors per DPP-row step (128)
 constexpr int kSmpMaxChunks = 2048;            // records per row
 
-// exp(z - m) in double for a logit z <= m (z = -inf gives 0; NaN and +inf
-// logits are caught by the rows' fp32 checks), table-driven (Tang, ACM TOMS
-// 15(2), 1989): z - m = (n / 32) ln 2 + r with |r| below about ln 2 / 64,
-// exp(z - m) = 2^(n >> 5) 2^((n & 31) / 32) exp(r), and exp(r) by its Taylor
-// polynomial to r^5 (truncation below 3e-15 relative).  Only the reduced
-// argument r needs double precision: n may be any integer near
-// (z - m) 32 / ln 2, so it comes from fp32 arithmetic, and it enters the
-// double arithmetic through its bits (2^52 + 2^31 + n has n in its low word)
-// rather than a conversion.  ln 2 / 32 is split in the Cody-Waite way (the
-// high part's 32 significant bits make n times it exact for |n| < 2^21).
-// 2^(n >> 5) goes into the exponent field by an integer add; below 2^-1000
-// the term is 0 (such terms are below 1e-300 of the largest).  The 32 table
-// entries fill one row of the LDS banks, so the lanes' lookups never
-// conflict.
+// exp(z - m) in double for a logit z <= m, table-driven (Tang, ACM TOMS
+// 15(2), 1989): d = z - m (exact in double) = (n / 32) ln 2 + r with |r| at
+// most about ln 2 / 64, exp(d) = 2^(n >> 5) 2^((n & 31) / 32) exp(r), and
+// exp(r) by its Taylor polynomial to r^5 (truncation below 3e-15 relative).
+// n = round(d 32 / ln 2) comes from one fused multiply-add onto 1.5 * 2^52,
+// whose low word is then n and whose value less 1.5 * 2^52 is n as a double;
+// ln 2 / 32 is split in the Cody-Waite way (the high part's 32 significant
+// bits make n times it exact for |n| < 2^21).  2^(n >> 5) goes into the
+// exponent field by an integer add.  Below d = -693 (a term below 1e-301 of
+// the largest; also z = -inf) the term is 0; a NaN d (a NaN logit, or z = m
+// = +inf) gives NaN, which leaves the record, and so the row, undefined.
+// The 32 table entries fill one row of the LDS banks, so the lanes' lookups
+// never conflict.
 constexpr int kExpTab = 32;
-constexpr float kInvStepF = 46.16624130844683f;              // 32 / ln 2
+constexpr double kInvStep = 46.166241308446828;            // 32 / ln 2
+constexpr double kShift52 = 6755399441055744.0;            // 1.5 * 2^52
 constexpr double kStepHi = 6.93147180369123816490e-01 / 32.0;
 constexpr double kStepLo = 1.90821492927058770002e-10 / 32.0;
-constexpr double kMagic = 4503601774854144.0;                // 2^52 + 2^31
 
 struct SmpLds {
   double s[kSmpMaxChunks];  // chunk sum at its max; then at the row max
@@ -194,49 +205,44 @@ struct SmpLds {
   float red[kSmpWaves];
 };
 
-// The term for one fp32 logit z against the chunk max m (md = m in double).
-// The single expression both the chunk records and the draws use, so the
-// draws recompute bit for bit the terms the records summed.
-__device__ __forceinline__ double term(float z, float m, double md, const double* tab) {
-  // n: an integer within about 0.5 of (z - m) 32 / ln 2 (z - m is rounded
-  // relative to itself, not to m).  Below -32000 (z - m < -693, a term below
-  // 1e-301 of the largest; also -inf) the term is 0, and n is clamped only so
-  // that the conversion stays defined.
-  const float x = (z - m) * kInvStepF;
-  const bool live = x > -32000.f;
-  const int n = (int)__builtin_rintf(fmaxf(x, -32000.f));
-  const double nd =
-      __builtin_bit_cast(double, (0x4330000000000000ull | (uint64_t)(uint32_t)(n + 0x80000000u))) -
-      kMagic;
-  const double d = (double)z - md;
+// (c24 is 1/24, passed in a vector register: one instruction cannot read two
+// scalar constants, and a register the caller holds is not re-materialised
+// per call)
+__device__ __forceinline__ double exp_reduced(double d, const double* tab, double c24) {
+  const double xs = fma(d, kInvStep, kShift52);
+  const double nd = xs - kShift52;
+  const int n = (int)(uint32_t)__builtin_bit_cast(uint64_t, xs);
   double r = fma(-nd, kStepHi, d);
   r = fma(-nd, kStepLo, r);
-  double p = fma(r, 1.0 / 120.0, 1.0 / 24.0);
+  double p = fma(r, 1.0 / 120.0, c24);
   p = fma(p, r, 1.0 / 6.0);
   p = fma(p, r, 0.5);
   p = fma(p, r, 1.0);
   p = fma(p, r, 1.0);
-  const double t = tab[n & (kExpTab - 1)] * p;  // in [0.98, 2.05]
-  const int k = n >> 5;                          // >= -1000 where live
-  const uint64_t bits = __builtin_bit_cast(uint64_t, t) + ((uint64_t)(int64_t)k << 52);
-  return live ? __builtin_bit_cast(double, bits) : 0.0;
+  u32x2 t = __builtin_bit_cast(u32x2, tab[n & (kExpTab - 1)] * p);  // in [0.98, 2.05]
+  uint32_t k = (uint32_t)(n >> 5);  // >= -1000 where the term is live
+  asm("" : "+v"(k));                 // (kept whole, so the add below is one shift-add)
+  t[1] += k << 20;
+  return !(d <= -693.0) ? __builtin_bit_cast(double, t) : 0.0;
 }
 
-// exp(x) for one double x <= 0 (the row-max scale of a chunk record),
-// through the same steps
+// 1/24 in a vector register (see exp_reduced)
+__device__ __forceinline__ double c24_reg() {
+  double c = 1.0 / 24.0;
+  asm volatile("" : "+v"(c));
+  return c;
+}
+
+// The term for one fp32 logit z against the chunk max (md, in double).  The
+// single expression both the chunk records and the draws use, so the draws
+// recompute bit for bit the terms the records summed.
+__device__ __forceinline__ double term(float z, double md, const double* tab, double c24) {
+  return exp_reduced((double)z - md, tab, c24);
+}
+
+// exp(x) for one double x <= 0 (the row-max scale of a chunk record)
 __device__ __forceinline__ double exp_neg(double x, const double* tab) {
-  const float xs = (float)x * kInvStepF;
-  const bool live = xs > -32000.f;
-  const int n = (int)__builtin_rintf(fmaxf(xs, -32000.f));
-  const double nd = (double)n;
-  double r = fma(-nd, kStepHi, x);
-  r = fma(-nd, kStepLo, r);
-  double p = fma(r, 1.0 / 120.0, 1.0 / 24.0);
-  p = fma(p, r, 1.0 / 6.0);
-  p = fma(p, r, 0.5);
-  p = fma(p, r, 1.0);
-  p = fma(p, r, 1.0);
-  return live ? __builtin_ldexp(tab[n & (kExpTab - 1)] * p, n >> 5) : 0.0;
+  return exp_reduced(x, tab, c24_reg());
 }
 
 // max over the 16 lanes of a DPP row, in every lane of the row
@@ -295,7 +301,7 @@ template <class TI>
 __device__ __forceinline__ void step_terms(const void* zrow, uint32_t v0, uint32_t c1,
                                            uint32_t nvec, int tail, float mq, const double* tab,
                                            double (&w)[8]) {
-  const double md = (double)mq;
+  const double md = (double)mq, c24 = c24_reg();
   const uint32_t v = v0 + 2u * (uint32_t)(threadIdx.x & 63);
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
@@ -303,7 +309,7 @@ __device__ __forceinline__ void step_terms(const void* zrow, uint32_t v0, uint32
     float f[4];
     unpack<TI>(in ? load_vec<TI>(zrow, v + h, nvec, tail) : neg_inf_vec<TI>(), f);
 #pragma unroll
-    for (int e = 0; e < 4; ++e) w[4 * h + e] = in ? term(f[e], mq, md, tab) : 0.0;
+    for (int e = 0; e < 4; ++e) w[4 * h + e] = in ? term(f[e], md, tab, c24) : 0.0;
   }
 }
 
@@ -430,40 +436,41 @@ __device__ __forceinline__ void chunk_record(const void* zrow, uint32_t q, uint3
       else
         x[b] = ld_nt<TI>(zrow, min(v, nvec - 1));
     }
+    // (a step wholly inside the chunk and clear of a ragged last vector
+    // needs no selects)
+    if (!(s0 + kSmpStepVecs <= c1 && !(ragged && s0 + kSmpStepVecs >= nvec))) {
 #pragma unroll
-    for (int b = 0; b < R; ++b) {
-      const uint32_t v = s0 + rl + 16u * b;
-      const Vec t = tail_masked<TI>(x[b], tail);
-      const Vec n = neg_inf_vec<TI>();
-      const bool out = v >= c1, last = ragged && v == nvec - 1;
+      for (int b = 0; b < R; ++b) {
+        const uint32_t v = s0 + rl + 16u * b;
+        const Vec t = tail_masked<TI>(x[b], tail);
+        const Vec n = neg_inf_vec<TI>();
+        const bool out = v >= c1, last = ragged && v == nvec - 1;
 #pragma unroll
-      for (int d = 0; d < (int)(sizeof(Vec) / 4); ++d)
-        x[b][d] = out ? n[d] : (last ? t[d] : x[b][d]);
+        for (int d = 0; d < (int)(sizeof(Vec) / 4); ++d)
+          x[b][d] = out ? n[d] : (last ? t[d] : x[b][d]);
+      }
     }
   };
-  // the plain sum of the elements turns NaN for a NaN in the chunk (and for
-  // +inf with -inf; +inf alone shows as an infinite maximum): either leaves
-  // the row without a distribution
-  float chk = 0.f;
+  // (a NaN element, or an infinite maximum, makes the chunk's sum NaN: the
+  // row then has no distribution)
   auto step_max = [&]() {
     float lm = kNegInf;
 #pragma unroll
     for (int b = 0; b < R; ++b) {
       float f[4];
       unpack<TI>(x[b], f);
-      lm = fmaxf(lm, fmaxf(fmaxf(f[0], f[1]), fmaxf(f[2], f[3])));
-      chk += (f[0] + f[1]) + (f[2] + f[3]);
+      lm = max3_raw(max3_raw(lm, f[0], f[1]), f[2], f[3]);
     }
     return lm;
   };
-  auto step_sum = [&](float m, double acc) {
-    const double md = (double)m;
+  const double c24 = c24_reg();
+  auto step_sum = [&](double md, double acc) {
 #pragma unroll
     for (int b = 0; b < R; ++b) {
       float f[4];
       unpack<TI>(x[b], f);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) acc += term(f[e], m, md, tab);
+      for (int e = 0; e < 4; ++e) acc += term(f[e], md, tab, c24);
     }
     return acc;
   };
@@ -479,19 +486,19 @@ __device__ __forceinline__ void chunk_record(const void* zrow, uint32_t q, uint3
   }
   const float mq = row16_max(lm);
   double ls = 0.0;
-  const bool undefined = __ballot(chk != chk || mq == __builtin_huge_valf()) != 0;
-  if (mq != kNegInf && !undefined) {  // an all -inf chunk has no mass
+  if (mq != kNegInf) {  // an all -inf chunk has no mass
+    const double md = (double)mq;
     if constexpr (!WIDE) {
-      ls = step_sum(mq, 0.0);
+      ls = step_sum(md, 0.0);
     } else {
       for (uint32_t s0 = c0; s0 < c1; s0 += kSmpStepVecs) {
         load_step(s0);
-        ls = step_sum(mq, ls);
+        ls = step_sum(md, ls);
       }
     }
   }
   mq_out = mq;
-  sq_out = undefined ? __builtin_nan("") : row16_sum(ls);
+  sq_out = row16_sum(ls);
 }
 
 template <class TI, bool WIDE>
@@ -881,28 +888,30 @@ __global__ void __launch_bounds__(NT) k_topk(CacheArgs a) {
 // each row once: 256-lane workgroups with about 38 KiB of LDS, four per CU.
 // Each lane keeps the running maximum of the values it has seen.  After each
 // tile of 8 coalesced loads per lane, and before any of the tile's elements
-// is kept, the wave raises its bound to the k-th largest of its 64 running
-// maxima (k lanes have each seen an element at least that large, so it is a
-// lower bound on the row's k-th largest; found by a radix select over order
-// keys with ballots, 16 key bits for bf16 rows), and to the largest bound
-// any wave of the workgroup has published in LDS (each is such a lower
-// bound).  The bound only rises.  A lane then keeps, in its own LDS slots,
-// the elements of the tile not below the bound (and NaNs): no cross-lane
-// compaction in the stream.  At the end the largest wave bound is still a
-// lower bound, every element at or above it is in some lane's slots, and a
-// block sort of those (at most 256) gives the support.  A row whose lane
-// slots overflow (many equal large values) or that leaves more than 256
-// candidates is marked, and a second launch runs the resident kernel on the
-// marked rows only.
+// is kept, the wave recomputes the ceil(k / 4)-th largest of its 64 running
+// maxima (a radix select over order keys with ballots, 16 key bits for bf16
+// rows) and publishes it in LDS; the bound in use is the smallest of the
+// four waves' published values (on a wave's first tile, the k-th largest of
+// its own maxima), a lower bound on the row's k-th largest, and it only
+// rises.  Only lanes whose tile maximum reaches the bound look at the tile
+// again, vector by vector, and keep the elements at or above it in their
+// own LDS slots: no cross-lane compaction in the stream.  The next tile's
+// loads are issued before the current tile is processed.  Since no bound
+// exceeded the row's k-th largest key, the slots hold every element at or
+// above it; at the end the largest known bound filters them, and a block
+// sort of those (at most 256) gives the support.  A row
+// whose lane slots overflow (many equal large values), that leaves more
+// than 256 candidates, or that holds a NaN is marked, and a second launch
+// runs the resident kernel on the marked rows only.
 constexpr int kTkThreads = 256;
 constexpr int kTkWaves = kTkThreads / 64;
 constexpr int kTkLoads = 8;    // vector loads per lane per tile
-constexpr int kTkSlots = 16;   // candidate slots per lane
+constexpr int kTkSlots = 16;   // candidate slots per lane (a power of two)
 constexpr int kTkMaxK = 64;    // one running maximum per lane bounds k
 constexpr int64_t kTkMinVec = 4096;
 
 struct TkLds {
-  uint64_t buf[kTkSlots][kTkThreads];  // lane-private candidate slots
+  uint64_t buf[kTkSlots][kTkThreads];  // lane-private candidates: (value bits, ~index)
   uint64_t sbuf[2][kTkThreads];
   uint64_t sel[kTkThreads];
   uint32_t theta[kTkWaves];            // published wave bounds (order keys)
@@ -953,20 +962,37 @@ __global__ void __launch_bounds__(kTkThreads) k_topk_stream(CacheArgs a) {
   const void* zrow = (const char*)a.logits + row * a.ld * TI::BYTES;
   const uint32_t nvec = (uint32_t)a.nvec;  // >= kTkMinVec: every wave's first tile is full
   const uint32_t V32 = (uint32_t)a.V;
+  constexpr uint32_t TILE = 64u * B, STRIDE = W * TILE;
+  // tiles wholly inside the row (and clear of a ragged last vector) take
+  // the path without per-element checks
+  const uint32_t nclean = a.tail == TI::EPV ? nvec : nvec - 1;
+  const uint32_t nfull = nclean / TILE * TILE;
   float run = kNegInf;  // this lane's running maximum (NaN ignored)
-  uint32_t theta = 0;   // the wave's bound as an order key (wave-uniform)
-  float thf = kNegInf;  // the same bound as a value
+  // The bound.  Each wave publishes the ceil(k / 4)-th largest of its 64
+  // running maxima (as an order key): that many of its lanes have each seen
+  // an element at least that large, so the smallest of the four published
+  // values has k distinct elements at or above it and is a lower bound on
+  // the row's k-th largest.  Published values only rise, so a stale read
+  // is still a lower bound.
+  const int kq = (k + W - 1) / W;
+  uint32_t qown = 0;    // this wave's published value (wave-uniform)
+  uint32_t theta = 0;   // the bound in use (wave-uniform)
+  bool first = true;    // this wave's first tile
   uint32_t cnt = 0;     // this lane's candidates so far
-  float m = kNegInf, sum = 0.f;
-  for (uint32_t t0 = (uint32_t)w * 64 * B; t0 < nvec; t0 += W * 64 * B) {  // wave-uniform
-    Vec xb[B];
-#pragma unroll
-    for (int b = 0; b < B; ++b) xb[b] = ld_nt<TI>(zrow, min(t0 + 64u * b + lane, nvec - 1));
-    // a whole tile inside the row needs no per-element checks (wave-uniform)
-    const bool full = t0 + 64u * B <= nvec && a.tail == TI::EPV;
+  float m = kNegInf, sum = 0.f, chk = 0.f;
+
+  // One tile of B vectors per lane at vector t0 (lane l holds t0 + 64 b + l).
+  // Pass A, for every lane: the tile's maximum (and its share of the
+  // log-partition); then the bound; then pass B, in the lanes whose tile
+  // maximum reaches the bound only, the elements kept.  A NaN anywhere in
+  // the row (and, when the log-partition is wanted, a lane that sees no
+  // finite value) sends the row to the exact fallback, so the bound and the
+  // comparisons here need only order the numbers.
+  auto process = [&](const Vec (&x)[B], uint32_t t0, auto full_tag) {
+    constexpr bool FULL = decltype(full_tag)::value;
     auto vals = [&](int b, float (&f)[4]) {
-      unpack<TI>(xb[b], f);
-      if (!full) {
+      unpack<TI>(x[b], f);
+      if constexpr (!FULL) {
         const uint32_t v = t0 + 64u * b + lane;
 #pragma unroll
         for (int e = 0; e < 4; ++e)
@@ -978,55 +1004,130 @@ __global__ void __launch_bounds__(kTkThreads) k_topk_stream(CacheArgs a) {
     for (int b = 0; b < B; ++b) {
       float f[4];
       vals(b, f);
-      tmx = fmaxf(tmx, fmaxf(fmaxf(f[0], f[1]), fmaxf(f[2], f[3])));
+      tmx = max3_raw(max3_raw(tmx, f[0], f[1]), f[2], f[3]);
+      if constexpr (!LSE) chk += (f[0] + f[1]) + (f[2] + f[3]);
     }
     if constexpr (LSE) {
       const float mn = fmaxf(m, tmx);
-      if (mn != kNegInf) {
-        float acc = 0.f;
+      if (mn != kNegInf) {  // (a lane that never sees a finite value sends its row to the fallback)
         const float nm = -mn * kLog2e;
+        float ex[B * 4];
 #pragma unroll
         for (int b = 0; b < B; ++b) {
           float f[4];
           vals(b, f);
 #pragma unroll
-          for (int e = 0; e < 4; ++e) acc += fast_exp2(fmaf(f[e], kLog2e, nm));
+          for (int e = 0; e < 4; ++e) ex[4 * b + e] = fast_exp2(fmaf(f[e], kLog2e, nm));
         }
-        sum = fmaf(sum, rescale(m, mn), acc);
+#pragma unroll
+        for (int h = B * 2; h >= 1; h >>= 1)
+#pragma unroll
+          for (int i = 0; i < h; ++i) ex[i] += ex[i + h];
+        sum = fmaf(sum, rescale(m, mn), ex[0]);  // NaN from a NaN element
         m = mn;
       }
     }
     run = fmaxf(run, tmx);
     // raise the bound before keeping any of the tile's elements
     const uint32_t rk = order_key(__float_as_uint(run));
-    if ((uint32_t)__popcll(__ballot(rk > theta)) >= (uint32_t)k) {  // wave-uniform
-      theta = wave_kth_key<LOWBITS>(rk, k);
-      if (lane == 0) sh.theta[w] = theta;
+    if ((uint32_t)__popcll(__ballot(rk > qown)) >= (uint32_t)kq) {  // wave-uniform
+      qown = wave_kth_key<LOWBITS>(rk, kq);
+      if (lane == 0) sh.theta[w] = qown;
     }
-    uint32_t pub = theta;
+    if (first) {  // until the other waves have published: the k-th of this wave's maxima
+      theta = wave_kth_key<LOWBITS>(rk, k);
+      first = false;
+    }
+    uint32_t pub = sh.theta[0];
 #pragma unroll
-    for (int q = 0; q < W; ++q) pub = max(pub, sh.theta[q]);
-    theta = __builtin_amdgcn_readfirstlane(pub);
-    thf = key_value(theta);
-    // keep every element not below the bound, and every NaN (!(x < bound)
-    // holds for both), in this lane's slots
+    for (int q = 1; q < W; ++q) pub = min(pub, sh.theta[q]);
+    theta = max(theta, (uint32_t)__builtin_amdgcn_readfirstlane(pub));
+    const float thf = key_value(theta);
+    // for numbers, f >= thf exactly when order_key(f) >= theta (a bf16
+    // bound's zero low key bits sit below every widened value's)
+    if (__ballot(tmx >= thf) != 0) {  // wave-uniform
+      if (tmx >= thf) {
 #pragma unroll
-    for (int b = 0; b < B; ++b) {
-      float f[4];
-      vals(b, f);
-      const uint32_t v = t0 + 64u * b + lane;
+        for (int b = 0; b < B; ++b) {
+          Vec xv = x[b];
+          keep_packed(xv);  // unpacked again here rather than held since pass A
+          float f[4];
+          unpack<TI>(xv, f);
+          if constexpr (!FULL) {
+            const uint32_t v = t0 + 64u * b + lane;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        if (!(f[e] < thf) && (full || (v < nvec && v * 4u + e < V32))) {
-          if (cnt < (uint32_t)kTkSlots)
-            sh.buf[cnt][tid] = ((uint64_t)order_key(__float_as_uint(f[e])) << 32) |
-                               (0xFFFFFFFFu - (v * 4u + e));
-          ++cnt;
+            for (int e = 0; e < 4; ++e)
+              if (!(v < nvec && v * 4u + e < V32)) f[e] = kNegInf;
+          }
+          if (max3_raw(max3_raw(f[0], f[1], f[2]), f[3], f[3]) >= thf) {
+            const uint32_t v = t0 + 64u * b + lane;
+            // each element is written to the lane's next free slot, which
+            // only a kept element then claims (a lane that reaches the last
+            // slot overflows, and its row goes to the fallback)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const bool keep = f[e] >= thf && (FULL || (v < nvec && v * 4u + e < V32));
+              sh.buf[cnt & (kTkSlots - 1)][tid] =
+                  ((uint64_t)__float_as_uint(f[e]) << 32) | (0xFFFFFFFFu - (v * 4u + e));
+              cnt += keep ? 1u : 0u;
+            }
+          }
         }
       }
     }
+  };
+  // full tiles through a buffer resource that starts at the tile (scalar
+  // arithmetic): the lane offset is fixed and each load's step an immediate
+  const uint32_t loff = (uint32_t)lane * (uint32_t)sizeof(Vec);
+  auto load = [&](Vec (&x)[B], uint32_t t0) {
+    const uint64_t off = (uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)t0) * sizeof(Vec);
+    const Rsrc r = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>((const char*)zrow + off), 0,
+                                                     (int)(TILE * sizeof(Vec)), kRsrcWord3);
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+      if constexpr (TI::BYTES == 2)
+        x[b] = __builtin_amdgcn_raw_buffer_load_b64(r, (int)(loff + 64u * sizeof(Vec) * b), 0,
+                                                    kAuxNt);
+      else
+        x[b] = __builtin_amdgcn_raw_buffer_load_b128(r, (int)(loff + 64u * sizeof(Vec) * b), 0,
+                                                     kAuxNt);
+    }
+  };
+  typedef std::integral_constant<bool, true> Full;
+  typedef std::integral_constant<bool, false> Partial;
+  // the wave's full tiles, two buffers: the next tile's loads are in flight
+  // while the current one is processed
+  Vec xa[B], xb[B];
+  uint32_t t0 = (uint32_t)w * TILE;
+  if (t0 < nfull) {  // wave-uniform
+    load(xa, t0);
+    while (t0 + 2 * STRIDE < nfull) {
+      load(xb, t0 + STRIDE);
+      process(xa, t0, Full());
+      load(xa, t0 + 2 * STRIDE);
+      process(xb, t0 + STRIDE, Full());
+      t0 += 2 * STRIDE;
+    }
+    if (t0 + STRIDE < nfull) {
+      load(xb, t0 + STRIDE);
+      process(xa, t0, Full());
+      process(xb, t0 + STRIDE, Full());
+      t0 += 2 * STRIDE;
+    } else {
+      process(xa, t0, Full());
+      t0 += STRIDE;
+    }
   }
-  if (cnt > (uint32_t)kTkSlots) sh.over = 1u;
+  // the one tile that reaches past the clean vectors (the wave whose turn it is)
+  if (t0 < nvec) {
+#pragma unroll
+    for (int b = 0; b < B; ++b) xa[b] = ld_nt<TI>(zrow, min(t0 + 64u * b + lane, nvec - 1));
+    process(xa, t0, Partial());
+  }
+  bool nan_seen;
+  if constexpr (LSE) nan_seen = sum != sum || m == kNegInf;
+  else nan_seen = chk != chk;
+  if (cnt >= (uint32_t)kTkSlots || nan_seen) sh.over = 1u;
   float L = 0.f;
   if constexpr (LSE) {
     Stats st = stats_empty();
@@ -1037,18 +1138,20 @@ __global__ void __launch_bounds__(kTkThreads) k_topk_stream(CacheArgs a) {
   } else {
     __syncthreads();
   }
-  uint32_t tstar = 0;
+  // every bound in use was at most the row's k-th largest key, so the slots
+  // hold every element at or above it; the largest bound known filters them
+  uint32_t tstar = sh.theta[0];
 #pragma unroll
-  for (int q = 0; q < W; ++q) tstar = max(tstar, sh.theta[q]);
+  for (int q = 1; q < W; ++q) tstar = min(tstar, sh.theta[q]);
+  tstar = max(tstar, theta);
   const bool overflow = sh.over != 0u;
   if (!overflow) {
-    // every element with key >= tstar is in some lane's slots: no wave's
-    // bound exceeded tstar while it kept elements
     for (uint32_t i = 0; i < cnt; ++i) {
-      const uint64_t e = sh.buf[i][tid];
-      if ((uint32_t)(e >> 32) >= tstar) {
+      const uint64_t e = sh.buf[i][tid];  // (value bits, ~index)
+      const uint32_t key = order_key((uint32_t)(e >> 32));
+      if (key >= tstar) {
         const uint32_t pos = atomicAdd(&sh.nsel, 1u);
-        if (pos < (uint32_t)T) sh.sel[pos] = e;
+        if (pos < (uint32_t)T) sh.sel[pos] = ((uint64_t)key << 32) | (uint32_t)e;
       }
     }
   }
