@@ -5,8 +5,8 @@ Small shapes cover every estimator, both input dtypes, both gradient dtypes,
 every kernel path (register-resident rows, streaming rows, split
 vocabulary), ragged tails (V not a multiple of the vector width), padded row
 strides, masks, and the degenerate cases.  Full-size workloads run in the
-configuration the benchmark times and compare every row's loss and
-log-partition plus a sample of gradient rows."""
+configuration the benchmark times and compare every row's loss,
+log-partition, gathered logits and coverage, and every gradient element."""
 import functools
 
 import numpy as np
