@@ -106,8 +106,7 @@ def test_sample_parity(shape, M):
 
 
 def test_sample_wide_rows():
-    # wider than the streamed sampler's chunk records (V > 1,048,576): the
-    # chunked kernel
+    # rows above 1,048,576 entries: more than one 128-vector step per chunk
     V, N, M = 1_200_000, 3, 64
     say("sample wide V=%d" % V)
     stored = make_logits(V, V, synth.BF16, N, seed=4)
@@ -115,9 +114,33 @@ def test_sample_wide_rows():
     out = opd.sample_actions(as_device(stored, V), to_dev(u), want_lse=True)
     torch.cuda.synchronize()
     ref = oracle.cache_rows("sample", synth.BF16, stored, V, M, uniforms=u)
-    # more than one 128-vector step per CDF chunk (rows above 1,048,576)
     check_draws("wide", out["ids"].cpu().numpy(), out["logp"].cpu().numpy(), stored, V,
                 synth.BF16, u, ref)
+
+
+@pytest.mark.parametrize("dtype", [synth.F32, synth.BF16])
+def test_sample_extreme_logit_ranges(dtype):
+    """The double-precision terms across logit ranges: a large positive and a
+    large negative row maximum, a row whose terms fall below the 1e-301 cut
+    (z - m down to -800), logits near zero, and a wide spread."""
+    rng = np.random.default_rng(31)
+    V, N, M = 20000, 5, 64
+    x = rng.normal(0.0, 3.0, (N, V))
+    x[0] += 5000.0
+    x[1] -= 5000.0
+    x[2] = -np.linspace(0.0, 800.0, V) + rng.normal(0.0, 0.5, V)
+    x[3] *= 1e-7
+    x[4] = rng.normal(0.0, 30.0, V)
+    stored = to_stored(x.astype(np.float32), dtype)
+    say("sample extreme ranges dtype=%d" % dtype)
+    u = f32_uniforms(41, N, M)
+    out = opd.sample_actions(as_device(stored, V), to_dev(u), want_lse=True)
+    torch.cuda.synchronize()
+    ref = oracle.cache_rows("sample", dtype, stored, V, M, uniforms=u)
+    check_draws("extreme", out["ids"].cpu().numpy(), out["logp"].cpu().numpy(), stored, V, dtype,
+                u, ref)
+    lse = out["lse"].cpu().numpy().astype(np.float64)
+    assert np.all(np.abs(lse - ref["lse"]) <= LP_TOL * (1 + np.abs(ref["lse"])))
 
 
 def test_sample_masked_rows_and_determinism():
@@ -316,6 +339,46 @@ def test_topk_streamed_ties_and_special_values(dtype, k, case):
     torch.cuda.synchronize()
     ref = oracle.cache_rows("topk", dtype, stored, V, k)
     check_topk(case, out, stored, V, k, dtype, ref)
+
+
+@pytest.mark.parametrize("k", [16, 64])
+@pytest.mark.parametrize("where", ["one_wave", "one_lane", "few_finite"])
+def test_topk_streamed_concentrated_maxima(k, where):
+    """The streamed kernel's bound is the smallest of the four waves'
+    published values.  Rows whose largest values all lie in one wave's tiles
+    (wave w reads tiles of 512 vectors numbered w mod 4; the other waves'
+    bounds stay low), in one lane's elements (its slots overflow and the
+    resident kernel redoes the row), or that hold only a few finite values
+    among -inf (a lane that sees no finite value sends the row to the
+    resident kernel when the log-partition is wanted)."""
+    rng = np.random.default_rng(37)
+    V, N = 65536, 3  # 16,384 vectors: 32 tiles, 8 per wave
+    x = rng.normal(0.0, 1.0, (N, V)).astype(np.float32)
+    vec = np.arange(V // 4)
+    tile, lane = vec // 512, vec % 64
+    if where == "one_wave":
+        pos = np.flatnonzero(np.repeat(tile % 4 == 1, 4))
+        for r in range(N):
+            x[r, rng.choice(pos, 3 * k, replace=False)] = 6.0 + rng.random(3 * k)
+    elif where == "one_lane":
+        pos = np.flatnonzero(np.repeat((tile % 4 == 2) & (lane == 5), 4))
+        for r in range(N):
+            x[r, pos] = 6.0 + rng.random(pos.size)
+    else:
+        x[:] = -np.inf
+        for r in range(N):
+            x[r, rng.choice(V, k + 5, replace=False)] = rng.normal(0.0, 1.0, k + 5)
+    stored = to_stored(x, synth.BF16)
+    say("topk streamed concentrated %s k=%d" % (where, k))
+    ref = oracle.cache_rows("topk", synth.BF16, stored, V, k)
+    out = opd.topk_support(as_device(stored, V), k, want_lse=True)
+    torch.cuda.synchronize()
+    check_topk(where, out, stored, V, k, synth.BF16, ref)
+    # without log-probs or the log-partition (the kernel variant without
+    # the exponentials)
+    out = opd.topk_support(as_device(stored, V), k, want_logp=False)
+    torch.cuda.synchronize()
+    check_topk(where + " ids only", out, stored, V, k, synth.BF16, ref)
 
 
 def test_topk_streamed_masked_rows_and_no_logp():
