@@ -178,57 +178,60 @@ constexpr int kSmpStepVecs = 16 * kSmpLoads;   // vectors per DPP-row step (128)
 constexpr int kSmpMaxChunks = 2048;            // records per row
 
 // exp(z - m) in double for a logit z <= m, table-driven (Tang, ACM TOMS
-// 15(2), 1989): d = z - m (exact in double) = (n / 32) ln 2 + r with |r| at
-// most about ln 2 / 64, exp(d) = 2^(n >> 5) 2^((n & 31) / 32) exp(r), and
-// exp(r) by its Taylor polynomial to r^5 (truncation below 3e-15 relative).
-// n = round(d 32 / ln 2) comes from one fused multiply-add onto 1.5 * 2^52,
-// whose low word is then n and whose value less 1.5 * 2^52 is n as a double;
-// ln 2 / 32 is split in the Cody-Waite way (the high part's 32 significant
-// bits make n times it exact for |n| < 2^21).  2^(n >> 5) goes into the
-// exponent field by an integer add.  Below d = -693 (a term below 1e-301 of
-// the largest; also z = -inf) the term is 0; a NaN d (a NaN logit, or z = m
-// = +inf) gives NaN, which leaves the record, and so the row, undefined.
-// The 32 table entries fill one row of the LDS banks, so the lanes' lookups
-// never conflict.
-constexpr int kExpTab = 32;
-constexpr double kInvStep = 46.166241308446828;            // 32 / ln 2
+// 15(2), 1989): d = z - m (exact in double) = (n / 64) ln 2 + r with |r| at
+// most about ln 2 / 128, exp(d) = 2^(n >> 6) 2^((n & 63) / 64) exp(r), and
+// exp(r) by a degree-4 polynomial: the interpolant of exp at the five
+// Chebyshev nodes of [-1.002 ln 2 / 128, 1.002 ln 2 / 128], computed in
+// extended precision and rounded to double (within 2.5e-15 relative of exp
+// there, against 3e-15 for the degree-5 Taylor polynomial on twice the
+// range).  n = round(d 64 / ln 2) comes from one fused multiply-add onto
+// 1.5 * 2^52, whose low word is then n and whose value less 1.5 * 2^52 is n
+// as a double; ln 2 / 64 is split in the Cody-Waite way (the high part's 32
+// significant bits make n times it exact for |n| < 2^21).  2^(n >> 6) goes
+// into the exponent field by an integer add.  Below d = -693 (a term below
+// 1e-301 of the largest; also z = -inf) the term is 0; a NaN d (a NaN logit,
+// or z = m = +inf) gives NaN, which leaves the record, and so the row,
+// undefined.
+constexpr int kExpTab = 64;
+constexpr double kInvStep = 92.332482616893656;            // 64 / ln 2
 constexpr double kShift52 = 6755399441055744.0;            // 1.5 * 2^52
-constexpr double kStepHi = 6.93147180369123816490e-01 / 32.0;
-constexpr double kStepLo = 1.90821492927058770002e-10 / 32.0;
+constexpr double kStepHi = 6.93147180369123816490e-01 / 64.0;
+constexpr double kStepLo = 1.90821492927058770002e-10 / 64.0;
+constexpr double kP4 = 0.041666717487447574, kP3 = 0.16666697335347525,
+                 kP2 = 0.4999999999996304, kP1 = 0.9999999999977427;
 
 struct SmpLds {
   double s[kSmpMaxChunks];  // chunk sum at its max; then at the row max
   float m[kSmpMaxChunks];   // chunk max
   double p[kSmpThreads];    // inclusive prefix of the runs
-  double tab[kExpTab];      // 2^(j / 32)
+  double tab[kExpTab];      // 2^(j / 64)
   double wt[kSmpWaves];
   float red[kSmpWaves];
 };
 
-// (c24 is 1/24, passed in a vector register: one instruction cannot read two
+// (c3 is kP3, passed in a vector register: one instruction cannot read two
 // scalar constants, and a register the caller holds is not re-materialised
 // per call)
-__device__ __forceinline__ double exp_reduced(double d, const double* tab, double c24) {
+__device__ __forceinline__ double exp_reduced(double d, const double* tab, double c3) {
   const double xs = fma(d, kInvStep, kShift52);
   const double nd = xs - kShift52;
   const int n = (int)(uint32_t)__builtin_bit_cast(uint64_t, xs);
   double r = fma(-nd, kStepHi, d);
   r = fma(-nd, kStepLo, r);
-  double p = fma(r, 1.0 / 120.0, c24);
-  p = fma(p, r, 1.0 / 6.0);
-  p = fma(p, r, 0.5);
+  double p = fma(r, kP4, c3);
+  p = fma(p, r, kP2);
+  p = fma(p, r, kP1);
   p = fma(p, r, 1.0);
-  p = fma(p, r, 1.0);
-  u32x2 t = __builtin_bit_cast(u32x2, tab[n & (kExpTab - 1)] * p);  // in [0.98, 2.05]
-  uint32_t k = (uint32_t)(n >> 5);  // >= -1000 where the term is live
+  u32x2 t = __builtin_bit_cast(u32x2, tab[n & (kExpTab - 1)] * p);  // in [0.99, 2.02]
+  uint32_t k = (uint32_t)(n >> 6);  // >= -1000 where the term is live
   asm("" : "+v"(k));                 // (kept whole, so the add below is one shift-add)
   t[1] += k << 20;
   return !(d <= -693.0) ? __builtin_bit_cast(double, t) : 0.0;
 }
 
-// 1/24 in a vector register (see exp_reduced)
-__device__ __forceinline__ double c24_reg() {
-  double c = 1.0 / 24.0;
+// kP3 in a vector register (see exp_reduced)
+__device__ __forceinline__ double c3_reg() {
+  double c = kP3;
   asm volatile("" : "+v"(c));
   return c;
 }
@@ -236,13 +239,13 @@ __device__ __forceinline__ double c24_reg() {
 // The term for one fp32 logit z against the chunk max (md, in double).  The
 // single expression both the chunk records and the draws use, so the draws
 // recompute bit for bit the terms the records summed.
-__device__ __forceinline__ double term(float z, double md, const double* tab, double c24) {
-  return exp_reduced((double)z - md, tab, c24);
+__device__ __forceinline__ double term(float z, double md, const double* tab, double c3) {
+  return exp_reduced((double)z - md, tab, c3);
 }
 
 // exp(x) for one double x <= 0 (the row-max scale of a chunk record)
 __device__ __forceinline__ double exp_neg(double x, const double* tab) {
-  return exp_reduced(x, tab, c24_reg());
+  return exp_reduced(x, tab, c3_reg());
 }
 
 // max over the 16 lanes of a DPP row, in every lane of the row
@@ -301,7 +304,7 @@ template <class TI>
 __device__ __forceinline__ void step_terms(const void* zrow, uint32_t v0, uint32_t c1,
                                            uint32_t nvec, int tail, float mq, const double* tab,
                                            double (&w)[8]) {
-  const double md = (double)mq, c24 = c24_reg();
+  const double md = (double)mq, c3 = c3_reg();
   const uint32_t v = v0 + 2u * (uint32_t)(threadIdx.x & 63);
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
@@ -309,7 +312,7 @@ __device__ __forceinline__ void step_terms(const void* zrow, uint32_t v0, uint32
     float f[4];
     unpack<TI>(in ? load_vec<TI>(zrow, v + h, nvec, tail) : neg_inf_vec<TI>(), f);
 #pragma unroll
-    for (int e = 0; e < 4; ++e) w[4 * h + e] = in ? term(f[e], md, tab, c24) : 0.0;
+    for (int e = 0; e < 4; ++e) w[4 * h + e] = in ? term(f[e], md, tab, c3) : 0.0;
   }
 }
 
@@ -463,14 +466,14 @@ __device__ __forceinline__ void chunk_record(const void* zrow, uint32_t q, uint3
     }
     return lm;
   };
-  const double c24 = c24_reg();
+  const double c3 = c3_reg();
   auto step_sum = [&](double md, double acc) {
 #pragma unroll
     for (int b = 0; b < R; ++b) {
       float f[4];
       unpack<TI>(x[b], f);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) acc += term(f[e], md, tab, c24);
+      for (int e = 0; e < 4; ++e) acc += term(f[e], md, tab, c3);
     }
     return acc;
   };
