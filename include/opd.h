@@ -305,7 +305,7 @@ int opd_validate_cache(const opd_cache* cache, int32_t estimator, int64_t N, int
  *   order) exceeds uniforms[t, i].  The uniforms are supplied by the caller
  *   ([N, M] fp32 in [0, 1)), so the draws are a deterministic function of
  *   them.  The CDF is evaluated in double precision (terms exp(z_j - max) to
- *   a few ulp, double sums), so a draw is the one exact arithmetic gives
+ *   about 3e-15 relative, double sums), so a draw is the one exact arithmetic gives
  *   unless uniforms[t, i] lies within about 1e-14 of a cumulative value;
  *   terms below 1e-301 of the largest count as 0, and a drawn id always has
  *   nonzero probability.
