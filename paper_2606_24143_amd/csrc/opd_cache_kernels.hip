@@ -723,14 +723,11 @@ __device__ __forceinline__ void each_key(typename TI::Vec (&x)[NSLOT > 0 ? NSLOT
   }
 }
 
+// One row (every return below is workgroup-uniform).
 template <class TI, int NSLOT, bool LSE>
-__global__ void __launch_bounds__(NT) k_topk(CacheArgs a) {
-  __shared__ TopkLds sh;
+__device__ __forceinline__ void topk_row(const CacheArgs& a, int64_t row, TopkLds& sh) {
   const int tid = threadIdx.x;
-  const int64_t row = xcd_remap(blockIdx.x, gridDim.x);
   const int k = a.K;
-  // after the streamed kernel: only the rows it left to this one
-  if (a.redo && a.ids_out[row * k] != kTopkRedo) return;
   if (a.mask && a.mask[row] == 0) {
     for (int i = tid; i < k; i += NT) {
       a.ids_out[row * k + i] = 0;
@@ -883,6 +880,27 @@ __global__ void __launch_bounds__(NT) k_topk(CacheArgs a) {
     if (a.logp) a.logp[row * k + tid] = key_value((uint32_t)(mine >> 32)) - L;
   }
   if (tid == 0 && a.lse_out) a.lse_out[row] = L;
+}
+
+// The top-k of a row per workgroup (register-resident for NSLOT > 0); and,
+// after the streamed kernel, a short grid whose workgroups walk the rows and
+// redo only those the streamed kernel marked (reading them from memory), so
+// that the usual case, no marked row, costs a few hundred workgroups rather
+// than one per row.
+constexpr int kTopkRedoGroups = 512;
+template <class TI, int NSLOT, bool LSE>
+__global__ void __launch_bounds__(NT) k_topk(CacheArgs a) {
+  __shared__ TopkLds sh;
+  topk_row<TI, NSLOT, LSE>(a, xcd_remap(blockIdx.x, gridDim.x), sh);
+}
+template <class TI, int NSLOT, bool LSE>
+__global__ void __launch_bounds__(NT) k_topk_redo(CacheArgs a) {
+  __shared__ TopkLds sh;
+  for (int64_t row = blockIdx.x; row < a.N; row += gridDim.x) {  // workgroup-uniform
+    if (a.ids_out[row * a.K] != kTopkRedo) continue;
+    topk_row<TI, NSLOT, LSE>(a, row, sh);
+    __syncthreads();  // the next row's writes to LDS wait for this row's reads
+  }
 }
 
 // ---------------------------------------------------------------- top-k, streamed
@@ -1253,14 +1271,25 @@ __global__ void __launch_bounds__(kScoreThreads) k_score(CacheArgs a) {
 template <class TI, int NSLOT>
 hipError_t launch_op(const CacheArgs& a, CacheOp op, hipStream_t stream) {
   const dim3 grid((unsigned)a.N), block(NT);
+  const dim3 rgrid((unsigned)min(a.N, (int64_t)kTopkRedoGroups));
   switch (op) {
     case CacheOp::Sample:
       break;
     case CacheOp::Topk:
-      if (a.logp || a.lse_out)
+      if constexpr (NSLOT == 0) {
+        if (a.redo) {
+          if (a.logp || a.lse_out)
+            hipLaunchKernelGGL((k_topk_redo<TI, 0, true>), rgrid, block, 0, stream, a);
+          else
+            hipLaunchKernelGGL((k_topk_redo<TI, 0, false>), rgrid, block, 0, stream, a);
+          break;
+        }
+      }
+      if (a.logp || a.lse_out) {
         hipLaunchKernelGGL((k_topk<TI, NSLOT, true>), grid, block, 0, stream, a);
-      else
+      } else {
         hipLaunchKernelGGL((k_topk<TI, NSLOT, false>), grid, block, 0, stream, a);
+      }
       break;
     case CacheOp::Score:
       break;
@@ -1294,11 +1323,8 @@ hipError_t launch_dt(const CacheArgs& a, CacheOp op, bool resident, hipStream_t 
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     CacheArgs b = a;
-    b.redo = 1;  // the rows the streamed kernel left
-    if (!resident) return launch_op<TI, 0>(b, op, stream);
-    constexpr int big = TI::BYTES == 2 ? 38 : 19, small = TI::BYTES == 2 ? 16 : 8;
-    if (b.nvec <= (int64_t)small * NT) return launch_op<TI, small>(b, op, stream);
-    return launch_op<TI, big>(b, op, stream);
+    b.redo = 1;  // the rows the streamed kernel left (rare: re-read, not held in registers)
+    return launch_op<TI, 0>(b, op, stream);
   }
   if (!resident) return launch_op<TI, 0>(a, op, stream);
   constexpr int big = TI::BYTES == 2 ? 38 : 19, small = TI::BYTES == 2 ? 16 : 8;
