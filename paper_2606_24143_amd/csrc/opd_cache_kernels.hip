@@ -896,10 +896,23 @@ __global__ void __launch_bounds__(NT) k_topk(CacheArgs a) {
 template <class TI, int NSLOT, bool LSE>
 __global__ void __launch_bounds__(NT) k_topk_redo(CacheArgs a) {
   __shared__ TopkLds sh;
-  for (int64_t row = blockIdx.x; row < a.N; row += gridDim.x) {  // workgroup-uniform
-    if (a.ids_out[row * a.K] != kTopkRedo) continue;
-    topk_row<TI, NSLOT, LSE>(a, row, sh);
-    __syncthreads();  // the next row's writes to LDS wait for this row's reads
+  __shared__ uint32_t s_n;
+  __shared__ int64_t s_rows[NT];
+  const int64_t stride = (int64_t)gridDim.x;
+  // the workgroup's rows are blockIdx.x + i * stride; a lane reads one row's
+  // mark, so a batch of NT rows costs one round trip, and only the marked
+  // rows are redone
+  for (int64_t base = blockIdx.x; base < a.N; base += stride * NT) {  // workgroup-uniform
+    if (threadIdx.x == 0) s_n = 0u;
+    __syncthreads();
+    const int64_t row = base + (int64_t)threadIdx.x * stride;
+    if (row < a.N && a.ids_out[row * a.K] == kTopkRedo) s_rows[atomicAdd(&s_n, 1u)] = row;
+    __syncthreads();
+    const uint32_t n = s_n;
+    for (uint32_t i = 0; i < n; ++i) {
+      topk_row<TI, NSLOT, LSE>(a, s_rows[i], sh);
+      __syncthreads();  // the next row's writes to LDS wait for this row's reads
+    }
   }
 }
 
