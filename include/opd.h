@@ -305,10 +305,10 @@ int opd_validate_cache(const opd_cache* cache, int32_t estimator, int64_t N, int
  *   order) exceeds uniforms[t, i].  The uniforms are supplied by the caller
  *   ([N, M] fp32 in [0, 1)), so the draws are a deterministic function of
  *   them.  The CDF is evaluated in double precision (terms exp(z_j - max) to
- *   about 3e-15 relative, double sums), so a draw is the one exact arithmetic gives
- *   unless uniforms[t, i] lies within about 1e-14 of a cumulative value;
- *   terms below 1e-301 of the largest count as 0, and a drawn id always has
- *   nonzero probability.
+ *   about 1.5e-15 relative, double sums), so a draw is the one exact arithmetic
+ *   gives unless uniforms[t, i] lies within about 1e-14 of a cumulative value;
+ *   terms follow double's gradual underflow, -inf logits have exactly zero
+ *   mass, and a drawn id always has nonzero probability.
  *     sampled_ids [N, M] int32 out; logp [N, M] fp32 out (nullable) =
  *     log softmax(z) at the draw, the rollout-time log-probability the MC
  *     estimators read as behav_logp.  A uniform outside [0, 1) (or NaN), or a

@@ -178,60 +178,59 @@ constexpr int kSmpStepVecs = 16 * kSmpLoads;   // vectors per DPP-row step (128)
 constexpr int kSmpMaxChunks = 2048;            // records per row
 
 // exp(z - m) in double for a logit z <= m, table-driven (Tang, ACM TOMS
-// 15(2), 1989): d = z - m (exact in double) = (n / 64) ln 2 + r with |r| at
-// most about ln 2 / 128, exp(d) = 2^(n >> 6) 2^((n & 63) / 64) exp(r), and
-// exp(r) by a degree-4 polynomial: the interpolant of exp at the five
-// Chebyshev nodes of [-1.002 ln 2 / 128, 1.002 ln 2 / 128], computed in
-// extended precision and rounded to double (within 2.5e-15 relative of exp
-// there, against 3e-15 for the degree-5 Taylor polynomial on twice the
-// range).  n = round(d 64 / ln 2) comes from one fused multiply-add onto
-// 1.5 * 2^52, whose low word is then n and whose value less 1.5 * 2^52 is n
-// as a double; ln 2 / 64 is split in the Cody-Waite way (the high part's 32
-// significant bits make n times it exact for |n| < 2^21).  2^(n >> 6) goes
-// into the exponent field by an integer add.  Below d = -693 (a term below
-// 1e-301 of the largest; also z = -inf) the term is 0; a NaN d (a NaN logit,
-// or z = m = +inf) gives NaN, which leaves the record, and so the row,
-// undefined.
-constexpr int kExpTab = 64;
-constexpr double kInvStep = 92.332482616893656;            // 64 / ln 2
+// 15(2), 1989): d = z - m (exact in double) = (n / 512) ln 2 + r with |r|
+// at most about ln 2 / 1024, exp(d) = 2^(n >> 9) 2^((n & 511) / 512) exp(r),
+// and exp(r) by a cubic: the interpolant of exp at the four Chebyshev nodes
+// of [-1.002 ln 2 / 1024, 1.002 ln 2 / 1024], computed in 50-digit decimal
+// arithmetic and rounded to double (within 1.2e-15 relative of exp there).
+// d is first raised to at least -2000, which keeps the reduction in range
+// (-inf and far negative terms come out as 0).  n = round(d 512 / ln 2)
+// comes from one fused multiply-add onto 1.5 * 2^52, whose low word is then
+// n and whose value less 1.5 * 2^52 is n as a double; ln 2 / 512 is split in
+// the Cody-Waite way (the high part's 32 significant bits make n times it
+// exact for |n| < 2^21).  2^(n >> 9) is applied by ldexp, which rounds
+// through double's gradual underflow (a term below about 4.9e-324 of the
+// chunk max is 0).  The clamp also turns a NaN d into 0: NaN logits and
+// infinite maxima are caught by the chunk max instead (chunk_record), whose
+// record is then NaN, and so the row undefined.
+constexpr int kExpTab = 512;
+constexpr int kExpTabBits = 9;
+constexpr double kDeadArg = -2000.0;
+constexpr double kInvStep = 738.6598609351493;             // 512 / ln 2
 constexpr double kShift52 = 6755399441055744.0;            // 1.5 * 2^52
-constexpr double kStepHi = 6.93147180369123816490e-01 / 64.0;
-constexpr double kStepLo = 1.90821492927058770002e-10 / 64.0;
-constexpr double kP4 = 0.041666717487447574, kP3 = 0.16666697335347525,
-                 kP2 = 0.4999999999996304, kP1 = 0.9999999999977427;
+constexpr double kStepHi = 6.93147180369123816490e-01 / kExpTab;
+constexpr double kStepLo = 1.90821492927058770002e-10 / kExpTab;
+constexpr double kQ3 = 0.16666667050025266, kQ2 = 0.50000001916793,
+                 kQ1 = 0.9999999999999998, kQ0 = 0.9999999999999989;
 
 struct SmpLds {
   double s[kSmpMaxChunks];  // chunk sum at its max; then at the row max
   float m[kSmpMaxChunks];   // chunk max
   double p[kSmpThreads];    // inclusive prefix of the runs
-  double tab[kExpTab];      // 2^(j / 64)
+  double tab[kExpTab];      // 2^(j / 512)
   double wt[kSmpWaves];
   float red[kSmpWaves];
 };
 
-// (c3 is kP3, passed in a vector register: one instruction cannot read two
+// (c2 is kQ2, passed in a vector register: one instruction cannot read two
 // scalar constants, and a register the caller holds is not re-materialised
 // per call)
-__device__ __forceinline__ double exp_reduced(double d, const double* tab, double c3) {
+__device__ __forceinline__ double exp_reduced(double d, const double* tab, double c2) {
+  d = fmax(d, kDeadArg);
   const double xs = fma(d, kInvStep, kShift52);
   const double nd = xs - kShift52;
   const int n = (int)(uint32_t)__builtin_bit_cast(uint64_t, xs);
   double r = fma(-nd, kStepHi, d);
   r = fma(-nd, kStepLo, r);
-  double p = fma(r, kP4, c3);
-  p = fma(p, r, kP2);
-  p = fma(p, r, kP1);
-  p = fma(p, r, 1.0);
-  u32x2 t = __builtin_bit_cast(u32x2, tab[n & (kExpTab - 1)] * p);  // in [0.99, 2.02]
-  uint32_t k = (uint32_t)(n >> 6);  // >= -1000 where the term is live
-  asm("" : "+v"(k));                 // (kept whole, so the add below is one shift-add)
-  t[1] += k << 20;
-  return !(d <= -693.0) ? __builtin_bit_cast(double, t) : 0.0;
+  double p = fma(r, kQ3, c2);
+  p = fma(p, r, kQ1);
+  p = fma(p, r, kQ0);
+  return ldexp(tab[n & (kExpTab - 1)] * p, n >> kExpTabBits);
 }
 
-// kP3 in a vector register (see exp_reduced)
-__device__ __forceinline__ double c3_reg() {
-  double c = kP3;
+// kQ2 in a vector register (see exp_reduced)
+__device__ __forceinline__ double c2_reg() {
+  double c = kQ2;
   asm volatile("" : "+v"(c));
   return c;
 }
@@ -239,27 +238,48 @@ __device__ __forceinline__ double c3_reg() {
 // The term for one fp32 logit z against the chunk max (md, in double).  The
 // single expression both the chunk records and the draws use, so the draws
 // recompute bit for bit the terms the records summed.
-__device__ __forceinline__ double term(float z, double md, const double* tab, double c3) {
-  return exp_reduced((double)z - md, tab, c3);
+__device__ __forceinline__ double term(float z, double md, const double* tab, double c2) {
+  return exp_reduced((double)z - md, tab, c2);
 }
 
 // exp(x) for one double x <= 0 (the row-max scale of a chunk record)
 __device__ __forceinline__ double exp_neg(double x, const double* tab) {
-  return exp_reduced(x, tab, c3_reg());
+  return exp_reduced(x, tab, c2_reg());
 }
 
-// max over the 16 lanes of a DPP row, in every lane of the row
+// max that propagates NaN (IEEE 754-2019 maximum; v_maximum3_f32 on gfx950)
+__device__ __forceinline__ float max_nan(float a, float b) {
+  return __builtin_elementwise_maximum(a, b);
+}
+__device__ __forceinline__ float max3_nan(float a, float b, float c) {
+  return __builtin_elementwise_maximum(__builtin_elementwise_maximum(a, b), c);
+}
+
+// max over the 16 lanes of a DPP row, in every lane of the row (NaN if any
+// lane holds NaN)
 __device__ __forceinline__ float row16_max(float x) {
-  x = fmaxf(x, dpp_move<0x140>(x));  // row_mirror
-  x = fmaxf(x, dpp_move<0x141>(x));  // row_half_mirror
-  x = fmaxf(x, dpp_move<0xB1>(x));   // quad_perm [1,0,3,2]
-  x = fmaxf(x, dpp_move<0x4E>(x));   // quad_perm [2,3,0,1]
+  x = max_nan(x, dpp_move<0x140>(x));  // row_mirror
+  x = max_nan(x, dpp_move<0x141>(x));  // row_half_mirror
+  x = max_nan(x, dpp_move<0xB1>(x));   // quad_perm [1,0,3,2]
+  x = max_nan(x, dpp_move<0x4E>(x));   // quad_perm [2,3,0,1]
   return x;
 }
-// sum over the 16 lanes of a DPP row (butterfly, fixed order), in every lane
+// a double moved across lanes by one DPP pattern (both halves)
+template <int CTRL>
+__device__ __forceinline__ double dpp_move_f64(double v) {
+  u32x2 h = __builtin_bit_cast(u32x2, v);
+  h[0] = (uint32_t)__builtin_amdgcn_mov_dpp((int)h[0], CTRL, 0xF, 0xF, false);
+  h[1] = (uint32_t)__builtin_amdgcn_mov_dpp((int)h[1], CTRL, 0xF, 0xF, false);
+  return __builtin_bit_cast(double, h);
+}
+// sum over the 16 lanes of a DPP row, in every lane of the row: the same
+// four patterns as row16_max; each step adds two values that every lane of a
+// pair holds in swapped order, so all 16 lanes end with the same sum
 __device__ __forceinline__ double row16_sum(double x) {
-#pragma unroll
-  for (int o = 8; o >= 1; o >>= 1) x += __shfl_xor(x, o, 64);
+  x += dpp_move_f64<0x140>(x);  // row_mirror
+  x += dpp_move_f64<0x141>(x);  // row_half_mirror
+  x += dpp_move_f64<0xB1>(x);   // quad_perm [1,0,3,2]
+  x += dpp_move_f64<0x4E>(x);   // quad_perm [2,3,0,1]
   return x;
 }
 // inclusive prefix sum over the 64 lanes of a wavefront, in double
@@ -304,7 +324,7 @@ template <class TI>
 __device__ __forceinline__ void step_terms(const void* zrow, uint32_t v0, uint32_t c1,
                                            uint32_t nvec, int tail, float mq, const double* tab,
                                            double (&w)[8]) {
-  const double md = (double)mq, c3 = c3_reg();
+  const double md = (double)mq, c2 = c2_reg();
   const uint32_t v = v0 + 2u * (uint32_t)(threadIdx.x & 63);
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
@@ -312,7 +332,7 @@ __device__ __forceinline__ void step_terms(const void* zrow, uint32_t v0, uint32
     float f[4];
     unpack<TI>(in ? load_vec<TI>(zrow, v + h, nvec, tail) : neg_inf_vec<TI>(), f);
 #pragma unroll
-    for (int e = 0; e < 4; ++e) w[4 * h + e] = in ? term(f[e], md, tab, c3) : 0.0;
+    for (int e = 0; e < 4; ++e) w[4 * h + e] = in ? term(f[e], md, tab, c2) : 0.0;
   }
 }
 
@@ -417,27 +437,36 @@ __device__ int64_t smp_draw(const SmpLds& c, const void* zrow, uint32_t nvec, in
 // The chunk pass of one DPP row over chunk q (vectors [q CV, q CV + CV)): the
 // chunk max and the double sum of exp(z - max), in every lane of the row.
 // WIDE (more than one step per chunk) takes a max pass and a term pass over
-// the chunk; otherwise the step's eight vectors stay in registers.
+// the chunk; otherwise the step's eight vectors stay in registers, loaded
+// through one buffer resource that starts at the wave's first chunk qw
+// (wave-uniform): the lane offset is fixed and each load's step an
+// immediate.  A q past the last chunk gives the record (-inf, 0).
 template <class TI, bool WIDE>
-__device__ __forceinline__ void chunk_record(const void* zrow, uint32_t q, uint32_t CV,
-                                             uint32_t nvec, int tail, const double* tab,
-                                             float& mq_out, double& sq_out) {
+__device__ __forceinline__ void chunk_record(const void* zrow, uint32_t q, uint32_t qw,
+                                             uint32_t CV, uint32_t nvec, int tail,
+                                             const double* tab, float& mq_out, double& sq_out) {
   typedef typename TI::Vec Vec;
   constexpr int R = kSmpLoads;
   const uint32_t rl = threadIdx.x & 15;
   const bool ragged = tail != TI::EPV;
   const uint32_t c0 = q * CV, c1 = min(c0 + CV, nvec);
   Vec x[R];
+  // (unused when WIDE)
+  const uint32_t wv = (uint32_t)__builtin_amdgcn_readfirstlane((int)(qw * CV));
+  const Rsrc wr = slot_rsrc(zrow, nvec * (uint32_t)sizeof(Vec), wv * (uint32_t)sizeof(Vec));
+  uint32_t loff = (c0 - wv + rl) * (uint32_t)sizeof(Vec);
+  asm("" : "+v"(loff));  // (kept whole, so each load's step is its immediate offset)
   // all R loads are issued before any is used; lanes past the chunk, and
   // elements past V, then become -inf through per-dword selects
   auto load_step = [&](uint32_t s0) {
 #pragma unroll
     for (int b = 0; b < R; ++b) {
-      const uint32_t v = s0 + rl + 16u * b;
-      if constexpr (WIDE)
-        x[b] = ld_cached<TI>(zrow, min(v, nvec - 1));
-      else
-        x[b] = ld_nt<TI>(zrow, min(v, nvec - 1));
+      if constexpr (WIDE) {
+        x[b] = ld_cached<TI>(zrow, min(s0 + rl + 16u * b, nvec - 1));
+      } else {
+        // (s0 is c0 here; lanes past the row read zeros, replaced below)
+        x[b] = buf_ld<TI, kAuxNt>(wr, loff + 16u * (uint32_t)sizeof(Vec) * b);
+      }
     }
     // (a step wholly inside the chunk and clear of a ragged last vector
     // needs no selects)
@@ -454,26 +483,26 @@ __device__ __forceinline__ void chunk_record(const void* zrow, uint32_t q, uint3
       }
     }
   };
-  // (a NaN element, or an infinite maximum, makes the chunk's sum NaN: the
-  // row then has no distribution)
+  // (the max propagates NaN; a NaN or +inf chunk max makes the record NaN:
+  // the row then has no distribution)
   auto step_max = [&]() {
     float lm = kNegInf;
 #pragma unroll
     for (int b = 0; b < R; ++b) {
       float f[4];
       unpack<TI>(x[b], f);
-      lm = max3_raw(max3_raw(lm, f[0], f[1]), f[2], f[3]);
+      lm = max3_nan(max3_nan(lm, f[0], f[1]), f[2], f[3]);
     }
     return lm;
   };
-  const double c3 = c3_reg();
+  const double c2 = c2_reg();
   auto step_sum = [&](double md, double acc) {
 #pragma unroll
     for (int b = 0; b < R; ++b) {
       float f[4];
       unpack<TI>(x[b], f);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) acc += term(f[e], md, tab, c3);
+      for (int e = 0; e < 4; ++e) acc += term(f[e], md, tab, c2);
     }
     return acc;
   };
@@ -484,7 +513,7 @@ __device__ __forceinline__ void chunk_record(const void* zrow, uint32_t q, uint3
   } else {
     for (uint32_t s0 = c0; s0 < c1; s0 += kSmpStepVecs) {
       load_step(s0);
-      lm = fmaxf(lm, step_max());
+      lm = max_nan(lm, step_max());
     }
   }
   const float mq = row16_max(lm);
@@ -500,8 +529,9 @@ __device__ __forceinline__ void chunk_record(const void* zrow, uint32_t q, uint3
       }
     }
   }
+  const double sum = row16_sum(ls);
   mq_out = mq;
-  sq_out = row16_sum(ls);
+  sq_out = mq < __builtin_huge_valf() ? sum : __builtin_nan("");  // NaN or +inf max: NaN
 }
 
 template <class TI, bool WIDE>
@@ -519,7 +549,7 @@ __global__ void __launch_bounds__(kSmpThreads) k_sample(CacheArgs a) {
     if (tid == 0 && a.lse_out) a.lse_out[row] = 0.f;
     return;
   }
-  if (tid < kExpTab) c.tab[tid] = exp2((double)tid / kExpTab);
+  for (int j = tid; j < kExpTab; j += kSmpThreads) c.tab[j] = exp2((double)j / kExpTab);
   __syncthreads();
   const void* zrow = (const char*)a.logits + row * a.ld * TI::BYTES;
   const uint32_t nvec = (uint32_t)a.nvec;
@@ -536,12 +566,12 @@ __global__ void __launch_bounds__(kSmpThreads) k_sample(CacheArgs a) {
     const uint32_t q = q0 + rowk;
     float mq;
     double sq;
-    chunk_record<TI, WIDE>(zrow, min(q, nchunk - 1), CV, nvec, a.tail, c.tab, mq, sq);
+    chunk_record<TI, WIDE>(zrow, q, q0, CV, nvec, a.tail, c.tab, mq, sq);
     if (rl == 15 && q < nchunk) {
       c.m[q] = mq;
       c.s[q] = sq;
     }
-    if (q < nchunk) lmax = fmaxf(lmax, mq);
+    if (q < nchunk) lmax = max_nan(lmax, mq);
   }
   const float Mx = block_max<W>(lmax, c.red);  // ends with a barrier: records visible
   const double Md = (double)Mx;

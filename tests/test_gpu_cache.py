@@ -121,8 +121,9 @@ def test_sample_wide_rows():
 @pytest.mark.parametrize("dtype", [synth.F32, synth.BF16])
 def test_sample_extreme_logit_ranges(dtype):
     """The double-precision terms across logit ranges: a large positive and a
-    large negative row maximum, a row whose terms fall below the 1e-301 cut
-    (z - m down to -800), logits near zero, and a wide spread."""
+    large negative row maximum, a row whose terms run through double's
+    underflow range and below it (z - m down to -800), logits near zero, and
+    a wide spread."""
     rng = np.random.default_rng(31)
     V, N, M = 20000, 5, 64
     x = rng.normal(0.0, 3.0, (N, V))
