@@ -368,7 +368,10 @@ __device__ __forceinline__ void finish_row(const Args& a, int64_t row, float L, 
 // The row jitter of k_row_resident: calls with fewer cache entries than
 // kJitterMaxK over at least kJitterMinRows rows (16 rounds of the 256 CUs).
 // Measured over 32,768 unmasked rows of V = 151,936 bf16: MC1 5.80 ms
-// without, 5.23 ms with (MC16 over the same rows, without: 5.23 ms).
+// without, 5.23 ms with (MC16 over the same rows, without: 5.23 ms); twice
+// the wait gave 5.37 ms.  k_row_dense_resident waits twice as long (its rows
+// take longer): FKL and RKL over 16,384 rows 3.59 -> 3.51 ms (half the wait:
+// 3.53 ms, three times: 3.54 ms).
 constexpr int kJitterMaxK = 16;
 constexpr int64_t kJitterMinRows = 4096;
 
@@ -583,6 +586,12 @@ __global__ void __launch_bounds__(kRowThreads) k_row_dense_resident(Args a) {
     return;
   }
   const uint32_t nvec = (uint32_t)a.nvec;  // <= NSLOT * NT
+  // Every dense row costs the same, so the CUs would fall into step (see
+  // k_row_resident): a wait of 0..7 x 4096 cycles, a hash of the row.
+  if (a.N >= kJitterMinRows) {
+    const uint32_t n = ((uint32_t)row * 0x9E3779B1u) >> 29;
+    for (uint32_t i = 0; i < n; ++i) __builtin_amdgcn_s_sleep(64);
+  }
   // Slot s of a lane is vector s * NT + tid of the row, read and written
   // through the slot's buffer resource: past the row's last vector, loads
   // return zeros (replaced by -inf below) and gradient stores are dropped.
