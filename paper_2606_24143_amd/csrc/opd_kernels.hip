@@ -272,12 +272,16 @@ __device__ __forceinline__ void apply_spikes(IdxT v, float (&g)[EPV], int K, con
 }
 
 // Exact spike map of a resident row: bit s of spk[s >> 5][lane] is set when
-// the vector that lane holds in register slot s carries a spike.  Wave 0
-// marks the K cached ids after the estimator has run; sweep 2 then tests one
-// bit per slot instead of looking every vector up.
+// the vector that lane holds in register slot s carries a spike, and bit i
+// of ent[s] (K bits) when cache entry i falls in slot s.  Wave 0 marks the K
+// cached ids after the estimator has run; sweep 2 then tests one bit per
+// slot instead of looking every vector up, and a vector with a spike visits
+// only its slot's entries.
+constexpr int kEntWords = kKMax / 64;
 template <int NT>
 __device__ __forceinline__ void mark_spike_slots(int K, uint32_t nvec, const CacheLds& c,
-                                                 uint32_t (*spk)[NT]) {
+                                                 uint32_t (*spk)[NT],
+                                                 uint64_t (*ent)[kEntWords]) {
   const uint32_t full = nvec / NT;  // slots that are not moved back
   for (int i = threadIdx.x & 63; i < K; i += 64) {
     const int id = c.id[i];
@@ -286,22 +290,33 @@ __device__ __forceinline__ void mark_spike_slots(int K, uint32_t nvec, const Cac
     const uint32_t s = v < full * NT ? v / NT : full;
     const uint32_t lane = v - slot_base<NT>((int)s, nvec);
     atomicOr(&spk[s >> 5][lane], 1u << (s & 31));
+    atomicOr(&ent[s][i >> 6], 1ull << (i & 63));
   }
 }
 
 // Add the spikes that fall inside vector v (a vector known to hold at least
-// one), in ascending cache order.
+// one), in ascending cache order: the entries of v's slot (ent, the same for
+// every lane of the wave), lowest index first.
 template <int EPV>
-__device__ __forceinline__ void add_spikes(uint32_t v, float (&g)[EPV], int K, const CacheLds& c) {
+__device__ __forceinline__ void add_spikes(uint32_t v, float (&g)[EPV], int K,
+                                           const uint64_t* ent, const CacheLds& c) {
   const int base = (int)(v * EPV);
 #pragma unroll 1
-  for (int i = 0; i < K; ++i) {
-    const uint32_t off = (uint32_t)(c.id[i] - base);
-    if (off < (uint32_t)EPV) {
-      const float w = c.w[i];
+  for (int wd = 0; wd < ((K + 63) >> 6); ++wd) {
+    uint64_t m = ent[wd];
+    m = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(m >> 32)) << 32) |
+        (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)m);
+#pragma unroll 1
+    while (m != 0ull) {
+      const int i = wd * 64 + __builtin_ctzll(m);
+      m &= m - 1ull;
+      const uint32_t off = (uint32_t)(c.id[i] - base);
+      if (off < (uint32_t)EPV) {
+        const float w = c.w[i];
 #pragma unroll
-      for (int e = 0; e < EPV; ++e)
-        if (off == (uint32_t)e) g[e] += w;
+        for (int e = 0; e < EPV; ++e)
+          if (off == (uint32_t)e) g[e] += w;
+      }
     }
   }
 }
@@ -365,14 +380,13 @@ __device__ __forceinline__ void finish_row(const Args& a, int64_t row, float L, 
 
 // ---------------------------------------------------------------- row-per-workgroup kernels
 
-// The row jitter of k_row_resident: calls with fewer cache entries than
-// kJitterMaxK over at least kJitterMinRows rows (16 rounds of the 256 CUs).
-// Measured over 32,768 unmasked rows of V = 151,936 bf16: MC1 5.80 ms
-// without, 5.23 ms with (MC16 over the same rows, without: 5.23 ms); twice
-// the wait gave 5.37 ms.  k_row_dense_resident waits twice as long (its rows
-// take longer): FKL and RKL over 16,384 rows 3.59 -> 3.51 ms (half the wait:
-// 3.53 ms, three times: 3.54 ms).
-constexpr int kJitterMaxK = 16;
+// The row jitter of the row kernels: calls over at least kJitterMinRows rows
+// (16 rounds of the 256 CUs).  Measured over 32,768 unmasked rows of
+// V = 151,936 bf16 in k_row_resident: MC1 5.80 ms without, 5.23 ms with;
+// twice the wait 5.37 ms, 0..15 x 1024 or 0..31 x 512 cycles 5.24-5.26 ms.
+// k_row_dense_resident waits twice as long (its rows take longer): FKL and
+// RKL over 16,384 rows 3.59 -> 3.51 ms (half the wait: 3.53 ms, three
+// times: 3.54 ms).
 constexpr int64_t kJitterMinRows = 4096;
 
 // One 1024-lane workgroup per token row, the whole row held in registers
@@ -386,6 +400,7 @@ __global__ void __launch_bounds__(kRowThreads) k_row_resident(Args a) {
   __shared__ float s_red[NW];
   __shared__ CacheLds c;
   __shared__ uint32_t s_spk[2][NT];
+  __shared__ uint64_t s_ent[NSLOT][kEntWords];
   static_assert(NSLOT <= 64, "spike map holds 64 slots");
   const int tid = threadIdx.x;
   const int64_t row = xcd_remap(blockIdx.x, gridDim.x);
@@ -397,14 +412,14 @@ __global__ void __launch_bounds__(kRowThreads) k_row_resident(Args a) {
   }
   s_spk[0][tid] = 0u;
   s_spk[1][tid] = 0u;
+  for (int w = tid; w < NSLOT * kEntWords; w += NT) (&s_ent[0][0])[w] = 0ull;
   const uint32_t nvec = (uint32_t)a.nvec;  // <= NSLOT * NT
   const int K = a.K;
-  // Rows with few cache entries take nearly the same time each, so the
-  // workgroups on all CUs fall into step: they load together and store
-  // together, and HBM idles between the bursts.  A wait of 0..7 x 2048
-  // cycles, a hash of the row, keeps them out of step (rows with more
-  // entries vary by their spike work already).
-  if (K < kJitterMaxK && a.N >= kJitterMinRows) {
+  // Every row takes nearly the same time, so the workgroups on all CUs
+  // fall into step: they load together and store together, and HBM idles
+  // between the bursts.  A wait of 0..7 x 2048 cycles, a hash of the row,
+  // keeps them out of step.
+  if (a.N >= kJitterMinRows) {
     const uint32_t n = ((uint32_t)row * 0x9E3779B1u) >> 29;
     for (uint32_t i = 0; i < n; ++i) __builtin_amdgcn_s_sleep(32);
   }
@@ -500,7 +515,7 @@ __global__ void __launch_bounds__(kRowThreads) k_row_resident(Args a) {
 
   if (tid < 64) {
     finish_row<TI, EST, false>(a, row, L, true, c);
-    mark_spike_slots<NT>(K, nvec, c, s_spk);
+    mark_spike_slots<NT>(K, nvec, c, s_spk, s_ent);
   }
   __syncthreads();
   // A row with an id outside [0, V) becomes NaN through its coefficient (MC:
@@ -527,7 +542,7 @@ __global__ void __launch_bounds__(kRowThreads) k_row_resident(Args a) {
         for (int e = 0; e < EPV; ++e) g[e] = g0;
       }
       if ((((s < 32 ? spk_lo : spk_hi) >> (s & 31)) & 1u) != 0u)
-        add_spikes<EPV>(b + (uint32_t)tid2, g, K, c);
+        add_spikes<EPV>(b + (uint32_t)tid2, g, K, s_ent[s], c);
       store_vec<TI, TO>((char*)grow + (size_t)b * EPV * TO::BYTES, (uint32_t)tid2, g, EPV);
     };
 #pragma unroll
