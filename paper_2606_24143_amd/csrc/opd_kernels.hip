@@ -107,6 +107,8 @@ struct CacheLds {
   float b[kKMax];
   float w[kKMax];  // spike weights, already scaled by gamma
   uint32_t filter[kFilterWords];
+  uint64_t skey[kKMax];  // (vector << 32 | entry), ascending (set_filter)
+  uint64_t ukey[kKMax];  // the same keys by entry index
   float C;        // coefficient of p_theta in the gradient row
   int bad;        // the row has an id outside [0, V)
 };
@@ -242,31 +244,58 @@ __device__ __forceinline__ float estimate(int K, float L, float gmu, int variant
   }
 }
 
+// Wave 0: the filter bits, and the entries sorted by (vector, index) in
+// skey (a rank sort: entry i goes to the number of keys below its own; the
+// keys are distinct, and an id outside [0, V) sorts last).
 template <int EPV>
 __device__ __forceinline__ void set_filter(int K, CacheLds& c) {
-  for (int i = threadIdx.x & 63; i < K; i += 64) {
+  const int lane = threadIdx.x & 63;
+  auto key = [&](int i) {
+    const int id = c.id[i];
+    const uint32_t v = id >= 0 ? (uint32_t)id / (uint32_t)EPV : 0xFFFFFFFFu;
+    return ((uint64_t)v << 32) | (uint32_t)i;
+  };
+  for (int i = lane; i < K; i += 64) {
     const int id = c.id[i];
     if (id >= 0) {
       const int v = id / EPV;
       atomicOr(&c.filter[(v & (kFilterBits - 1)) >> 5], 1u << (v & 31));
     }
   }
+  // the keys by entry index, then each group of 64 ranked against all K and
+  // written to its place in skey
+  for (int i = lane; i < K; i += 64) c.ukey[i] = key(i);
+#pragma unroll 1
+  for (int i0 = 0; i0 < K; i0 += 64) {  // wave-uniform
+    const uint64_t ki = i0 + lane < K ? c.ukey[i0 + lane] : ~0ull;
+    int r = 0;
+#pragma unroll 4
+    for (int j = 0; j < K; ++j) r += c.ukey[j] < ki ? 1 : 0;
+    if (i0 + lane < K) c.skey[r] = ki;
+  }
 }
 
-// Add the spikes that fall inside vector v, in ascending cache order.
+// Add the spikes that fall inside vector v, in ascending cache order: a
+// binary search of skey for v's first entry, then v's run.
 template <int EPV, class IdxT>
 __device__ __forceinline__ void apply_spikes(IdxT v, float (&g)[EPV], int K, const CacheLds& c) {
   const uint32_t word = c.filter[(v & (kFilterBits - 1)) >> 5];
   if ((word >> (v & 31)) & 1u) {
-    const int64_t base = v * EPV;
-    for (int i = 0; i < K; ++i) {
+    const uint64_t lo = (uint64_t)(uint32_t)v << 32;
+    int a = 0, b = K;
+    while (a < b) {
+      const int mid = (a + b) >> 1;
+      if (c.skey[mid] < lo) a = mid + 1;
+      else b = mid;
+    }
+    const int64_t base = (int64_t)v * EPV;
+    for (; a < K && (c.skey[a] >> 32) == (uint64_t)(uint32_t)v; ++a) {
+      const int i = (int)(uint32_t)c.skey[a];
       const int64_t off = (int64_t)c.id[i] - base;
-      if (off >= 0 && off < EPV) {
-        const float w = c.w[i];
+      const float w = c.w[i];
 #pragma unroll
-        for (int e = 0; e < EPV; ++e)
-          if (off == e) g[e] += w;
-      }
+      for (int e = 0; e < EPV; ++e)
+        if (off == e) g[e] += w;
     }
   }
 }
