@@ -14,7 +14,8 @@ Prints one JSON line on stdout:
               over the mean launch time measured with HIP events on the
               launch stream, against the 8 TB/s MI355X peak; also the same
               rate as a fraction of a plain device copy measured in the same
-              process (frac_of_copy)
+              process (frac_of_copy), and a plain read's rate (read_GBps, from
+              bench_probe.so; for the cache-building calls also frac_of_read)
   accounting_model  the launch priced with a second read of each row for the
               estimators whose gradient is dense (MC, truncated top-k,
               dense), as a two-read/one-write accounting counts it.  The
@@ -215,6 +216,47 @@ def copy_peak(dev, stream, mib: int = 2048):
     return res
 
 
+def read_peak(dev, stream, mib: int = 2048):
+    """GB/s of one plain read of `mib` MiB by bench_probe.so (8,192
+    workgroups of 256 lanes, each streaming its own share with non-temporal
+    16-byte loads); None when the probe is not built."""
+    import ctypes
+
+    import torch
+
+    path = os.path.join(ROOT, "bench_probe.so")
+    if not os.path.exists(path):
+        return None
+    lib = ctypes.CDLL(path)
+    lib.bench_read_probe.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_void_p,
+                                     ctypes.c_int, ctypes.c_void_p]
+    lib.bench_read_probe.restype = ctypes.c_int
+    nbytes, groups = mib << 20, 8192
+    buf = torch.ones(nbytes // 4, dtype=torch.int32, device=dev)
+    out = torch.empty(groups, dtype=torch.int32, device=dev)
+
+    def once():
+        rc = lib.bench_read_probe(ctypes.c_void_p(buf.data_ptr()), nbytes,
+                                  ctypes.c_void_p(out.data_ptr()), groups,
+                                  ctypes.c_void_p(stream.cuda_stream))
+        if rc != 0:
+            raise RuntimeError("bench_read_probe failed: hipError_t %d" % rc)
+
+    for _ in range(3):
+        once()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(10):
+        once()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    gbs = nbytes * 10 / (e0.elapsed_time(e1) / 1e3) / 1e9
+    del buf, out
+    torch.cuda.empty_cache()
+    return gbs
+
+
 def cpu_baseline(w, est, d, rows: int, threads: int, chunk: int = 512):
     """The oracle as it stands, over the first `rows` token rows of the timed
     workload, in chunks (so its fp64 gradient buffer stays small); only the
@@ -318,6 +360,7 @@ def main():
     stream = torch.cuda.current_stream()
     copies = copy_peak(dev, stream, args.copy_mib) if args.copy_mib else None
     copy_gbs = max(copies.values()) if copies else None
+    read_gbs = read_peak(dev, stream, args.copy_mib) if args.copy_mib else None
 
     def loss_inputs():
         kw = {}
@@ -449,6 +492,10 @@ def main():
         res["roofline"]["copy_GBps"] = copy_gbs
         res["roofline"]["copy_patterns_GBps"] = copies
         res["roofline"]["frac_of_copy"] = achieved / copy_gbs
+    if read_gbs:
+        res["roofline"]["read_GBps"] = read_gbs
+        if op != "loss":  # the cache-building calls read each row once and write little
+            res["roofline"]["frac_of_read"] = achieved / read_gbs
     if op == "loss":
         model = alg + second_read_bytes(w, est, n_valid)
         res["accounting_model"] = {
