@@ -218,6 +218,29 @@ def test_no_is_estimator_needs_no_behaviour_logprobs():
     compare("nois", w, d, "rkl_mc_nois", out, oracle_for(w, d, "rkl_mc_nois", mask), mask)
 
 
+@pytest.mark.parametrize("est", ["rkl_mc", "fkl_topk", "rkl_topk_trunc"])
+def test_large_support_on_the_streaming_path(est):
+    """K = 256 on rows the streaming kernel takes (V not a multiple of 4), and
+    on the split path: spikes found through the sorted entries, MC with
+    repeated ids (40 distinct values over 256 draws) adding in order."""
+    V, ld, N, K = 5001, 5008, 5, 256
+    w = synth.Workload("t_kstream", N=N, V=V, dtype=synth.BF16, estimators=(est,), k=K, M=K,
+                       sigma_student=2.0, sigma_behaviour=0.4, seed=77)
+    d = synth.generate(w, ld=ld)
+    if est == "rkl_mc":
+        rng = np.random.default_rng(7)
+        ids = d["mc_ids"].copy()
+        for r in range(N):
+            ids[r] = rng.choice(rng.choice(V, 40, replace=False), K)
+        d = dict(d, mc_ids=ids)
+    say("large support on the streaming path %s" % est)
+    ids, tau, beta = cache_arrays(d, est)
+    logits = to_dev(d["logits"])[:, :V]
+    for flags in PATHS.values():
+        out = run_gpu(logits, est, ids, tau, beta, flags=flags, want_lse=True, want_gathered=True)
+        compare("%s/stream K=%d" % (est, K), w, d, est, out, oracle_for(w, d, est, None))
+
+
 def test_mc_duplicate_samples_accumulate():
     """Samples are iid with replacement (App. E): repeated ids are separate
     terms of the average, so their gradient spikes add."""
