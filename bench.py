@@ -28,6 +28,10 @@ between steps) are rotated over several copies of the inputs and outputs, so
 consecutive steps read and write different memory; config.buffer_sets says how
 many.
 
+--graph captures each call in a HIP graph and times the replays, which
+removes the host's launch overhead from the small, launch-bound workloads
+(config.launch says which was timed).
+
 --op sample|topk|score times one of the cache-building calls instead (Stage
 1 draws with their log-probs, the top-k support, or scoring at cached ids)
 on the same kind of rows; each reads every valid row once.
@@ -308,6 +312,9 @@ def main():
                     help="time only the first ROWS rows of the workload (0 = all)")
     ap.add_argument("--path", default="auto", choices=("auto", "rowwise", "split"),
                     help="force the loss call's path (the split path gets its workspace)")
+    ap.add_argument("--graph", action="store_true",
+                    help="capture each call in a HIP graph and time its replays (no host "
+                         "launch overhead in the timed steps)")
     ap.add_argument("--min-set-gib", type=float, default=1.0,
                     help="rotate input/output copies until the timed steps span this many GiB")
     args = ap.parse_args()
@@ -394,11 +401,11 @@ def main():
         ws = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev) if nbytes else None
         counter = [0]
 
-        def step():
+        def step(s=stream):
             b = bufs[counter[0] % sets]
             counter[0] += 1
             opd.loss_fwd_bwd(b["logits"], est, mask=mask, out=b["out"], workspace=ws,
-                             stream=stream, flags=path_flags, **b["kw"])
+                             stream=s, flags=path_flags, **b["kw"])
     else:
         if op == "sample":
             u_np = np.stack([synth.uniforms(w.seed + 1, synth.STREAM_SAMPLE, r, w.M)
@@ -406,11 +413,11 @@ def main():
             u_np = (np.floor(u_np * 2.0 ** 24) / 2.0 ** 24).astype(np.float32)
             u_dev = dev_t(u_np)
 
-            def step():
-                opd.sample_actions(logits, u_dev, mask=mask, stream=stream)
+            def step(s=stream):
+                opd.sample_actions(logits, u_dev, mask=mask, stream=s)
         elif op == "topk":
-            def step():
-                opd.topk_support(logits, w.k, mask=mask, stream=stream)
+            def step(s=stream):
+                opd.topk_support(logits, w.k, mask=mask, stream=s)
         elif op == "diag":
             # the inputs are what an MC loss call returns (lse_out, gathered_out)
             aux = opd.loss_fwd_bwd(logits, est, mask=mask, want_lse=True, want_gathered=True, **kw)
@@ -419,19 +426,41 @@ def main():
             tau_dev, beta_dev = kw["teacher_logp"], kw["behav_logp"]
             seq = w.rollout_len if w.ragged else 2048
 
-            def step():
+            def step(s=stream):
                 opd.mc_diagnostics(lse_dev, gat_dev, tau_dev, beta_dev, mask=mask,
-                                   group_sizes=(2, 4, 8), seq_len=seq, stream=stream)
+                                   group_sizes=(2, 4, 8), seq_len=seq, stream=s)
         else:
             ids_dev = dev_t(d["mc_ids"])
 
-            def step():
-                opd.score_actions(logits, ids_dev, mask=mask, stream=stream)
+            def step(s=stream):
+                opd.score_actions(logits, ids_dev, mask=mask, stream=s)
         nbytes = 0
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    if args.graph and op == "diag":
+        print("--graph covers the loss and cache-building calls", file=sys.stderr)
+        sys.exit(2)
+    if args.graph:
+        # one HIP graph per buffer set, each holding one call; the timed steps
+        # replay them in turn on the launch stream
+        graphs = []
+        for _ in range(sets):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                step(torch.cuda.current_stream())
+            graphs.append(g)
+        torch.cuda.synchronize()
+        turn = [0]
+
+        def step(s=stream):
+            graphs[turn[0] % len(graphs)].replay()
+            turn[0] += 1
+
+        for _ in range(args.warmup):
+            step()
+        torch.cuda.synchronize()
 
     starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
     ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
@@ -478,7 +507,7 @@ def main():
                    "dlogits_dtype": "f32", "k": w.k, "M": w.M,
                    "path": "split" if nbytes and op == "loss" else "rowwise",
                    "first_rows_of": synth.WORKLOADS[args.workload].N if args.rows else None,
-                   "buffer_sets": sets},
+                   "buffer_sets": sets, "launch": "hip_graph" if args.graph else "eager"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": achieved / PEAK_HBM_GBS,
                      "traffic": traffic,
