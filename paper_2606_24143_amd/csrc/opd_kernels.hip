@@ -422,7 +422,7 @@ constexpr int64_t kJitterMinRows = 4096;
 // between the sweeps (NSLOT 16-byte vectors per lane): HBM sees one read of
 // the logits and one write of the gradient.  Requires whole vectors
 // (V a multiple of the elements per vector).
-template <class TI, class TO, int EST, int NSLOT>
+template <class TI, class TO, int EST, int NSLOT, bool TAIL>
 __global__ void __launch_bounds__(kRowThreads) k_row_resident(Args a) {
   constexpr int NT = kRowThreads, NW = NT / 64, EPV = TI::EPV;
   static_assert(!is_dense(EST), "dense estimators stream two rows");
@@ -499,11 +499,16 @@ __global__ void __launch_bounds__(kRowThreads) k_row_resident(Args a) {
   float L;
   {
     // only a slot that reaches past the row end has lanes to mask (a
-    // wave-uniform test, so full slots cost no lane work)
+    // wave-uniform test, so full slots cost no lane work); in the slot that
+    // holds the row's last vector, that vector's elements past V become -inf
 #pragma unroll
-    for (int s = 0; s < NSLOT; ++s)
+    for (int s = 0; s < NSLOT; ++s) {
       if ((uint32_t)(s * NT + NT) > nvec && !slot_owns<NT>(s, slot_base<NT>(s, nvec), tid, nvec))
         x[s] = neg_inf_vec<TI>();
+      if constexpr (TAIL)
+        if ((uint32_t)s == (nvec - 1) / NT && slot_base<NT>(s, nvec) + (uint32_t)tid == nvec - 1)
+          mask_tail<TI>(x[s], a.tail);
+    }
     // sweep 1a: row max (EPV independent chains)
     float mx[EPV];
 #pragma unroll
@@ -572,7 +577,12 @@ __global__ void __launch_bounds__(kRowThreads) k_row_resident(Args a) {
       }
       if ((((s < 32 ? spk_lo : spk_hi) >> (s & 31)) & 1u) != 0u)
         add_spikes<EPV>(b + (uint32_t)tid2, g, K, s_ent[s], c);
-      store_vec<TI, TO>((char*)grow + (size_t)b * EPV * TO::BYTES, (uint32_t)tid2, g, EPV);
+      // (with TAIL the row's last vector stores its V - (nvec - 1) EPV
+      // elements only)
+      int valid = EPV;
+      if constexpr (TAIL)
+        valid = (uint32_t)(s * NT + NT) >= nvec2 && b + (uint32_t)tid2 == nvec2 - 1 ? a.tail : EPV;
+      store_vec<TI, TO>((char*)grow + (size_t)b * EPV * TO::BYTES, (uint32_t)tid2, g, valid);
     };
 #pragma unroll
     for (int s = 0; s < NSLOT; ++s) {
@@ -1129,12 +1139,17 @@ hipError_t row_t(const Args& a, Path path, bool read, hipStream_t s) {
   } else {
     if (!read) {
       return hipErrorInvalidValue;  // the write-only top-k form runs launch_topk_sparse
+    } else if (a.tail != TI::EPV && path != Path::RowStream) {
+      // a partial last vector: the variant that masks and stores it element
+      // by element (the others keep whole-vector code)
+      constexpr int NS = slots_large(TI::BYTES == 2 ? BF16 : F32);
+      hipLaunchKernelGGL((k_row_resident<TI, TO, EST, NS, true>), grid, block, 0, s, a);
     } else if (path == Path::RowResidentSmall) {
       constexpr int NS = slots_small(TI::BYTES == 2 ? BF16 : F32);
-      hipLaunchKernelGGL((k_row_resident<TI, TO, EST, NS>), grid, block, 0, s, a);
+      hipLaunchKernelGGL((k_row_resident<TI, TO, EST, NS, false>), grid, block, 0, s, a);
     } else if (path == Path::RowResidentLarge) {
       constexpr int NS = slots_large(TI::BYTES == 2 ? BF16 : F32);
-      hipLaunchKernelGGL((k_row_resident<TI, TO, EST, NS>), grid, block, 0, s, a);
+      hipLaunchKernelGGL((k_row_resident<TI, TO, EST, NS, false>), grid, block, 0, s, a);
     } else {
       hipLaunchKernelGGL((k_row_stream<TI, TO, EST>), grid, block, 0, s, a);
     }

@@ -218,13 +218,18 @@ def test_no_is_estimator_needs_no_behaviour_logprobs():
     compare("nois", w, d, "rkl_mc_nois", out, oracle_for(w, d, "rkl_mc_nois", mask), mask)
 
 
+@pytest.mark.parametrize("rows", ["stream_f32", "resident_tail_bf16"])
 @pytest.mark.parametrize("est", ["rkl_mc", "fkl_topk", "rkl_topk_trunc"])
-def test_large_support_on_the_streaming_path(est):
-    """K = 256 on rows the streaming kernel takes (V not a multiple of 4), and
-    on the split path: spikes found through the sorted entries, MC with
-    repeated ids (40 distinct values over 256 draws) adding in order."""
-    V, ld, N, K = 5001, 5008, 5, 256
-    w = synth.Workload("t_kstream", N=N, V=V, dtype=synth.BF16, estimators=(est,), k=K, M=K,
+def test_large_support_on_the_streaming_path(est, rows):
+    """K = 256 on fp32 rows wider than the registers (the streaming kernel:
+    spikes found through the entries sorted by vector) and on bf16 rows
+    whose last vector is partial (the resident kernel's tail), each also on
+    the split path; MC with repeated ids (40 distinct values over 256
+    draws) adding in order."""
+    dtype, V, ld = {"stream_f32": (synth.F32, 80000, 80000),
+                    "resident_tail_bf16": (synth.BF16, 5001, 5008)}[rows]
+    N, K = 5, 256
+    w = synth.Workload("t_kstream", N=N, V=V, dtype=dtype, estimators=(est,), k=K, M=K,
                        sigma_student=2.0, sigma_behaviour=0.4, seed=77)
     d = synth.generate(w, ld=ld)
     if est == "rkl_mc":
@@ -233,12 +238,12 @@ def test_large_support_on_the_streaming_path(est):
         for r in range(N):
             ids[r] = rng.choice(rng.choice(V, 40, replace=False), K)
         d = dict(d, mc_ids=ids)
-    say("large support on the streaming path %s" % est)
+    say("large support %s %s" % (rows, est))
     ids, tau, beta = cache_arrays(d, est)
     logits = to_dev(d["logits"])[:, :V]
     for flags in PATHS.values():
         out = run_gpu(logits, est, ids, tau, beta, flags=flags, want_lse=True, want_gathered=True)
-        compare("%s/stream K=%d" % (est, K), w, d, est, out, oracle_for(w, d, est, None))
+        compare("%s/%s K=%d" % (est, rows, K), w, d, est, out, oracle_for(w, d, est, None))
 
 
 def test_mc_duplicate_samples_accumulate():
