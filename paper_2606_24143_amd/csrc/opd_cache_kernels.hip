@@ -1063,14 +1063,25 @@ __global__ void __launch_bounds__(kTkThreads) k_topk_stream(CacheArgs a) {
           if (!(v < nvec && v * 4u + e < V32)) f[e] = kNegInf;
       }
     };
+    // the tile's maximum; with LSE (registers to spare) each vector's
+    // maximum is also kept, so pass B skips vectors below the bound unread
+    static_assert(B == 8, "the tile maximum below folds eight vectors");
+    float vmx[B];
     float tmx = kNegInf;
 #pragma unroll
     for (int b = 0; b < B; ++b) {
       float f[4];
       vals(b, f);
-      tmx = max3_raw(max3_raw(tmx, f[0], f[1]), f[2], f[3]);
-      if constexpr (!LSE) chk += (f[0] + f[1]) + (f[2] + f[3]);
+      if constexpr (LSE) {
+        vmx[b] = max3_raw(max3_raw(f[0], f[1], f[2]), f[3], f[3]);
+      } else {
+        tmx = max3_raw(max3_raw(tmx, f[0], f[1]), f[2], f[3]);
+        chk += (f[0] + f[1]) + (f[2] + f[3]);
+      }
     }
+    if constexpr (LSE)
+      tmx = max3_raw(max3_raw(vmx[0], vmx[1], vmx[2]), max3_raw(vmx[3], vmx[4], vmx[5]),
+                     max3_raw(vmx[6], vmx[7], vmx[7]));
     if constexpr (LSE) {
       const float mn = fmaxf(m, tmx);
       if (mn != kNegInf) {  // (a lane that never sees a finite value sends its row to the fallback)
@@ -1116,14 +1127,15 @@ __global__ void __launch_bounds__(kTkThreads) k_topk_stream(CacheArgs a) {
           Vec xv = x[b];
           keep_packed(xv);  // unpacked again here rather than held since pass A
           float f[4];
-          unpack<TI>(xv, f);
-          if constexpr (!FULL) {
-            const uint32_t v = t0 + 64u * b + lane;
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-              if (!(v < nvec && v * 4u + e < V32)) f[e] = kNegInf;
+          bool reach;
+          if constexpr (LSE) {
+            reach = vmx[b] >= thf;
+          } else {
+            unpack<TI>(xv, f);
+            reach = max3_raw(max3_raw(f[0], f[1], f[2]), f[3], f[3]) >= thf;
           }
-          if (max3_raw(max3_raw(f[0], f[1], f[2]), f[3], f[3]) >= thf) {
+          if (reach) {
+            if constexpr (LSE) unpack<TI>(xv, f);
             const uint32_t v = t0 + 64u * b + lane;
             // each element is written to the lane's next free slot, which
             // only a kept element then claims (a lane that reaches the last
