@@ -420,8 +420,9 @@ constexpr int64_t kJitterMinRows = 4096;
 
 // One 1024-lane workgroup per token row, the whole row held in registers
 // between the sweeps (NSLOT 16-byte vectors per lane): HBM sees one read of
-// the logits and one write of the gradient.  Requires whole vectors
-// (V a multiple of the elements per vector).
+// the logits and one write of the gradient.  TAIL: V is not a multiple of
+// the elements per vector, so the row's last vector is masked past V after
+// its load and stored element by element.
 template <class TI, class TO, int EST, int NSLOT, bool TAIL>
 __global__ void __launch_bounds__(kRowThreads) k_row_resident(Args a) {
   constexpr int NT = kRowThreads, NW = NT / 64, EPV = TI::EPV;
