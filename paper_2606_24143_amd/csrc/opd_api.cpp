@@ -386,13 +386,12 @@ int loss_call(const void* logits, int32_t dtype, int64_t N, int64_t V, int64_t l
   // and the student's support coverage (both need L).
   const bool read_row = !est_topk(estimator) || lse_out != nullptr || coverage_out != nullptr;
   Path path = Path::RowStream;
-  // register-resident rows (the dense kernel needs whole vectors)
-  if (tail == epv || !est_dense(estimator)) {
-    if (nvec <= (int64_t)opd::slots_small(dtype) * opd::kRowThreads)
-      path = Path::RowResidentSmall;
-    else if (nvec <= (int64_t)opd::slots_large(dtype) * opd::kRowThreads)
-      path = Path::RowResidentLarge;
-  }
+  // register-resident rows (a partial last vector takes the kernels' TAIL
+  // variant)
+  if (nvec <= (int64_t)opd::slots_small(dtype) * opd::kRowThreads)
+    path = Path::RowResidentSmall;
+  else if (nvec <= (int64_t)opd::slots_large(dtype) * opd::kRowThreads)
+    path = Path::RowResidentLarge;
   // rows per launch: the split grid has P workgroups of kSplitThreads lanes
   // per row, the others at most kRowThreads lanes per row (the top-k zero
   // fill chunks its own grid)

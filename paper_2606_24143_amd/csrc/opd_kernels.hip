@@ -619,7 +619,7 @@ constexpr int kYLdsBytes = 144 * 1024;
 // spill in any variant; sixteen spill in the fp32 build.
 constexpr int kYRegVgprs = 12;
 
-template <class TI, class TO, int EST, int NSLOT>
+template <class TI, class TO, int EST, int NSLOT, bool TAIL>
 __global__ void __launch_bounds__(kRowThreads) k_row_dense_resident(Args a) {
   constexpr int NT = kRowThreads, NW = NT / 64, EPV = TI::EPV;
   typedef typename TI::Vec Vec;
@@ -701,6 +701,11 @@ __global__ void __launch_bounds__(kRowThreads) k_row_dense_resident(Args a) {
         x[s] = neg_inf_vec<TI>();
         yv = neg_inf_vec<TI>();
       }
+      if constexpr (TAIL)
+        if ((uint32_t)(s * NT + tid1) == nvec1 - 1) {  // the row's last vector, past V
+          mask_tail<TI>(x[s], a.tail);
+          mask_tail<TI>(yv, a.tail);
+        }
       float fz[EPV], fy[EPV], az[EPV], ay[EPV];
       unpack<TI>(x[s], fz);
       unpack<TI>(yv, fy);
@@ -798,7 +803,10 @@ __global__ void __launch_bounds__(kRowThreads) k_row_dense_resident(Args a) {
       after(x[s], yv);
       float g[EPV];
       dense_grad<TI, EST, NEG>(x[s], yv, k, g);
-      buf_store<TO>(g_slot(s), vg2, g);
+      if (TAIL && (uint32_t)(s * NT + tid2) == nvec - 1)  // its first tail elements only
+        store_vec<TI, TO>(grow, nvec - 1, g, a.tail);
+      else
+        buf_store<TO>(g_slot(s), vg2, g);
       __builtin_amdgcn_sched_barrier(0);
     }
   };
@@ -1128,12 +1136,27 @@ template <class TI, class TO, int EST>
 hipError_t row_t(const Args& a, Path path, bool read, hipStream_t s) {
   const dim3 grid((unsigned)a.N), block(kRowThreads);
   if constexpr (is_dense(EST)) {
-    if (path == Path::RowResidentSmall) {
+    if (a.tail != TI::EPV && path != Path::RowStream) {
+      // a partial last vector (see k_row_resident's TAIL); the fp32 variant
+      // would spill, so fp32 rows of that kind stream
+      // (the large variant assumes its first slots_small slots whole, so
+      // the path's own size class is kept)
+      if constexpr (TI::BYTES == 2) {
+        if (path == Path::RowResidentSmall)
+          hipLaunchKernelGGL((k_row_dense_resident<TI, TO, EST, slots_small(BF16), true>), grid,
+                             block, 0, s, a);
+        else
+          hipLaunchKernelGGL((k_row_dense_resident<TI, TO, EST, slots_large(BF16), true>), grid,
+                             block, 0, s, a);
+      } else {
+        hipLaunchKernelGGL((k_row_stream<TI, TO, EST>), grid, block, 0, s, a);
+      }
+    } else if (path == Path::RowResidentSmall) {
       constexpr int NS = slots_small(TI::BYTES == 2 ? BF16 : F32);
-      hipLaunchKernelGGL((k_row_dense_resident<TI, TO, EST, NS>), grid, block, 0, s, a);
+      hipLaunchKernelGGL((k_row_dense_resident<TI, TO, EST, NS, false>), grid, block, 0, s, a);
     } else if (path == Path::RowResidentLarge) {
       constexpr int NS = slots_large(TI::BYTES == 2 ? BF16 : F32);
-      hipLaunchKernelGGL((k_row_dense_resident<TI, TO, EST, NS>), grid, block, 0, s, a);
+      hipLaunchKernelGGL((k_row_dense_resident<TI, TO, EST, NS, false>), grid, block, 0, s, a);
     } else {
       hipLaunchKernelGGL((k_row_stream<TI, TO, EST>), grid, block, 0, s, a);
     }

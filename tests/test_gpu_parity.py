@@ -413,6 +413,36 @@ def test_dense_rows_with_late_and_far_maxima(dtype, V, est):
                 teacher=ys)
 
 
+@pytest.mark.parametrize("est", DENSE)
+def test_dense_rows_with_a_partial_last_vector(est):
+    """bf16 rows of full width whose V is not a multiple of 4 (the dense
+    kernel's TAIL variant): the last vector's missing elements, here NaN in
+    the padding, must be neither read into the sums nor written."""
+    V, ld, N = 151933, 151936, 5
+    z, y = _wide_range_rows(V, V + 3, est)
+    zs, ys = _store(z, synth.BF16), _store(y, synth.BF16)
+
+    def padded(a):
+        p = np.full((N, ld), 0x7FC0, np.uint16)  # bf16 NaN in the padding
+        p[:, :V] = a
+        return p
+
+    say("dense partial last vector %s" % est)
+    ref = oracle.rows(est, oracle_dtype(synth.BF16), zs, V, teacher_logits=ys, gamma=0.5)
+    w = synth.Workload("t_dtail", N=N, V=V, dtype=synth.BF16, estimators=(est,),
+                       dense_teacher=True)
+    for path, flags in PATHS.items():
+        sentinel = -12345.0
+        out = {"loss": torch.empty(N, device=DEV),
+               "dlogits": torch.full((N, ld), sentinel, device=DEV)}
+        res = run_gpu(to_dev(padded(zs))[:, :V], est, None, None, None,
+                      to_dev(padded(ys))[:, :V], flags=flags, grad_scale=0.5, want_lse=True,
+                      out=out)
+        compare("dtail/%s/%s" % (est, path), w, {}, est, res, ref, gamma=0.5, logits=zs,
+                teacher=ys)
+        assert bool((out["dlogits"][:, V:] == sentinel).all()), "padding columns written"
+
+
 def test_nan_logits_propagate_to_their_row_only():
     w, d, _ = small_inputs("v1000", synth.F32)
     logits = d["logits"].copy()
