@@ -303,6 +303,52 @@ def test_padding_columns_and_skip_masked_rows_untouched():
                    mag[torch.from_numpy(keep).to(DEV)])
 
 
+@pytest.mark.parametrize("dtype,V,ld,est,out_dt", [
+    (synth.BF16, 5001, 5008, "rkl_mc", torch.float32),      # resident row, partial last vector
+    (synth.BF16, 4096, 4104, "fkl_dense", torch.bfloat16),  # dense resident row, bf16 gradient
+    (synth.F32, 80001, 80004, "rkl_mc", torch.float32),     # fp32 row wider than the registers
+], ids=["mc-bf16-tail", "dense-bf16-out", "mc-f32-stream"])
+def test_masked_rows_of_large_calls(dtype, V, ld, est, out_dt):
+    """A mask on a call of over 4,096 rows (where the row kernels stagger
+    their rows): every masked row exactly zero over its V columns, no padding
+    column written, and the rows on either side of each masked run, and a
+    random sample of the others, as the oracle's."""
+    N = 4100
+    w = synth.Workload("t_fillmask", N=N, V=V, dtype=dtype, estimators=(est,), M=4,
+                       sigma_student=2.5, sigma_teacher=1.0, sigma_behaviour=0.5,
+                       dense_teacher=est in DENSE, seed=V + N)
+    d = synth.generate(w, ld=ld)
+    rng = np.random.default_rng(V)
+    mask = (rng.random(N) > 0.1).astype(np.uint8)
+    for r0, r1 in [(0, 300), (1000, 1001), (2047, 2600), (N - 1, N)]:
+        mask[r0:r1] = 0
+    say("masked rows of a large call: %s V=%d %s" % ("bf16" if dtype else "f32", V, est))
+    sentinel = -3.0
+    buf = torch.full((N, ld), sentinel, dtype=out_dt, device=DEV)
+    loss = torch.full((N,), sentinel, dtype=torch.float32, device=DEV)
+    ids, tau, beta = cache_arrays(d, est)
+    teacher = to_dev(d["teacher_logits"])[:, :V] if est in DENSE else None
+    run_gpu(to_dev(d["logits"])[:, :V], est, ids, tau, beta, teacher, mask=mask,
+            dlogits_dtype=out_dt, out={"loss": loss, "dlogits": buf})
+    masked = torch.from_numpy(mask == 0).to(DEV)
+    assert bool((buf[:, V:] == sentinel).all()), "padding columns written"
+    assert bool((buf[masked, :V] == 0).all()), "masked rows not zero"
+    assert bool((loss[masked] == 0).all()), "masked rows' loss not zero"
+    sel = np.r_[0:4, 296:306, 996:1006, 2040:2052, 2596:2606, N - 12:N,
+                rng.choice(N, 40, replace=False)]
+    sub = lambda a: None if a is None else np.ascontiguousarray(a[sel])  # noqa: E731
+    ref = oracle.rows(est, oracle_dtype(dtype), d["logits"][sel], V, ids=sub(ids), tau=sub(tau),
+                      beta=sub(beta), mask=mask[sel],
+                      teacher_logits=sub(d["teacher_logits"]) if est in DENSE else None)
+    check_loss("fillmask", loss.cpu().numpy()[sel], ref["loss"],
+               loss_scale(est, sub(ids), sub(tau), sub(beta), ref), rtol_for(dtype), mask[sel])
+    mag = grad_mag(est, widen_dev(d["logits"][sel], V), ref, sub(ids), sub(tau), sub(beta),
+                   widen_dev(d["teacher_logits"][sel], V) if est in DENSE else None,
+                   mask=mask[sel])
+    check_grad("fillmask", buf[torch.from_numpy(sel).to(DEV), :V], ref["grad"], mag,
+               bf16_out=out_dt == torch.bfloat16)
+
+
 def test_topk_full_support_matches_dense_on_gpu():
     """k = V: renormalised top-k equals the dense KL (App. A.1 with S = V)."""
     N, V = 6, 256
