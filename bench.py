@@ -158,12 +158,18 @@ def cpu_diag_baseline(w, d, lse, gathered, seq):
                       "%.2f s wall on 1 thread" % (w.N, el)}
 
 
+FUSED_TOPK_MAX_BYTES = 128 << 20  # fp32 gradient bytes below which top-k takes one launch
+
+
 def dominant_kernels(op: str, est: str, w, split: bool):
     """Names of the kernels a launch runs (as rocprofv3 lists them)."""
     if op == "loss":
         if split:
             return ["k_split_stats", "k_split_write"]
         if est in ("fkl_topk", "rkl_topk"):
+            # (the library writes gradients of at most 128 MiB in one launch)
+            if w.N * ((w.V + 3) // 4) * 16 <= FUSED_TOPK_MAX_BYTES:
+                return ["k_topk_fused"]
             return ["k_fill_zero", "k_topk_sparse"]
         if est in ("fkl_dense", "rkl_dense"):
             return ["k_row_dense_resident"]

@@ -1051,6 +1051,80 @@ __global__ void __launch_bounds__(kFillThreads) k_fill_zero(Args a, int64_t row0
   }
 }
 
+// Wave 0: the support entries of a row over its zeros.  Ids are distinct by
+// precondition; should one repeat, its first occurrence writes the sum over
+// its occurrences in cache order, so the result stays deterministic.
+template <class TO>
+__device__ __forceinline__ void write_support(void* grow, int K, const CacheLds& c) {
+  const int lane = threadIdx.x & 63;
+  for (int i = lane; i < K; i += 64) {
+    const int id = c.id[i];
+    bool first = true;
+    for (int j = 0; j < i; ++j) first = first && c.id[j] != id;
+    if (!first) continue;
+    float g = 0.f;
+    for (int j = i; j < K; ++j)
+      if (c.id[j] == id) g += c.w[j];
+    if constexpr (TO::BYTES == 4)
+      ((float*)grow)[id] = g;
+    else
+      ((uint16_t*)grow)[id] = __builtin_bit_cast(uint16_t, (__bf16)g);
+  }
+}
+
+// One value in every element of a gradient row of nvec vectors (the last
+// holding tail elements), lanes striding by NT.
+template <class TO, int NT>
+__device__ __forceinline__ void fill_row(void* grow, int64_t nvec, int tail, float x) {
+  const float g[4] = {x, x, x, x};
+  for (int64_t v = threadIdx.x; v < nvec; v += NT) {
+    if (v == nvec - 1 && tail != 4) {
+      store_vec<InF32, TO>(grow, v, g, tail);
+    } else if constexpr (TO::BYTES == 4) {
+      __builtin_nontemporal_store(f32x4{x, x, x, x}, (f32x4*)grow + v);
+    } else {
+      const uint32_t h = pack_bf16x2(x, x);
+      __builtin_nontemporal_store(u32x2{h, h}, (u32x2*)grow + v);
+    }
+  }
+}
+
+// The write-only top-k form in one launch, for calls whose gradient is
+// small enough that a second launch costs more than the one-shot fill gains
+// over a row per workgroup: the workgroup writes its row's zeros, wave 0
+// meanwhile evaluates the estimator, and after a barrier (which waits for
+// every store of the workgroup) wave 0 writes the support entries over the
+// zeros, or every lane NaN over the row if its cache was bad.
+template <class TI, class TO, int EST>
+__global__ void __launch_bounds__(kFillThreads) k_topk_fused(Args a) {
+  __shared__ CacheLds c;
+  const int tid = threadIdx.x;
+  const int64_t row = blockIdx.x;
+  const void* zrow = (const char*)a.logits + row * a.ld * TI::BYTES;
+  void* grow = (char*)a.dlogits + row * a.ld * TO::BYTES;
+  const int K = a.K;
+  const bool masked = a.mask && a.mask[row] == 0;
+  if (!(masked && a.skip_masked)) fill_row<TO, kFillThreads>(grow, a.nvec, a.tail, 0.f);
+  if (masked) {  // (workgroup-uniform, before any barrier)
+    if (tid == 0) a.loss[row] = 0.f;
+    if (a.gathered_out)
+      for (int i = tid; i < K; i += kFillThreads) a.gathered_out[row * K + i] = 0.f;
+    return;
+  }
+  if (tid < 64) {
+    load_cache<TI>(a, row, zrow, c);
+    const float loss = estimate<EST>(K, 0.f, a.gamma, 0, 0.f, c);
+    if (tid == 0) a.loss[row] = c.bad ? __builtin_nanf("") : loss;
+    if (a.gathered_out)
+      for (int i = tid; i < K; i += 64) a.gathered_out[row * K + i] = c.z[i];
+  }
+  __syncthreads();
+  if (c.bad)
+    fill_row<TO, kFillThreads>(grow, a.nvec, a.tail, __builtin_nanf(""));
+  else if (tid < 64)
+    write_support<TO>(grow, K, c);
+}
+
 template <class TI, class TO, int EST>
 __global__ void __launch_bounds__(64 * kSparseRowsPerBlock) k_topk_sparse(Args a) {
   __shared__ CacheLds cs[kSparseRowsPerBlock];
@@ -1081,22 +1155,7 @@ __global__ void __launch_bounds__(64 * kSparseRowsPerBlock) k_topk_sparse(Args a
       store_vec<InF32, TO>(grow, v, g, v == a.nvec - 1 ? a.tail : 4);
     return;
   }
-  // Support entries.  Ids are distinct by precondition; should one repeat,
-  // its first occurrence writes the sum over its occurrences in cache order,
-  // so the result stays deterministic.
-  for (int i = lane; i < K; i += 64) {
-    const int id = c.id[i];
-    bool first = true;
-    for (int j = 0; j < i; ++j) first = first && c.id[j] != id;
-    if (!first) continue;
-    float g = 0.f;
-    for (int j = i; j < K; ++j)
-      if (c.id[j] == id) g += c.w[j];
-    if constexpr (TO::BYTES == 4)
-      ((float*)grow)[id] = g;
-    else
-      ((uint16_t*)grow)[id] = __builtin_bit_cast(uint16_t, (__bf16)g);
-  }
+  write_support<TO>(grow, K, c);
 }
 
 // ---------------------------------------------------------------- cache validation
@@ -1212,9 +1271,23 @@ hipError_t by_types(int est, int in_dt, int out_dt, F&& f) {
   return out_dt == BF16 ? by_est<InF32, OutBf16>(est, f) : by_est<InF32, OutF32>(est, f);
 }
 
+// Calls whose gradient rows total at most this many bytes take k_topk_fused.
+// Measured with fp32 gradients: one launch 0.019 ms against 0.022 ms for the
+// two at 65.5 MB (512 x 32,000), the same time at 155 and 262 MB, and 0.124
+// against 0.109 ms at 622 MB (1,024 x 151,936).
+#ifndef OPD_FUSED_TOPK_MAX_BYTES
+#define OPD_FUSED_TOPK_MAX_BYTES (128ll << 20)
+#endif
+constexpr int64_t kFusedTopkMaxBytes = OPD_FUSED_TOPK_MAX_BYTES;
+
 template <class TI, class TO, int EST>
 hipError_t topk_sparse_t(const Args& a, hipStream_t s) {
   if constexpr (is_topk(EST)) {
+    if (a.N * a.nvec * 4 * TO::BYTES <= kFusedTopkMaxBytes) {
+      hipLaunchKernelGGL((k_topk_fused<TI, TO, EST>), dim3((unsigned)a.N), dim3(kFillThreads), 0,
+                         s, a);
+      return hipGetLastError();
+    }
     const int64_t bpr = (a.nvec + kFillThreads - 1) / kFillThreads;
     // row chunks keep every grid under 2^32 work-items
     const int64_t rows_per_launch = (int64_t)0xFFFFFFFFll / (bpr * kFillThreads);

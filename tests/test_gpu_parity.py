@@ -278,6 +278,52 @@ def test_topk_gradient_zero_pattern_is_exact():
             assert np.count_nonzero(g[support]) > 0.9 * support.sum()
 
 
+@pytest.mark.parametrize("N,V,ld", [(40, 32000, 32008), (600, 131071, 131072)],
+                         ids=["one-launch", "fill-then-sparse"])
+@pytest.mark.parametrize("est", ["fkl_topk", "rkl_topk"])
+def test_write_only_topk_forms(N, V, ld, est):
+    """The renormalised top-k estimators without lse_out write only the
+    gradient's zeros and the support entries: in one launch for small calls,
+    as a zero fill and a sparse writer for large ones (over 128 MiB of
+    gradient).  Both with masked rows, with and without SKIP_MASKED, rows
+    with an out-of-range id (NaN over their V columns), padding columns and
+    (for the large call) a partial last vector; a sample of the other rows
+    against the oracle."""
+    w = synth.Workload("t_wo", N=N, V=V, dtype=synth.BF16, estimators=(est,), k=16,
+                       sigma_student=2.5, sigma_teacher=1.0, seed=N + V)
+    d = synth.generate(w, ld=ld)
+    ids, tau = d["topk_idx"].copy(), d["topk_tau"].copy()
+    bad = [3, N - 2]
+    ids[3, 5], ids[N - 2, 0] = V, -1
+    mask = np.ones(N, np.uint8)
+    mask[[0, 7, N - 1]] = 0
+    good = np.array([r for r in range(N) if mask[r] and r not in bad])
+    sel = good[::max(1, len(good) // 24)]
+    ref = oracle.rows(est, oracle_dtype(synth.BF16), d["logits"][sel], V,
+                      ids=np.ascontiguousarray(ids[sel]), tau=np.ascontiguousarray(tau[sel]),
+                      mask=mask[sel])
+    mag = grad_mag(est, widen_dev(d["logits"][sel], V), ref, ids[sel], tau[sel], None,
+                   mask=mask[sel])
+    for skip in (False, True):
+        say("write-only top-k %s N=%d V=%d skip=%d" % (est, N, V, skip))
+        sentinel = 5.0
+        buf = torch.full((N, ld), sentinel, dtype=torch.float32, device=DEV)
+        loss = torch.full((N,), sentinel, dtype=torch.float32, device=DEV)
+        run_gpu(to_dev(d["logits"])[:, :V], est, ids, tau, None, mask=mask,
+                flags=opd.FLAG_SKIP_MASKED if skip else 0, out={"loss": loss, "dlogits": buf})
+        b, lo = buf.cpu().numpy(), loss.cpu().numpy()
+        m = mask == 0
+        assert np.all(b[:, V:] == sentinel), "padding columns written"
+        assert np.all(b[m, :V] == (sentinel if skip else 0.0)), "masked rows"
+        assert np.all(lo[m] == 0.0)
+        assert np.isnan(b[bad, :V]).all() and np.isnan(lo[bad]).all(), "bad rows not NaN"
+        check_loss("wo/%s" % est, lo[sel], ref["loss"],
+                   loss_scale(est, ids[sel], tau[sel], None, ref), rtol_for(synth.BF16),
+                   mask[sel])
+        check_grad("wo/%s" % est, torch.from_numpy(b[sel, :V].astype(np.float64)), ref["grad"],
+                   mag)
+
+
 def test_padding_columns_and_skip_masked_rows_untouched():
     N, V, ld = 11, 1001, 1008
     w = synth.Workload("t_pad", N=N, V=V, dtype=synth.BF16, estimators=("rkl_mc",), M=4, seed=9)
