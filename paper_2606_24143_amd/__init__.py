@@ -6,12 +6,12 @@ provides device memory and streams only.
 """
 from ._binding import (DENSE, DIAG_OUTPUTS, ESTIMATORS, EXPORTS, FLAG_FORCE_ROWWISE,
                        FLAG_FORCE_SPLITV, FLAG_SKIP_MASKED, K_MAX, LIB_PATH, TOPK, OpdCache,
-                       OpdError, OpdMcDiag, OpdOpts, lib, loss_fwd_bwd, mc_diagnostics,
-                       sample_actions, score_actions, status_string, topk_support, validate_cache,
-                       version, workspace_bytes)
+                       OpdError, OpdMcDiag, OpdOpts, PreparedCall, lib, loss_fwd_bwd,
+                       mc_diagnostics, prepare_loss_fwd_bwd, sample_actions, score_actions,
+                       status_string, topk_support, validate_cache, version, workspace_bytes)
 
 __all__ = ["DENSE", "DIAG_OUTPUTS", "ESTIMATORS", "EXPORTS", "FLAG_FORCE_ROWWISE",
            "FLAG_FORCE_SPLITV", "FLAG_SKIP_MASKED", "K_MAX", "LIB_PATH", "TOPK", "OpdCache",
-           "OpdError", "OpdMcDiag", "OpdOpts", "lib", "loss_fwd_bwd", "mc_diagnostics",
-           "sample_actions", "score_actions", "status_string", "topk_support", "validate_cache",
-           "version", "workspace_bytes"]
+           "OpdError", "OpdMcDiag", "OpdOpts", "PreparedCall", "lib", "loss_fwd_bwd",
+           "mc_diagnostics", "prepare_loss_fwd_bwd", "sample_actions", "score_actions",
+           "status_string", "topk_support", "validate_cache", "version", "workspace_bytes"]

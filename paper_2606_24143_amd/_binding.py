@@ -188,19 +188,54 @@ def workspace_bytes(N: int, V: int, dtype: int, estimator: str, k: int = 0, M: i
     return int(lib().opd_workspace_bytes(N, V, dtype, ESTIMATORS[estimator], k, M, flags))
 
 
-def loss_fwd_bwd(logits: torch.Tensor, estimator: str, *, idx=None, sampled_ids=None,
-                 teacher_logp=None, behav_logp=None, teacher_logits=None, mask=None,
-                 grad_scale: float = 1.0, dlogits_dtype=torch.float32, flags: int = 0,
-                 clip_eps: float = 0.2, want_lse: bool = False, want_gathered: bool = False,
-                 want_coverage: bool = False, workspace=None, out=None, stream=None,
-                 no_alloc: bool = False):
+class PreparedCall:
+    """A library call whose arguments were checked and marshalled once.
+
+    Calling it issues the same C call again: the same tensors, options and
+    stream (the one given, or the current one, at preparation).  It checks
+    nothing and allocates nothing, so a loop that repeats one call on the
+    same buffers pays only for the foreign call.  `outputs` holds the result
+    tensors the call writes; the prepared object keeps every tensor it was
+    prepared with alive.
+    """
+    __slots__ = ("_fn", "_args", "_name", "_keep", "outputs")
+
+    def __init__(self, fn, args, name, keep, outputs):
+        self._fn, self._args, self._name, self._keep = fn, args, name, keep
+        self.outputs = outputs
+
+    def __call__(self):
+        rc = self._fn(*self._args)
+        if rc != 0:
+            raise OpdError(rc, self._name)
+        return self.outputs
+
+
+def loss_fwd_bwd(logits: torch.Tensor, estimator: str, **kw):
     """One fused forward+backward call of opd_loss_fwd_bwd.
 
     logits: [N, V] device tensor (a row-strided view of an [N, ld] buffer is
     fine).  Cache tensors are [N, k] / [N, M] device tensors.  Returns a dict
     with "loss" [N], "dlogits" [N, V] (a view of the [N, ld] buffer), and
     "lse" / "gathered" / "coverage" ([N, 2]: Z_p^S, Z_q^S; estimators with a
-    cached support only) when requested.  `workspace=None` allocates what the
+    cached support only) when requested.  The keyword arguments are those of
+    prepare_loss_fwd_bwd.
+    """
+    return prepare_loss_fwd_bwd(logits, estimator, **kw)()
+
+
+def prepare_loss_fwd_bwd(logits: torch.Tensor, estimator: str, *, idx=None, sampled_ids=None,
+                         teacher_logp=None, behav_logp=None, teacher_logits=None, mask=None,
+                         grad_scale: float = 1.0, dlogits_dtype=torch.float32, flags: int = 0,
+                         clip_eps: float = 0.2, want_lse: bool = False,
+                         want_gathered: bool = False, want_coverage: bool = False,
+                         workspace=None, out=None, stream=None,
+                         no_alloc: bool = False) -> PreparedCall:
+    """The checks, output allocation and marshalling of one opd_loss_fwd_bwd
+    call, returned as a PreparedCall (nothing is launched until it is
+    called; its `outputs` are loss_fwd_bwd's result dict).
+
+    The arguments are loss_fwd_bwd's.  `workspace=None` allocates what the
     split path needs; pass a tensor to supply your own (or an empty one to
     force the row-per-workgroup path).  `out` may hold preallocated "loss"
     and "dlogits" ([N, ld]) tensors.  `no_alloc=True` calls
@@ -262,26 +297,24 @@ def loss_fwd_bwd(logits: torch.Tensor, estimator: str, *, idx=None, sampled_ids=
     if want_coverage and estimator not in TOPK:
         raise ValueError("support coverage exists for the estimators with a cached support only")
     coverage = torch.empty((N, 2), dtype=torch.float32, device=dev) if want_coverage else None
+    keep = (logits, idx, sampled_ids, teacher_logp, behav_logp, teacher_logits, mask, loss, dbuf,
+            lse, gathered, coverage, cache, opts)
     if no_alloc:
-        rc = lib().opd_loss_fwd_bwd_noalloc(_ptr(logits), dt, N, V, ld, ctypes.byref(cache), est,
-                                            k, M, _ptr(mask), ctypes.byref(opts), _ptr(loss),
-                                            _ptr(dbuf), _ptr(lse), _ptr(gathered),
-                                            _ptr(coverage), _stream(stream))
-        if rc != 0:
-            raise OpdError(rc, "opd_loss_fwd_bwd_noalloc")
+        fn, name = lib().opd_loss_fwd_bwd_noalloc, "opd_loss_fwd_bwd_noalloc"
+        args = (_ptr(logits), dt, N, V, ld, ctypes.byref(cache), est, k, M, _ptr(mask),
+                ctypes.byref(opts), _ptr(loss), _ptr(dbuf), _ptr(lse), _ptr(gathered),
+                _ptr(coverage), _stream(stream))
     else:
         if workspace is None:
             nbytes = workspace_bytes(N, V, dt, estimator, k, M, flags)
             workspace = (torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
                          if nbytes else None)
         ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
-        rc = lib().opd_loss_fwd_bwd(_ptr(logits), dt, N, V, ld, ctypes.byref(cache), est, k, M,
-                                    _ptr(mask), ctypes.byref(opts), _ptr(loss), _ptr(dbuf),
-                                    _ptr(lse), _ptr(gathered), _ptr(coverage),
-                                    _ptr(workspace) if ws_bytes else None, ws_bytes,
-                                    _stream(stream))
-        if rc != 0:
-            raise OpdError(rc, "opd_loss_fwd_bwd")
+        fn, name = lib().opd_loss_fwd_bwd, "opd_loss_fwd_bwd"
+        args = (_ptr(logits), dt, N, V, ld, ctypes.byref(cache), est, k, M, _ptr(mask),
+                ctypes.byref(opts), _ptr(loss), _ptr(dbuf), _ptr(lse), _ptr(gathered),
+                _ptr(coverage), _ptr(workspace) if ws_bytes else None, ws_bytes, _stream(stream))
+        keep = keep + (workspace,)
     res = {"loss": loss, "dlogits": dbuf[:, :V]}
     if lse is not None:
         res["lse"] = lse
@@ -289,7 +322,7 @@ def loss_fwd_bwd(logits: torch.Tensor, estimator: str, *, idx=None, sampled_ids=
         res["gathered"] = gathered[:, :K]
     if coverage is not None:
         res["coverage"] = coverage
-    return res
+    return PreparedCall(fn, args, name, keep, res)
 
 
 def validate_cache(estimator: str, V: int, *, idx=None, sampled_ids=None, teacher_logp=None,

@@ -535,6 +535,49 @@ def test_dense_rows_with_a_partial_last_vector(est):
         assert bool((out["dlogits"][:, V:] == sentinel).all()), "padding columns written"
 
 
+@pytest.mark.parametrize("est", ["rkl_mc", "fkl_topk", "rkl_dense"])
+def test_prepared_call_repeats_the_call(est):
+    """A prepared call re-issues the same C call on the same tensors: after
+    new data is copied into the inputs it gives what a fresh call on that
+    data gives, bit for bit, and it allocates no device memory."""
+    w1, d1, mask = small_inputs("v32000", synth.BF16)
+    w2 = synth.Workload("t_prep", N=w1.N, V=w1.V, dtype=synth.BF16, estimators=(est,),
+                        k=w1.k, M=w1.M, dense_teacher=True, seed=77)
+    d2 = synth.generate(w2)
+    N, V = w1.N, w1.V
+    say("prepared call %s" % est)
+
+    def inputs(d):
+        ids, tau, beta = cache_arrays(d, est)
+        kw = {}
+        if est in SUPPORT:
+            kw = dict(idx=to_dev(ids), teacher_logp=to_dev(tau))
+        elif est in MC:
+            kw = dict(sampled_ids=to_dev(ids), teacher_logp=to_dev(tau), behav_logp=to_dev(beta))
+        else:
+            kw = dict(teacher_logits=to_dev(d["teacher_logits"]))
+        return to_dev(d["logits"]), kw
+
+    logits, kw = inputs(d1)
+    m = to_dev(mask)
+    out = {"loss": torch.empty(N, device=DEV), "dlogits": torch.empty(N, V, device=DEV)}
+    call = opd.prepare_loss_fwd_bwd(logits, est, mask=m, out=out, want_lse=True, **kw)
+    for d in (d1, d2, d1):
+        new_logits, new_kw = inputs(d)
+        logits.copy_(new_logits)
+        for key, t in kw.items():
+            t.copy_(new_kw[key])
+        torch.cuda.synchronize()
+        before = torch.cuda.memory_allocated()
+        res = call()
+        torch.cuda.synchronize()
+        assert torch.cuda.memory_allocated() == before, "a prepared call allocated"
+        ref = opd.loss_fwd_bwd(new_logits, est, mask=m, want_lse=True, **new_kw)
+        torch.cuda.synchronize()
+        for key in ("loss", "dlogits", "lse"):
+            assert torch.equal(res[key], ref[key]), key
+
+
 def test_nan_logits_propagate_to_their_row_only():
     w, d, _ = small_inputs("v1000", synth.F32)
     logits = d["logits"].copy()
