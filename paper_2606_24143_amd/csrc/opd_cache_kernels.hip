@@ -949,7 +949,7 @@ __global__ void __launch_bounds__(NT) k_topk_redo(CacheArgs a) {
 // ---------------------------------------------------------------- top-k, streamed
 
 // The top-k support of rows of at least 16,384 entries, for k <= 64, reads
-// each row once: 256-lane workgroups with about 38 KiB of LDS, four per CU.
+// each row once: 256-lane workgroups with about 34 KiB of LDS, four per CU.
 // Each lane keeps the running maximum of the values it has seen.  After each
 // tile of 8 coalesced loads per lane, and before any of the tile's elements
 // is kept, the wave recomputes the ceil(k / 4)-th largest of its 64 running
@@ -976,8 +976,7 @@ constexpr int64_t kTkMinVec = 4096;
 
 struct TkLds {
   uint64_t buf[kTkSlots][kTkThreads];  // lane-private candidates: (value bits, ~index)
-  uint64_t sbuf[2][kTkThreads];
-  uint64_t sel[kTkThreads];
+  uint64_t sel[kTkThreads];            // survivors: (order key, ~index)
   uint32_t theta[kTkWaves];            // published wave bounds (order keys)
   uint32_t nsel;
   uint32_t over;
@@ -1121,32 +1120,48 @@ __global__ void __launch_bounds__(kTkThreads) k_topk_stream(CacheArgs a) {
     // for numbers, f >= thf exactly when order_key(f) >= theta (a bf16
     // bound's zero low key bits sit below every widened value's)
     if (__ballot(tmx >= thf) != 0) {  // wave-uniform
+      // the lane's vectors whose maximum reaches the bound, one bit each
+      uint32_t rm = 0u;
       if (tmx >= thf) {
 #pragma unroll
         for (int b = 0; b < B; ++b) {
-          Vec xv = x[b];
-          keep_packed(xv);  // unpacked again here rather than held since pass A
-          float f[4];
           bool reach;
           if constexpr (LSE) {
             reach = vmx[b] >= thf;
           } else {
+            Vec xv = x[b];
+            keep_packed(xv);  // unpacked again here rather than held since pass A
+            float f[4];
             unpack<TI>(xv, f);
             reach = max3_raw(max3_raw(f[0], f[1], f[2]), f[3], f[3]) >= thf;
           }
-          if (reach) {
-            if constexpr (LSE) unpack<TI>(xv, f);
-            const uint32_t v = t0 + 64u * b + lane;
-            // each element is written to the lane's next free slot, which
-            // only a kept element then claims (a lane that reaches the last
-            // slot overflows, and its row goes to the fallback)
+          rm |= reach ? 1u << b : 0u;
+        }
+      }
+      // One reaching vector per lane per round, in index order within the
+      // lane, for as many rounds as the busiest lane needs (usually one):
+      // a body per vector position instead would run whenever any lane's
+      // vector at that position reaches.
+      while (__ballot(rm != 0u) != 0) {  // wave-uniform
+        if (rm != 0u) {
+          const int b = __builtin_ctz(rm);
+          rm &= rm - 1u;
+          Vec xv = x[0];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const bool keep = f[e] >= thf && (FULL || (v < nvec && v * 4u + e < V32));
-              sh.buf[cnt & (kTkSlots - 1)][tid] =
-                  ((uint64_t)__float_as_uint(f[e]) << 32) | (0xFFFFFFFFu - (v * 4u + e));
-              cnt += keep ? 1u : 0u;
-            }
+          for (int j = 1; j < B; ++j) xv = b == j ? x[j] : xv;
+          keep_packed(xv);  // selected packed, then unpacked
+          float f[4];
+          unpack<TI>(xv, f);
+          const uint32_t v = t0 + 64u * (uint32_t)b + lane;
+          // each element is written to the lane's next free slot, which
+          // only a kept element then claims (a lane that reaches the last
+          // slot overflows, and its row goes to the fallback)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const bool keep = f[e] >= thf && (FULL || (v < nvec && v * 4u + e < V32));
+            sh.buf[cnt & (kTkSlots - 1)][tid] =
+                ((uint64_t)__float_as_uint(f[e]) << 32) | (0xFFFFFFFFu - (v * 4u + e));
+            cnt += keep ? 1u : 0u;
           }
         }
       }
@@ -1237,14 +1252,20 @@ __global__ void __launch_bounds__(kTkThreads) k_topk_stream(CacheArgs a) {
     if (tid == 0) a.ids_out[row * k] = kTopkRedo;
     return;
   }
-  int P = 2;
-  while (P < (int)nsel) P <<= 1;
-  const uint64_t mine =
-      block_sort_desc<uint64_t, T>(tid < (int)nsel ? sh.sel[tid] : 0ull, sh.sbuf, P);
-  if (tid < k) {
-    const uint32_t j = 0xFFFFFFFFu - (uint32_t)mine;
-    a.ids_out[row * k + tid] = (int32_t)j;
-    if (a.logp) a.logp[row * k + tid] = key_value((uint32_t)(mine >> 32)) - L;
+  // Each survivor's rank is the number of survivors above it (the entries
+  // are distinct); the k of rank below k are the top k, each written at its
+  // rank.  Every lane reads the same entry at a time (an LDS broadcast), and
+  // the reads do not depend on each other, unlike the exchanges of a sort.
+  if (tid < (int)nsel) {
+    const uint64_t mine = sh.sel[tid];
+    uint32_t rank = 0;
+#pragma unroll 8
+    for (uint32_t i = 0; i < nsel; ++i) rank += sh.sel[i] > mine ? 1u : 0u;
+    if (rank < (uint32_t)k) {
+      const uint32_t j = 0xFFFFFFFFu - (uint32_t)mine;
+      a.ids_out[row * k + rank] = (int32_t)j;
+      if (a.logp) a.logp[row * k + rank] = key_value((uint32_t)(mine >> 32)) - L;
+    }
   }
   if (tid == 0 && a.lse_out) a.lse_out[row] = L;
 }
