@@ -327,7 +327,7 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path (rows are independent; "
+        print("bench.py measures one GPU: the library has no multi-GPU path (rows are independent; "
               "each GPU would run the same kernel on its own share of rows). Use --gpus 1.",
               file=sys.stderr)
         sys.exit(2)
