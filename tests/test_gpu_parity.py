@@ -278,10 +278,11 @@ def test_topk_gradient_zero_pattern_is_exact():
             assert np.count_nonzero(g[support]) > 0.9 * support.sum()
 
 
+@pytest.mark.parametrize("out_dt", [torch.float32, torch.bfloat16], ids=["f32-grad", "bf16-grad"])
 @pytest.mark.parametrize("N,V,ld", [(40, 32000, 32008), (600, 131071, 131072)],
                          ids=["one-launch", "fill-then-sparse"])
 @pytest.mark.parametrize("est", ["fkl_topk", "rkl_topk"])
-def test_write_only_topk_forms(N, V, ld, est):
+def test_write_only_topk_forms(N, V, ld, est, out_dt):
     """The renormalised top-k estimators without lse_out write only the
     gradient's zeros and the support entries: in one launch for small calls,
     as a zero fill and a sparse writer for large ones (over 128 MiB of
@@ -307,11 +308,12 @@ def test_write_only_topk_forms(N, V, ld, est):
     for skip in (False, True):
         say("write-only top-k %s N=%d V=%d skip=%d" % (est, N, V, skip))
         sentinel = 5.0
-        buf = torch.full((N, ld), sentinel, dtype=torch.float32, device=DEV)
+        buf = torch.full((N, ld), sentinel, dtype=out_dt, device=DEV)
         loss = torch.full((N,), sentinel, dtype=torch.float32, device=DEV)
         run_gpu(to_dev(d["logits"])[:, :V], est, ids, tau, None, mask=mask,
-                flags=opd.FLAG_SKIP_MASKED if skip else 0, out={"loss": loss, "dlogits": buf})
-        b, lo = buf.cpu().numpy(), loss.cpu().numpy()
+                flags=opd.FLAG_SKIP_MASKED if skip else 0, dlogits_dtype=out_dt,
+                out={"loss": loss, "dlogits": buf})
+        b, lo = buf.float().cpu().numpy(), loss.cpu().numpy()
         m = mask == 0
         assert np.all(b[:, V:] == sentinel), "padding columns written"
         assert np.all(b[m, :V] == (sentinel if skip else 0.0)), "masked rows"
@@ -321,7 +323,7 @@ def test_write_only_topk_forms(N, V, ld, est):
                    loss_scale(est, ids[sel], tau[sel], None, ref), rtol_for(synth.BF16),
                    mask[sel])
         check_grad("wo/%s" % est, torch.from_numpy(b[sel, :V].astype(np.float64)), ref["grad"],
-                   mag)
+                   mag, bf16_out=out_dt == torch.bfloat16)
 
 
 def test_padding_columns_and_skip_masked_rows_untouched():
